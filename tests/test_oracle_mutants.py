@@ -1,0 +1,101 @@
+"""Plant mistakes in copies of the oracle and check that the pins catch each one.
+
+Each mutant is a textual change to a copy of oracle/darb_oracle.c, compiled on
+the CPU into a temporary library and driven through a fresh copy of the oracle's
+Python wrapper.  The real oracle must pass ``pin_suite``; every mutant must fail it.
+"""
+import importlib.util
+import os
+import shutil
+import sys
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+import oracle
+from tests._brute import block_size_brute, kept_positions
+
+ORACLE_DIR = os.path.dirname(oracle.__file__)
+
+MUTANTS = {
+    "tie_goes_to_last": [("if (key > best_key)", "if (key >= best_key)")],
+    "sign_not_cleared": [("& 0x7FFFFFFFu;\n            for", "& 0xFFFFFFFFu;\n            for"),
+                         ("uint32_t key = row[k * b + j] & 0x7FFFFFFFu",
+                          "uint32_t key = row[k * b + j] & 0xFFFFFFFFu")],
+    "tail_block_dropped": [("(N + b - 1) / b", "N / b")],
+    "rounding_direction_swapped": [("d >= matrix_density", "d < matrix_density")],
+    "round_down_off_by_one": [("(f * d == 1.0) ? f : 2.0 * f", "2.0 * f")],
+    "gather_index_wrong": [("int64_t c = k * b + offsets[s];", "int64_t c = k + offsets[s];")],
+    "product_sign_flipped": [("y[j] += v *", "y[j] -= v *")],
+    "bins_in_wrong_order": [("for (int l = 0; l <= 7; ++l)", "for (int l = 7; l >= 0; --l)")],
+    "half_exponent_bias": [("e - 25", "e - 24")],
+}
+
+
+def _load_variant(tmp_path, name, edits):
+    src = open(os.path.join(ORACLE_DIR, "darb_oracle.c")).read()
+    for old, new in edits:
+        assert old in src, (name, old)
+        src = src.replace(old, new)
+    d = tmp_path / name
+    d.mkdir()
+    (d / "darb_oracle.c").write_text(src)
+    shutil.copy(os.path.join(ORACLE_DIR, "__init__.py"), d / "__init__.py")
+    spec = importlib.util.spec_from_file_location(f"oracle_mutant_{name}", str(d / "__init__.py"))
+    mod = importlib.util.module_from_spec(spec)
+    sys.modules[spec.name] = mod          # dataclasses look their module up here
+    spec.loader.exec_module(mod)
+    return mod
+
+
+def pin_suite(orc):
+    """A compact run of the pins; raises AssertionError on the first miss."""
+    # section 3.2 worked example (paper mode) and the floor rule's closed form
+    for D, d, b in [(0.2188, 0.375, 2), (0.2188, 0.1875, 8), (0.2188, 0.25, 4)]:
+        assert (1 << int(orc.block_log2(np.array([d]), D, orc.ROUND_PAPER, 1, 128)[0])) == b
+    counts = np.arange(0, 257)
+    got = orc.block_log2(counts / 256.0, 0.3, orc.ROUND_PAPER, 1, 128)
+    for c in counts:
+        want = block_size_brute(int(c), 256, Fraction(0.3), "paper", 1, 128)
+        assert (1 << int(got[c])) == want
+    # Table 7: sum of ceil(1500/b), b = 2..64, is 1478
+    assert orc.layout(1500, np.arange(1, 7, dtype=np.uint8)).nnz == 1478
+    # rows grouped by block size, smallest first
+    assert list(orc.layout(100, np.array([3, 1, 3, 0], dtype=np.uint8)).perm) == [3, 1, 0, 2]
+    # BMWM against the brute-force predicate, with ties and negative values
+    rng = np.random.default_rng(0)
+    for dtype, ut in [(np.float32, np.uint32), (np.float16, np.uint16)]:
+        for _ in range(6):
+            M, N = int(rng.integers(2, 6)), int(rng.integers(5, 40))
+            W = (rng.integers(-3, 4, size=(M, N)) * 0.5).astype(dtype)
+            log2b = rng.integers(0, 5, size=M).astype(np.uint8)
+            lay = orc.layout(N, log2b)
+            v, o = orc.encode(W, lay)
+            kept = np.zeros((M, N), dtype=bool)
+            for r in range(M):
+                b = 1 << int(log2b[r])
+                s = int(lay.row_start[r])
+                cols = [k * b + int(o[s + k]) for k in range(-(-N // b))]
+                assert cols == kept_positions(W[r], b)
+                kept[r, cols] = True
+            Wm = orc.decode(v, o, lay)
+            assert np.array_equal(Wm.view(ut), np.where(kept, W, dtype(0)).view(ut))
+            X = rng.standard_normal((N, 3)).astype(np.float32)
+            Y = orc.spmm(v, o, lay, X)
+            ref = np.where(kept, W, 0).astype(np.float64) @ X.astype(np.float64)
+            assert np.allclose(Y, ref, rtol=0, atol=1e-12)
+    # fp16 decoding of a few bit patterns against numpy
+    for bits in [0x3C00, 0x0001, 0x7BFF, 0xC000, 0x0400]:
+        assert orc.half_to_double(bits) == float(np.array([bits], np.uint16).view(np.float16)[0])
+
+
+def test_real_oracle_passes_pin_suite():
+    pin_suite(oracle)
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_pins_catch_planted_mistake(tmp_path, name):
+    mod = _load_variant(tmp_path, name, MUTANTS[name])
+    with pytest.raises((AssertionError, ValueError)):
+        pin_suite(mod)

@@ -1,0 +1,358 @@
+"""Pins for the CPU oracle: worked examples, closed forms, brute force, invariants.
+
+Nothing here needs a GPU.  Every check compares the oracle with something other
+than the oracle itself: numbers the paper states (tests/golden/), exact
+rational brute force, numpy library routines, or algebraic invariants.
+"""
+import os
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+import oracle
+from tests._brute import block_size_brute, encode_brute, kept_positions
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _rows(name):
+    with open(os.path.join(GOLDEN, name)) as f:
+        return [ln.split() for ln in f if ln.strip() and not ln.startswith("#")]
+
+
+# ----------------------------------------------------------------------------------
+# block-size rule (section 3.2)
+# ----------------------------------------------------------------------------------
+
+def test_block_size_worked_example_paper_mode():
+    for D, d, b in _rows("block_size_worked_example.txt"):
+        got = oracle.block_log2(np.array([float(d)]), float(D), oracle.ROUND_PAPER, 1, 128)
+        assert (1 << int(got[0])) == int(b), (D, d, b)
+
+
+def test_worked_example_differs_between_modes():
+    # floor mode always rounds the density up: 0.1875 -> 0.25 -> block size 4
+    got = oracle.block_log2(np.array([0.1875]), 0.2188, oracle.ROUND_FLOOR, 1, 128)
+    assert (1 << int(got[0])) == 4
+
+
+@pytest.mark.parametrize("N", [256, 1500, 3072, 9216, 1000, 7])
+def test_floor_rule_exhaustive_counts(N):
+    """Floor mode equals 'largest 2^k with 2^k * count <= N' for every count."""
+    counts = np.arange(N + 1)
+    d = counts / float(N)
+    got = oracle.block_log2(d, 0.5, oracle.ROUND_FLOOR, 1, 128)
+    for c in range(N + 1):
+        if c == 0:
+            want = 128
+        else:
+            want = 1
+            while 2 * want * c <= N:
+                want *= 2
+            want = min(want, 128)
+        assert (1 << int(got[c])) == want, (N, c)
+
+
+@pytest.mark.parametrize("N", [256, 1500, 2048, 9216])
+@pytest.mark.parametrize("bounds", [(1, 128), (4, 32), (8, 128), (4, 64)])
+def test_paper_rule_vs_rational_brute_force(N, bounds):
+    b_min, b_max = bounds
+    rng = np.random.default_rng(N + b_min)
+    counts = np.unique(np.concatenate([np.arange(0, 40), rng.integers(0, N + 1, 400),
+                                       [N, N // 2, N // 4, N // 8, N // 3]]))
+    k_total = int(counts.sum())
+    D = k_total / float(N * counts.size)
+    Dexact = Fraction(D)          # the rule compares against the fp64 value it is given
+    d = counts / float(N)
+    for mode, name in [(oracle.ROUND_PAPER, "paper"), (oracle.ROUND_FLOOR, "floor")]:
+        got = oracle.block_log2(d, D, mode, b_min, b_max)
+        for i, c in enumerate(counts):
+            want = block_size_brute(int(c), N, Dexact, name, b_min, b_max)
+            assert (1 << int(got[i])) == want, (name, N, c, bounds)
+
+
+def test_row_density_equal_to_matrix_density_rounds_up():
+    # reading: a row exactly at the matrix density is treated like a denser row
+    got = oracle.block_log2(np.array([0.3]), 0.3, oracle.ROUND_PAPER, 1, 128)
+    assert (1 << int(got[0])) == 2   # 0.3 -> up to 0.5
+    got = oracle.block_log2(np.array([0.3]), 0.30000001, oracle.ROUND_PAPER, 1, 128)
+    assert (1 << int(got[0])) == 4   # 0.3 -> down to 0.25
+
+
+def test_empty_and_full_rows_and_clamp():
+    got = oracle.block_log2(np.array([0.0, 1.0, 0.9, 1e-300]), 0.1, oracle.ROUND_PAPER, 4, 64)
+    assert [1 << int(v) for v in got] == [64, 4, 4, 64]
+
+
+@pytest.mark.parametrize("bad", [
+    dict(d=[float("nan")]), dict(d=[-0.1]), dict(d=[1.5]), dict(b_min=3), dict(b_max=256),
+    dict(b_min=64, b_max=8), dict(mode=7), dict(D=float("nan")),
+])
+def test_block_rule_rejects_bad_arguments(bad):
+    args = dict(d=[0.1], D=0.1, mode=0, b_min=4, b_max=64)
+    args.update(bad)
+    with pytest.raises(ValueError):
+        oracle.block_log2(np.array(args["d"]), args["D"], args["mode"], args["b_min"], args["b_max"])
+
+
+# ----------------------------------------------------------------------------------
+# layout and block counts (section 3.2, section 4.2 / Table 7)
+# ----------------------------------------------------------------------------------
+
+def test_table7_decoding_total_pins_tail_block():
+    (n, bs, total), = _rows("decoding_table7.txt")
+    bs = [int(b) for b in bs.split(",")]
+    log2b = np.array([int(np.log2(b)) for b in bs], dtype=np.uint8)
+    lay = oracle.layout(int(n), log2b)
+    assert lay.nnz == int(total)
+
+
+def test_stated_block_counts():
+    for n, b, blocks in _rows("bmwm_block_counts.txt"):
+        n, b, blocks = int(n), int(b), int(blocks)
+        # one kept weight per block: a row of n elements keeps exactly n/b weights
+        row = np.random.default_rng(1).standard_normal(n).astype(np.float32)
+        assert len(kept_positions(row, b)) == blocks
+        if b & (b - 1) == 0:
+            lay = oracle.layout(n, np.array([int(np.log2(b))], dtype=np.uint8))
+            assert lay.nnz == blocks
+
+
+def test_layout_groups_rows_by_block_size():
+    log2b = np.array([3, 1, 3, 0, 7, 1, 2], dtype=np.uint8)
+    N = 100
+    lay = oracle.layout(N, log2b)
+    assert list(lay.perm) == [3, 1, 5, 6, 0, 2, 4]
+    nblk = [(N + (1 << l) - 1) >> l for l in log2b]
+    pos = 0
+    for r in lay.perm:
+        assert lay.row_start[r] == pos
+        pos += nblk[r]
+    assert lay.nnz == pos == sum(nblk)
+
+
+# ----------------------------------------------------------------------------------
+# BMWM (section 3.1) against brute force and library special cases
+# ----------------------------------------------------------------------------------
+
+def _tiny_matrix(rng, M, N, dtype):
+    # small integers make equal magnitudes (ties) and signed zeros frequent
+    vals = rng.integers(-3, 4, size=(M, N)).astype(np.float64)
+    vals *= rng.choice([1.0, 0.5, 0.25], size=(M, N))
+    W = vals.astype(dtype)
+    negz = rng.random((M, N)) < 0.1
+    W[negz] = -0.0
+    return W
+
+
+@pytest.mark.parametrize("dtype", [np.float32, np.float16])
+def test_bmwm_vs_brute_force(dtype):
+    rng = np.random.default_rng(11)
+    for trial in range(40):
+        M = int(rng.integers(1, 9))
+        N = int(rng.integers(1, 41))
+        W = _tiny_matrix(rng, M, N, dtype)
+        log2b = rng.integers(0, 6, size=M).astype(np.uint8)
+        lay = oracle.layout(N, log2b)
+        values, offsets = oracle.encode(W, lay)
+        ref = encode_brute(W, [1 << int(l) for l in log2b])
+        for r in range(M):
+            b = 1 << int(log2b[r])
+            s = int(lay.row_start[r])
+            cols = [k * b + int(offsets[s + k]) for k in range(int(lay.nblk[r]))]
+            assert cols == ref[r], (trial, r)
+            got_bits = values[s:s + len(cols)].view(np.uint32 if dtype == np.float32 else np.uint16)
+            want_bits = W[r, cols].view(got_bits.dtype)
+            assert np.array_equal(got_bits, want_bits)
+
+
+@pytest.mark.parametrize("dtype", [np.float32, np.float16])
+@pytest.mark.parametrize("b", [1, 2, 4])
+def test_bmwm_exhaustive_tie_patterns(dtype, b):
+    alphabet = np.array([-2.0, -1.0, -0.0, 0.0, 1.0, 2.0], dtype=dtype)
+    grid = np.stack(np.meshgrid(*([np.arange(6)] * b), indexing="ij"), -1).reshape(-1, b)
+    W = alphabet[grid]                              # every pattern is one row of one block
+    lay = oracle.layout(b, np.full(W.shape[0], int(np.log2(b)), dtype=np.uint8))
+    values, offsets = oracle.encode(W, lay)
+    for r in range(W.shape[0]):
+        assert kept_positions(W[r], b) == [int(offsets[lay.row_start[r]])]
+
+
+def test_bmwm_special_values_fp32():
+    f = np.float32
+    den = np.array([1e-45, 3e-45], dtype=f)     # denormals
+    row = np.array([0.0, -0.0, den[0], -den[1], np.inf, -np.inf, 1.0, 2.0], dtype=f)
+    lay = oracle.layout(8, np.array([1], dtype=np.uint8))   # blocks of 2
+    values, offsets = oracle.encode(row[None, :], lay)
+    assert list(offsets) == [0, 1, 0, 1]                     # +0 vs -0 tie -> first
+    assert values.view(np.uint32)[1] == row[3:4].view(np.uint32)[0]   # sign kept
+    assert np.isinf(values[2]) and values[2] > 0
+
+
+def test_bmwm_nan_outranks_inf_by_bits():
+    # reading: the magnitude key is the sign-cleared bit pattern, so NaN beats inf
+    row = np.array([np.inf, np.nan, 1.0, 2.0], dtype=np.float32)
+    lay = oracle.layout(4, np.array([2], dtype=np.uint8))
+    values, offsets = oracle.encode(row[None, :], lay)
+    assert int(offsets[0]) == 1 and np.isnan(values[0])
+
+
+@pytest.mark.parametrize("dtype", [np.float32, np.float16])
+def test_block_wider_than_row_is_numpy_argmax(dtype):
+    rng = np.random.default_rng(5)
+    W = rng.standard_normal((64, 37)).astype(dtype)
+    W[::7, 3] = W[::7, 11]                       # some exact ties
+    lay = oracle.layout(37, np.full(64, 6, dtype=np.uint8))   # b = 64 > N
+    values, offsets = oracle.encode(W, lay)
+    assert lay.nnz == 64
+    want = np.argmax(np.abs(W.astype(np.float64)), axis=1)    # first occurrence
+    assert np.array_equal(offsets.astype(np.int64), want)
+
+
+def test_block_size_one_is_identity():
+    W = np.random.default_rng(3).standard_normal((5, 13)).astype(np.float32)
+    lay = oracle.layout(13, np.zeros(5, dtype=np.uint8))
+    values, offsets = oracle.encode(W, lay)
+    assert not offsets.any()
+    assert np.array_equal(values.reshape(5, 13), W)
+
+
+def test_half_conversion_all_patterns():
+    bits = np.arange(65536, dtype=np.uint32).astype(np.uint16)
+    want = bits.view(np.float16).astype(np.float64)
+    got = np.array([oracle.half_to_double(int(b)) for b in bits])
+    nan = np.isnan(want)
+    assert np.array_equal(np.isnan(got), nan)
+    assert np.array_equal(got[~nan], want[~nan])
+    assert np.array_equal(np.signbit(got[~nan]), np.signbit(want[~nan]))
+
+
+# ----------------------------------------------------------------------------------
+# format invariants
+# ----------------------------------------------------------------------------------
+
+@pytest.mark.parametrize("dtype", [np.float32, np.float16])
+def test_format_invariants_and_roundtrip(dtype):
+    rng = np.random.default_rng(21)
+    M, N = 37, 203                                  # N not a multiple of any b > 1
+    W = rng.standard_normal((M, N)).astype(dtype)
+    W[rng.random((M, N)) < 0.05] = -0.0
+    log2b = rng.integers(0, 8, size=M).astype(np.uint8)
+    lay = oracle.layout(N, log2b)
+    values, offsets = oracle.encode(W, lay)
+    kept = np.zeros((M, N), dtype=bool)
+    for r in range(M):
+        b = 1 << int(log2b[r])
+        nb = int(lay.nblk[r])
+        assert nb == -(-N // b)
+        s = int(lay.row_start[r])
+        offs = offsets[s:s + nb].astype(np.int64)
+        assert (offs < b).all()
+        cols = np.arange(nb) * b + offs
+        assert (cols < N).all()
+        kept[r, cols] = True
+        # exactly one kept weight per block
+        assert np.array_equal(np.bincount(cols // b, minlength=nb), np.ones(nb))
+    Wm = oracle.decode(values, offsets, lay)
+    ut = np.uint32 if dtype == np.float32 else np.uint16
+    want = np.where(kept, W, dtype(0.0))
+    assert np.array_equal(Wm.view(ut), want.view(ut))        # +0.0 where not kept
+
+
+@pytest.mark.parametrize("dtype", [np.float32, np.float16])
+def test_negation_and_power_of_two_scaling_equivariance(dtype):
+    rng = np.random.default_rng(8)
+    W = rng.standard_normal((20, 70)).astype(dtype)
+    lay = oracle.layout(70, rng.integers(0, 7, size=20).astype(np.uint8))
+    v, o = oracle.encode(W, lay)
+    vn, on = oracle.encode(-W, lay)
+    v2, o2 = oracle.encode(W * dtype(2.0), lay)
+    assert np.array_equal(o, on) and np.array_equal(o, o2)
+    assert np.array_equal(vn, -v) and np.array_equal(v2, v * dtype(2.0))
+
+
+# ----------------------------------------------------------------------------------
+# products (sections 2 / 3.2): equal to the dense masked product
+# ----------------------------------------------------------------------------------
+
+@pytest.mark.parametrize("wdt,xdt", [(np.float32, np.float32), (np.float16, np.float16),
+                                     (np.float16, np.float32)])
+def test_product_equals_dense_masked_matmul(wdt, xdt):
+    rng = np.random.default_rng(4)
+    M, N, B = 50, 300, 7
+    W = rng.standard_normal((M, N)).astype(wdt)
+    lay = oracle.layout(N, rng.integers(0, 8, size=M).astype(np.uint8))
+    v, o = oracle.encode(W, lay)
+    X = rng.standard_normal((N, B)).astype(xdt)
+    Y = oracle.spmm(v, o, lay, X)
+    ref = oracle.dense_masked_product(oracle.decode(v, o, lay), X)
+    scale = oracle.spmm_absdot(v, o, lay, X)
+    assert np.all(np.abs(Y - ref) <= 1e-14 * scale + 1e-300)
+    y = oracle.spmm(v, o, lay, X[:, 0].copy())
+    assert np.array_equal(y, Y[:, 0])
+
+
+def test_product_with_unit_vector_returns_masked_column():
+    rng = np.random.default_rng(6)
+    M, N = 30, 90
+    W = rng.standard_normal((M, N)).astype(np.float32)
+    lay = oracle.layout(N, rng.integers(0, 6, size=M).astype(np.uint8))
+    v, o = oracle.encode(W, lay)
+    Wm = oracle.decode(v, o, lay)
+    for c in [0, 1, 45, 89]:
+        e = np.zeros(N, dtype=np.float32)
+        e[c] = 1.0
+        assert np.array_equal(oracle.spmm(v, o, lay, e), Wm[:, c].astype(np.float64))
+
+
+def test_block_size_one_product_is_dense_gemv():
+    rng = np.random.default_rng(7)
+    W = rng.standard_normal((16, 40)).astype(np.float32)
+    x = rng.standard_normal(40).astype(np.float32)
+    lay = oracle.layout(40, np.zeros(16, dtype=np.uint8))
+    v, o = oracle.encode(W, lay)
+    y = oracle.spmm(v, o, lay, x)
+    assert np.allclose(y, W.astype(np.float64) @ x.astype(np.float64), rtol=0, atol=1e-13)
+
+
+def test_malformed_offsets_are_rejected():
+    lay = oracle.layout(10, np.array([2], dtype=np.uint8))    # b = 4, 3 blocks, tail of 2
+    v = np.ones(3, dtype=np.float32)
+    o = np.array([0, 1, 3], dtype=np.uint8)                    # 8 + 3 = 11 >= 10
+    with pytest.raises(ValueError):
+        oracle.decode(v, o, lay)
+    with pytest.raises(ValueError):
+        oracle.spmm(v, o, lay, np.ones(10, dtype=np.float32))
+
+
+# ----------------------------------------------------------------------------------
+# the recurrent workload's LSTM against torch.nn.LSTM (library routine)
+# ----------------------------------------------------------------------------------
+
+def test_lstm_forward_matches_torch_lstm():
+    torch = pytest.importorskip("torch")
+    rng = np.random.default_rng(9)
+    H, T, Bt, L = 8, 5, 3, 2
+    masked = []
+    for _ in range(L):
+        pair = []
+        for _ in range(2):
+            W = (0.3 * rng.standard_normal((4 * H, H))).astype(np.float16)
+            lay = oracle.layout(H, rng.integers(0, 3, size=4 * H).astype(np.uint8))
+            v, o = oracle.encode(W, lay)
+            pair.append(oracle.decode(v, o, lay).astype(np.float64))
+        masked.append(tuple(pair))
+    xs = rng.standard_normal((H, T * Bt)).astype(np.float32)
+    out, finals = oracle.lstm_forward(masked, xs, H, T, Bt)
+    lstm = torch.nn.LSTM(H, H, num_layers=L, bias=False).double()
+    with torch.no_grad():
+        for l in range(L):
+            getattr(lstm, f"weight_ih_l{l}").copy_(torch.from_numpy(masked[l][0]))
+            getattr(lstm, f"weight_hh_l{l}").copy_(torch.from_numpy(masked[l][1]))
+        seq = torch.from_numpy(xs.astype(np.float64)).reshape(H, T, Bt).permute(1, 2, 0)
+        ref, (hn, cn) = lstm(seq)
+    ref = ref.permute(2, 0, 1).reshape(H, T * Bt).numpy()
+    assert np.allclose(out, ref, rtol=0, atol=1e-12)
+    for l in range(L):
+        assert np.allclose(finals[l][1], cn[l].numpy().T, rtol=0, atol=1e-12)
