@@ -1,0 +1,297 @@
+"""Python binding of the MI355X DARB library (libdarb.so, C ABI in include/darb.h).
+
+Argument marshalling only: every step of DARB runs in the library's HIP
+kernels.  torch supplies device memory and the current HIP stream; numpy
+arrays are accepted for host-side inputs (row densities).
+
+    plan = Plan(M, N, row_density, matrix_density, mode=ROUND_FLOOR, b_min=4, b_max=64)
+    plan.upload()                           # device metadata into a torch workspace
+    values, offsets = plan.encode(W)        # W: cuda tensor [M, N] fp32/fp16
+    y = plan.spmv(values, offsets, x)       # fp32 [M]
+    Y = plan.spmm(values, offsets, X)       # X: [N, B], fp32 [M, B]
+
+The library must have been built (``python -m paper_1911_08020_amd.build`` or
+``__graft_entry__.build()``); importing this package fails loudly otherwise.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Tuple
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libdarb.so")
+
+OK = 0
+E_INVALID = -1
+E_DTYPE = -2
+E_NOT_UPLOADED = -3
+E_HIP = -4
+E_NOMEM = -5
+E_WORKSPACE = -6
+
+F32 = 0
+F16 = 1
+ROUND_FLOOR = 0
+ROUND_PAPER = 1
+
+
+class DarbError(RuntimeError):
+    def __init__(self, code: int, where: str, detail: str):
+        super().__init__(f"{where}: {_strerror(code)} ({code}): {detail}")
+        self.code = code
+
+
+class _Bin(ctypes.Structure):
+    _fields_ = [("log2b", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("first_row", ctypes.c_int64), ("rows", ctypes.c_int64),
+                ("first_elem", ctypes.c_int64), ("nblk", ctypes.c_int64)]
+
+
+class _Info(ctypes.Structure):
+    _fields_ = [("M", ctypes.c_int64), ("N", ctypes.c_int64), ("nnz", ctypes.c_int64),
+                ("workspace_bytes", ctypes.c_int64), ("nbins", ctypes.c_int32),
+                ("reserved", ctypes.c_int32), ("bins", _Bin * 8)]
+
+
+def _load_library():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(
+            f"DARB HIP library not built: {LIB_PATH} is missing. "
+            "Run `python -m paper_1911_08020_amd.build` (hipcc, gfx950) first.")
+    lib = ctypes.CDLL(LIB_PATH)
+    P, I64, I = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int
+    sig = {
+        "darb_version": ([], I),
+        "darb_strerror": ([I], ctypes.c_char_p),
+        "darb_last_error": ([], ctypes.c_char_p),
+        "darb_plan_create": ([I64, I64, P, ctypes.c_double, I, I, I, ctypes.POINTER(P)], I),
+        "darb_plan_info": ([P, ctypes.POINTER(_Info)], I),
+        "darb_plan_export": ([P, P, P, P], I),
+        "darb_plan_upload": ([P, P, I64, P], I),
+        "darb_plan_destroy": ([P], None),
+        "darb_encode": ([P, I, P, I64, P, P, P], I),
+        "darb_decode": ([P, I, P, P, P, I64, P], I),
+        "darb_spmv": ([P, I, P, P, I, P, P, P], I),
+        "darb_spmm": ([P, I, P, P, I, I64, P, I64, P, I64, P], I),
+        "darb_lstm_layer": ([P, P, P, P, P, P, I, I64, I64, I64, P, P, P, P, P, I64, P], I),
+        "darb_stream_read": ([P, I64, P, P], I),
+        "darb_stream_copy": ([P, P, I64, P], I),
+    }
+    for name, (args, res) in sig.items():
+        fn = getattr(lib, name)
+        fn.argtypes = args
+        fn.restype = res
+    return lib
+
+
+_lib = _load_library()
+
+#: every symbol include/darb.h declares
+EXPORTED = ("darb_plan_create", "darb_plan_info", "darb_plan_export", "darb_plan_upload",
+            "darb_plan_destroy", "darb_encode", "darb_decode", "darb_spmv", "darb_spmm",
+            "darb_lstm_layer", "darb_stream_read", "darb_stream_copy", "darb_strerror",
+            "darb_last_error", "darb_version")
+
+
+def lib():
+    return _lib
+
+
+def _strerror(code: int) -> str:
+    return _lib.darb_strerror(code).decode()
+
+
+def _check(rc: int, where: str):
+    if rc != OK:
+        raise DarbError(rc, where, _lib.darb_last_error().decode())
+
+
+def _torch():
+    import torch
+    return torch
+
+
+def _stream_ptr(stream=None):
+    torch = _torch()
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _dtype_code(t) -> int:
+    torch = _torch()
+    if t.dtype == torch.float32:
+        return F32
+    if t.dtype == torch.float16:
+        return F16
+    raise TypeError(f"unsupported dtype {t.dtype} (fp32 or fp16)")
+
+
+def _ptr(t) -> ctypes.c_void_p:
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _require_cuda(*ts):
+    for t in ts:
+        if not t.is_cuda:
+            raise ValueError("device tensors required (torch cuda tensors)")
+
+
+def _row_major_ld(t, rows: int, cols: int, name: str) -> int:
+    if t.dim() != 2 or t.shape[0] != rows or t.shape[1] != cols:
+        raise ValueError(f"{name} must be [{rows}, {cols}], got {tuple(t.shape)}")
+    if t.stride(1) != 1:
+        raise ValueError(f"{name} must have unit column stride")
+    return t.stride(0) if rows > 1 else max(cols, t.stride(0))
+
+
+class Plan:
+    """A DARB plan: block sizes and grouped layout from row densities (section 3.2)."""
+
+    def __init__(self, M: int, N: int, row_density, matrix_density: float,
+                 mode: int = ROUND_FLOOR, b_min: int = 1, b_max: int = 128):
+        d = np.ascontiguousarray(row_density, dtype=np.float64)
+        if d.shape != (M,):
+            raise ValueError(f"row_density must have shape ({M},)")
+        h = ctypes.c_void_p()
+        _check(_lib.darb_plan_create(int(M), int(N), d.ctypes.data_as(ctypes.c_void_p),
+                                     float(matrix_density), int(mode), int(b_min), int(b_max),
+                                     ctypes.byref(h)), "darb_plan_create")
+        self._h = h
+        info = _Info()
+        _check(_lib.darb_plan_info(h, ctypes.byref(info)), "darb_plan_info")
+        self.M, self.N, self.nnz = info.M, info.N, info.nnz
+        self.workspace_bytes = info.workspace_bytes
+        self.bins = [dict(log2b=b.log2b, first_row=b.first_row, rows=b.rows,
+                          first_elem=b.first_elem, nblk=b.nblk)
+                     for b in info.bins[:info.nbins]]
+        self.workspace = None
+
+    def __del__(self):
+        h = getattr(self, "_h", None)
+        if h is not None and h.value:
+            _lib.darb_plan_destroy(h)
+            self._h = None
+
+    @property
+    def handle(self):
+        return self._h
+
+    def export(self) -> Tuple[np.ndarray, np.ndarray, np.ndarray]:
+        log2b = np.zeros(self.M, dtype=np.uint8)
+        row_start = np.zeros(self.M, dtype=np.int64)
+        perm = np.zeros(self.M, dtype=np.int32)
+        _check(_lib.darb_plan_export(self._h, log2b.ctypes.data_as(ctypes.c_void_p),
+                                     row_start.ctypes.data_as(ctypes.c_void_p),
+                                     perm.ctypes.data_as(ctypes.c_void_p)), "darb_plan_export")
+        return log2b, row_start, perm
+
+    def upload(self, device=None, stream=None):
+        torch = _torch()
+        dev = torch.device("cuda") if device is None else torch.device(device)
+        ws = torch.empty(self.workspace_bytes, dtype=torch.uint8, device=dev)
+        _check(_lib.darb_plan_upload(self._h, _ptr(ws), self.workspace_bytes,
+                                     _stream_ptr(stream)), "darb_plan_upload")
+        self.workspace = ws
+        return self
+
+    # -- device calls -----------------------------------------------------------------
+    def empty_format(self, dtype, device=None):
+        torch = _torch()
+        dev = self.workspace.device if device is None else device
+        return (torch.empty(self.nnz, dtype=dtype, device=dev),
+                torch.empty(self.nnz, dtype=torch.uint8, device=dev))
+
+    def encode(self, W, values=None, offsets=None, stream=None):
+        """BMWM encode of W [M, N] (cuda, fp32/fp16, unit column stride)."""
+        _require_cuda(W)
+        ldw = _row_major_ld(W, self.M, self.N, "W")
+        if values is None or offsets is None:
+            values, offsets = self.empty_format(W.dtype, W.device)
+        _check(_lib.darb_encode(self._h, _dtype_code(W), _ptr(W), ldw, _ptr(values),
+                                _ptr(offsets), _stream_ptr(stream)), "darb_encode")
+        return values, offsets
+
+    def decode(self, values, offsets, out=None, stream=None):
+        torch = _torch()
+        _require_cuda(values, offsets)
+        if out is None:
+            out = torch.empty((self.M, self.N), dtype=values.dtype, device=values.device)
+        ldw = _row_major_ld(out, self.M, self.N, "out")
+        _check(_lib.darb_decode(self._h, _dtype_code(values), _ptr(values), _ptr(offsets),
+                                _ptr(out), ldw, _stream_ptr(stream)), "darb_decode")
+        return out
+
+    def spmv(self, values, offsets, x, y=None, stream=None):
+        torch = _torch()
+        _require_cuda(values, offsets, x)
+        if x.dim() != 1 or x.shape[0] != self.N or not x.is_contiguous():
+            raise ValueError(f"x must be a contiguous [{self.N}] tensor")
+        if y is None:
+            y = torch.empty(self.M, dtype=torch.float32, device=x.device)
+        _check(_lib.darb_spmv(self._h, _dtype_code(values), _ptr(values), _ptr(offsets),
+                              _dtype_code(x), _ptr(x), _ptr(y), _stream_ptr(stream)),
+               "darb_spmv")
+        return y
+
+    def spmm(self, values, offsets, X, Y=None, stream=None):
+        torch = _torch()
+        _require_cuda(values, offsets, X)
+        if X.dim() != 2 or X.shape[0] != self.N:
+            raise ValueError(f"X must be [{self.N}, B]")
+        B = X.shape[1]
+        ldx = _row_major_ld(X, self.N, B, "X")
+        if Y is None:
+            Y = torch.empty((self.M, B), dtype=torch.float32, device=X.device)
+        ldy = _row_major_ld(Y, self.M, B, "Y")
+        _check(_lib.darb_spmm(self._h, _dtype_code(values), _ptr(values), _ptr(offsets),
+                              _dtype_code(X), B, _ptr(X), ldx, _ptr(Y), ldy,
+                              _stream_ptr(stream)), "darb_spmm")
+        return Y
+
+
+def lstm_layer(wih: Tuple[Plan, object, object], whh: Tuple[Plan, object, object], x_seq,
+               hidden: int, seq_len: int, batch: int, h=None, c=None, h_seq=None,
+               workspace=None, stream=None):
+    """One LSTM layer over a sequence with DARB weights (gate order i, f, g, o, no bias).
+
+    ``wih``/``whh`` are (plan, values, offsets); ``x_seq`` is fp32 [I, T*batch].
+    Returns (h_seq [H, T*batch], h [H, batch], c [H, batch]).
+    """
+    torch = _torch()
+    H, T, Bt = hidden, seq_len, batch
+    dev = x_seq.device
+    if h is None:
+        h = torch.zeros((H, Bt), dtype=torch.float32, device=dev)
+    if c is None:
+        c = torch.zeros((H, Bt), dtype=torch.float32, device=dev)
+    if h_seq is None:
+        h_seq = torch.empty((H, T * Bt), dtype=torch.float32, device=dev)
+    need = 4 * H * T * Bt + 4 * H * Bt
+    if workspace is None:
+        workspace = torch.empty(need, dtype=torch.float32, device=dev)
+    for t in (x_seq, h, c, h_seq, workspace):
+        if t.dtype != torch.float32 or not t.is_contiguous():
+            raise ValueError("LSTM state and sequences must be contiguous fp32")
+    if x_seq.shape != (wih[0].N, T * Bt):
+        raise ValueError("x_seq must be [I, T*batch]")
+    _check(_lib.darb_lstm_layer(wih[0].handle, _ptr(wih[1]), _ptr(wih[2]), whh[0].handle,
+                                _ptr(whh[1]), _ptr(whh[2]), _dtype_code(wih[1]), H, T, Bt,
+                                _ptr(x_seq), _ptr(h_seq), _ptr(h), _ptr(c), _ptr(workspace),
+                                workspace.numel(), _stream_ptr(stream)), "darb_lstm_layer")
+    return h_seq, h, c
+
+
+def stream_read(buf, sink, stream=None):
+    _check(_lib.darb_stream_read(_ptr(buf), buf.numel() * buf.element_size(), _ptr(sink),
+                                 _stream_ptr(stream)), "darb_stream_read")
+
+
+def stream_copy(dst, src, stream=None):
+    nbytes = src.numel() * src.element_size()
+    if dst.numel() * dst.element_size() < nbytes:
+        raise ValueError("dst smaller than src")
+    _check(_lib.darb_stream_copy(_ptr(dst), _ptr(src), nbytes, _stream_ptr(stream)),
+           "darb_stream_copy")

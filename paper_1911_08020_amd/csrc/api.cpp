@@ -1,0 +1,340 @@
+// Host side of the DARB library: plan construction (section 3.2 block-size
+// rule and grouped layout), argument checking and dispatch to the kernels.
+#include <cmath>
+#include <cstring>
+#include <new>
+#include <string>
+
+#include "darb_internal.h"
+
+namespace darb {
+
+static thread_local std::string g_last_error;
+
+int fail(int code, const std::string &detail) {
+    g_last_error = detail;
+    return code;
+}
+
+void clear_error() { g_last_error.clear(); }
+
+static bool is_pow2(int64_t v) { return v > 0 && (v & (v - 1)) == 0; }
+
+static int log2_exact(int64_t v) {
+    int l = 0;
+    while ((int64_t(1) << l) != v) ++l;
+    return l;
+}
+
+// Section 3.2: move the row density d to a power-of-two fraction and take its
+// reciprocal.  With d = m * 2^e (frexp, m in [0.5, 1)), the smallest power-of-
+// two fraction >= d is 2^(e-1) when m == 0.5 (d already is one) and 2^e
+// otherwise; the largest one <= d is 2^(e-1).  Rounding up therefore gives
+// log2 b = 1 - e (m == 0.5) or -e, rounding down gives 1 - e.  Paper mode rounds
+// up for d >= D and down for d < D; floor mode always rounds up.  A row of
+// density 0 gets b_max.  The result is clamped to [log2 b_min, log2 b_max].
+static int row_log2b(double d, double D, int mode, int lmin, int lmax) {
+    if (d == 0.0) return lmax;
+    int e = 0;
+    const double m = std::frexp(d, &e);
+    const bool exact = (m == 0.5);
+    const bool round_up = (mode == DARB_ROUND_FLOOR) || (d >= D);
+    int64_t l = (round_up && !exact) ? -int64_t(e) : 1 - int64_t(e);
+    if (l < lmin) l = lmin;
+    if (l > lmax) l = lmax;
+    return int(l);
+}
+
+}  // namespace darb
+
+using namespace darb;
+
+extern "C" {
+
+int darb_version(void) { return 100; }
+
+const char *darb_strerror(int code) {
+    switch (code) {
+        case DARB_OK: return "success";
+        case DARB_E_INVALID: return "invalid argument";
+        case DARB_E_DTYPE: return "unsupported dtype";
+        case DARB_E_NOT_UPLOADED: return "plan has no device metadata (call darb_plan_upload)";
+        case DARB_E_HIP: return "HIP runtime error";
+        case DARB_E_NOMEM: return "host allocation failed";
+        case DARB_E_WORKSPACE: return "workspace too small";
+        default: return "unknown error code";
+    }
+}
+
+const char *darb_last_error(void) { return g_last_error.c_str(); }
+
+int darb_plan_create(int64_t M, int64_t N, const double *row_density, double matrix_density,
+                     int round_mode, int b_min, int b_max, darb_plan **out) {
+    clear_error();
+    if (!out) return fail(DARB_E_INVALID, "out is NULL");
+    *out = nullptr;
+    if (M < 1 || M >= (int64_t(1) << 31)) return fail(DARB_E_INVALID, "M must be in [1, 2^31)");
+    if (N < 1 || N >= (int64_t(1) << 31)) return fail(DARB_E_INVALID, "N must be in [1, 2^31)");
+    if (!row_density) return fail(DARB_E_INVALID, "row_density is NULL");
+    if (round_mode != DARB_ROUND_FLOOR && round_mode != DARB_ROUND_PAPER)
+        return fail(DARB_E_INVALID, "unknown round_mode");
+    if (!is_pow2(b_min) || !is_pow2(b_max) || b_min > b_max || b_max > 128)
+        return fail(DARB_E_INVALID, "b_min, b_max must be powers of two, 1 <= b_min <= b_max <= 128");
+    if (!(matrix_density >= 0.0 && matrix_density <= 1.0))
+        return fail(DARB_E_INVALID, "matrix_density must be in [0, 1]");
+    for (int64_t r = 0; r < M; ++r) {
+        const double d = row_density[r];
+        if (!(d >= 0.0 && d <= 1.0))
+            return fail(DARB_E_INVALID, "row_density[" + std::to_string(r) + "] not in [0, 1]");
+    }
+    darb_plan *p = new (std::nothrow) darb_plan();
+    if (!p) return fail(DARB_E_NOMEM, "plan allocation");
+    try {
+        p->M = M;
+        p->N = N;
+        p->mode = round_mode;
+        p->b_min = b_min;
+        p->b_max = b_max;
+        p->log2b.resize(M);
+        p->row_start.resize(M);
+        p->perm.resize(M);
+    } catch (const std::bad_alloc &) {
+        delete p;
+        return fail(DARB_E_NOMEM, "plan arrays");
+    }
+    const int lmin = log2_exact(b_min), lmax = log2_exact(b_max);
+    int64_t count[kMaxBins] = {0};
+    for (int64_t r = 0; r < M; ++r) {
+        const int l = row_log2b(row_density[r], matrix_density, round_mode, lmin, lmax);
+        p->log2b[r] = uint8_t(l);
+        ++count[l];
+    }
+    // grouped layout: groups by ascending block size, rows ascending inside
+    int64_t group_row[kMaxBins], group_elem[kMaxBins];
+    int64_t row = 0, elem = 0;
+    BinTable &bt = p->bins;
+    bt.nbins = 0;
+    for (int l = 0; l <= kMaxLog2B; ++l) {
+        const int64_t nblk = (N + (int64_t(1) << l) - 1) >> l;
+        group_row[l] = row;
+        group_elem[l] = elem;
+        if (count[l] > 0) {
+            const int g = bt.nbins++;
+            bt.log2b[g] = l;
+            bt.first_row[g] = row;
+            bt.rows[g] = count[l];
+            bt.first_elem[g] = elem;
+            bt.nblk[g] = nblk;
+        }
+        row += count[l];
+        elem += count[l] * nblk;
+    }
+    p->nnz = elem;
+    for (int64_t r = 0; r < M; ++r) {
+        const int l = p->log2b[r];
+        const int64_t nblk = (N + (int64_t(1) << l) - 1) >> l;
+        const int64_t i = group_row[l]++;
+        p->perm[i] = int32_t(r);
+        p->row_start[r] = group_elem[l];
+        group_elem[l] += nblk;
+    }
+    p->workspace_bytes = ((M * int64_t(sizeof(int32_t))) + 255) / 256 * 256;
+    *out = p;
+    return DARB_OK;
+}
+
+int darb_plan_info(const darb_plan *p, darb_plan_info_t *info) {
+    clear_error();
+    if (!p || !info) return fail(DARB_E_INVALID, "NULL argument");
+    std::memset(info, 0, sizeof(*info));
+    info->M = p->M;
+    info->N = p->N;
+    info->nnz = p->nnz;
+    info->workspace_bytes = p->workspace_bytes;
+    info->nbins = p->bins.nbins;
+    for (int g = 0; g < p->bins.nbins; ++g) {
+        info->bins[g].log2b = p->bins.log2b[g];
+        info->bins[g].first_row = p->bins.first_row[g];
+        info->bins[g].rows = p->bins.rows[g];
+        info->bins[g].first_elem = p->bins.first_elem[g];
+        info->bins[g].nblk = p->bins.nblk[g];
+    }
+    return DARB_OK;
+}
+
+int darb_plan_export(const darb_plan *p, uint8_t *log2b, int64_t *row_start, int32_t *perm) {
+    clear_error();
+    if (!p) return fail(DARB_E_INVALID, "plan is NULL");
+    if (log2b) std::memcpy(log2b, p->log2b.data(), p->M * sizeof(uint8_t));
+    if (row_start) std::memcpy(row_start, p->row_start.data(), p->M * sizeof(int64_t));
+    if (perm) std::memcpy(perm, p->perm.data(), p->M * sizeof(int32_t));
+    return DARB_OK;
+}
+
+int darb_plan_upload(darb_plan *p, void *workspace, int64_t workspace_bytes, void *stream) {
+    clear_error();
+    if (!p || !workspace) return fail(DARB_E_INVALID, "NULL argument");
+    if ((reinterpret_cast<uintptr_t>(workspace) & 255) != 0)
+        return fail(DARB_E_INVALID, "workspace must be 256-byte aligned");
+    if (workspace_bytes < p->workspace_bytes)
+        return fail(DARB_E_WORKSPACE, "workspace needs " + std::to_string(p->workspace_bytes) +
+                                          " bytes, got " + std::to_string(workspace_bytes));
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return fail(DARB_E_HIP, std::string("hipGetDevice: ") + hipGetErrorString(e));
+    int32_t *d_perm = static_cast<int32_t *>(workspace);
+    e = hipMemcpyAsync(d_perm, p->perm.data(), p->M * sizeof(int32_t), hipMemcpyHostToDevice,
+                       static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return fail(DARB_E_HIP, std::string("hipMemcpyAsync: ") + hipGetErrorString(e));
+    p->d_perm = d_perm;
+    p->device = dev;
+    return DARB_OK;
+}
+
+void darb_plan_destroy(darb_plan *p) { delete p; }
+
+}  // extern "C"
+
+// ---------------------------------------------------------------------------
+// device entry points
+// ---------------------------------------------------------------------------
+
+static int check_uploaded(const darb_plan *p) {
+    if (!p) return fail(DARB_E_INVALID, "plan is NULL");
+    if (!p->d_perm) return fail(DARB_E_NOT_UPLOADED, "plan was not uploaded");
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return fail(DARB_E_HIP, std::string("hipGetDevice: ") + hipGetErrorString(e));
+    if (dev != p->device)
+        return fail(DARB_E_INVALID, "plan was uploaded on device " + std::to_string(p->device) +
+                                        ", current device is " + std::to_string(dev));
+    return DARB_OK;
+}
+
+static bool valid_dtype(int t) { return t == DARB_F32 || t == DARB_F16; }
+
+static int launched(hipError_t e, const char *what) {
+    if (e == hipSuccess) e = hipGetLastError();
+    else (void)hipGetLastError();
+    if (e != hipSuccess) return fail(DARB_E_HIP, std::string(what) + ": " + hipGetErrorString(e));
+    return DARB_OK;
+}
+
+static int check_product_dtypes(int wdtype, int xdtype) {
+    if (!valid_dtype(wdtype) || !valid_dtype(xdtype)) return fail(DARB_E_DTYPE, "unknown dtype");
+    if (wdtype == DARB_F32 && xdtype != DARB_F32)
+        return fail(DARB_E_DTYPE, "fp32 weights need fp32 activations");
+    return DARB_OK;
+}
+
+extern "C" {
+
+int darb_encode(const darb_plan *p, int wdtype, const void *W, int64_t ldw, void *values,
+                uint8_t *offsets, void *stream) {
+    clear_error();
+    int rc = check_uploaded(p);
+    if (rc) return rc;
+    if (!valid_dtype(wdtype)) return fail(DARB_E_DTYPE, "unknown weight dtype");
+    if (!W || !values || !offsets) return fail(DARB_E_INVALID, "NULL buffer");
+    if (ldw < p->N) return fail(DARB_E_INVALID, "ldw < N");
+    return launched(launch_encode(*p, wdtype, W, ldw, values, offsets,
+                                  static_cast<hipStream_t>(stream)), "encode launch");
+}
+
+int darb_decode(const darb_plan *p, int wdtype, const void *values, const uint8_t *offsets,
+                void *W_out, int64_t ldw, void *stream) {
+    clear_error();
+    int rc = check_uploaded(p);
+    if (rc) return rc;
+    if (!valid_dtype(wdtype)) return fail(DARB_E_DTYPE, "unknown weight dtype");
+    if (!W_out || !values || !offsets) return fail(DARB_E_INVALID, "NULL buffer");
+    if (ldw < p->N) return fail(DARB_E_INVALID, "ldw < N");
+    return launched(launch_decode(*p, wdtype, values, offsets, W_out, ldw,
+                                  static_cast<hipStream_t>(stream)), "decode launch");
+}
+
+int darb_spmv(const darb_plan *p, int wdtype, const void *values, const uint8_t *offsets,
+              int xdtype, const void *x, float *y, void *stream) {
+    clear_error();
+    int rc = check_uploaded(p);
+    if (rc) return rc;
+    rc = check_product_dtypes(wdtype, xdtype);
+    if (rc) return rc;
+    if (!values || !offsets || !x || !y) return fail(DARB_E_INVALID, "NULL buffer");
+    return launched(launch_spmv(*p, wdtype, values, offsets, xdtype, x, y,
+                                static_cast<hipStream_t>(stream)), "spmv launch");
+}
+
+int darb_spmm(const darb_plan *p, int wdtype, const void *values, const uint8_t *offsets,
+              int xdtype, int64_t B, const void *X, int64_t ldx, float *Y, int64_t ldy,
+              void *stream) {
+    clear_error();
+    int rc = check_uploaded(p);
+    if (rc) return rc;
+    rc = check_product_dtypes(wdtype, xdtype);
+    if (rc) return rc;
+    if (!values || !offsets || !X || !Y) return fail(DARB_E_INVALID, "NULL buffer");
+    if (B < 1 || B >= (int64_t(1) << 31)) return fail(DARB_E_INVALID, "B must be in [1, 2^31)");
+    if (ldx < B) return fail(DARB_E_INVALID, "ldx < B");
+    if (ldy < B) return fail(DARB_E_INVALID, "ldy < B");
+    return launched(launch_spmm(*p, wdtype, values, offsets, xdtype, B, X, ldx, Y, ldy,
+                                static_cast<hipStream_t>(stream)), "spmm launch");
+}
+
+int darb_lstm_layer(const darb_plan *wih, const void *wih_values, const uint8_t *wih_offsets,
+                    const darb_plan *whh, const void *whh_values, const uint8_t *whh_offsets,
+                    int wdtype, int64_t H, int64_t T, int64_t batch, const float *x_seq,
+                    float *h_seq, float *h, float *c, float *workspace,
+                    int64_t workspace_floats, void *stream) {
+    clear_error();
+    int rc = check_uploaded(wih);
+    if (rc) return rc;
+    rc = check_uploaded(whh);
+    if (rc) return rc;
+    if (!valid_dtype(wdtype)) return fail(DARB_E_DTYPE, "unknown weight dtype");
+    if (!wih_values || !wih_offsets || !whh_values || !whh_offsets || !x_seq || !h_seq || !h ||
+        !c || !workspace)
+        return fail(DARB_E_INVALID, "NULL buffer");
+    if (H < 1 || T < 1 || batch < 1) return fail(DARB_E_INVALID, "H, T, batch must be >= 1");
+    if (whh->M != 4 * H || whh->N != H) return fail(DARB_E_INVALID, "W_hh must be [4H x H]");
+    if (wih->M != 4 * H) return fail(DARB_E_INVALID, "W_ih must have 4H rows");
+    const int64_t TB = T * batch;
+    if (TB >= (int64_t(1) << 31)) return fail(DARB_E_INVALID, "T * batch too large");
+    const int64_t need = 4 * H * TB + 4 * H * batch;
+    if (workspace_floats < need)
+        return fail(DARB_E_WORKSPACE, "lstm workspace needs " + std::to_string(need) + " floats");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    float *U = workspace;              // [4H x T*batch]: input products of every step
+    float *G = workspace + 4 * H * TB; // [4H x batch]: recurrent product of one step
+    rc = launched(launch_spmm(*wih, wdtype, wih_values, wih_offsets, DARB_F32, TB, x_seq, TB, U,
+                              TB, s), "lstm input product");
+    if (rc) return rc;
+    for (int64_t t = 0; t < T; ++t) {
+        rc = launched(launch_spmm(*whh, wdtype, whh_values, whh_offsets, DARB_F32, batch, h,
+                                  batch, G, batch, s), "lstm recurrent product");
+        if (rc) return rc;
+        rc = launched(launch_lstm_cell(H, batch, G, U + t * batch, TB, h, c, h_seq + t * batch, TB,
+                                       s), "lstm cell");
+        if (rc) return rc;
+    }
+    return DARB_OK;
+}
+
+int darb_stream_read(const void *buf, int64_t bytes, float *sink, void *stream) {
+    clear_error();
+    if (!buf || !sink || bytes <= 0 || (bytes & 15) || (reinterpret_cast<uintptr_t>(buf) & 15))
+        return fail(DARB_E_INVALID, "buf/sink NULL or bytes/alignment not a multiple of 16");
+    return launched(launch_stream_read(buf, bytes, sink, static_cast<hipStream_t>(stream)),
+                    "stream read launch");
+}
+
+int darb_stream_copy(void *dst, const void *src, int64_t bytes, void *stream) {
+    clear_error();
+    if (!dst || !src || bytes <= 0 || (bytes & 15) || (reinterpret_cast<uintptr_t>(dst) & 15) ||
+        (reinterpret_cast<uintptr_t>(src) & 15))
+        return fail(DARB_E_INVALID, "dst/src NULL or bytes/alignment not a multiple of 16");
+    return launched(launch_stream_copy(dst, src, bytes, static_cast<hipStream_t>(stream)),
+                    "stream copy launch");
+}
+
+}  // extern "C"

@@ -1,0 +1,77 @@
+// Internal declarations shared by the host code and the kernel launchers of
+// the DARB library.  Not part of the public ABI (include/darb.h is).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include "darb.h"
+
+namespace darb {
+
+constexpr int kMaxBins = 8;      // block sizes 1, 2, ..., 128
+constexpr int kMaxLog2B = 7;
+constexpr int kWave = 64;        // CDNA wavefront width
+
+// The block-size groups, passed to kernels by value.
+struct BinTable {
+    int32_t nbins;
+    int32_t log2b[kMaxBins];
+    int64_t first_row[kMaxBins];   // storage-order index of the group's first row
+    int64_t rows[kMaxBins];
+    int64_t first_elem[kMaxBins];  // slot of the group's first retained weight
+    int64_t nblk[kMaxBins];        // retained weights per row
+};
+
+// Per-group work split of the product kernels: one wave handles `rows_per_wave`
+// rows of one group with `lanes_per_row` lanes each, `tiles` waves per group.
+struct ProductSchedule {
+    int32_t nbins;
+    int32_t vec[kMaxBins];            // elements per vector load (1 = scalar path)
+    int32_t lanes_per_row[kMaxBins];  // power of two, divides 64
+    int64_t tile_begin[kMaxBins + 1]; // prefix of wave tiles over groups
+    int64_t col_slabs;                // batch-column slabs (products with B > 1)
+};
+
+}  // namespace darb
+
+struct darb_plan {
+    int64_t M = 0, N = 0, nnz = 0;
+    int mode = 0, b_min = 1, b_max = 1;
+    std::vector<uint8_t> log2b;
+    std::vector<int64_t> row_start;
+    std::vector<int32_t> perm;
+    darb::BinTable bins{};
+    int64_t workspace_bytes = 0;
+    // device side
+    int32_t *d_perm = nullptr;
+    int device = -1;
+};
+
+namespace darb {
+
+// error reporting (thread-local detail string)
+int fail(int code, const std::string &detail);
+void clear_error();
+
+// kernel launchers (return hipError_t of the launch)
+hipError_t launch_encode(const darb_plan &p, int wdtype, const void *W, int64_t ldw,
+                         void *values, uint8_t *offsets, hipStream_t s);
+hipError_t launch_decode(const darb_plan &p, int wdtype, const void *values,
+                         const uint8_t *offsets, void *W_out, int64_t ldw, hipStream_t s);
+hipError_t launch_spmv(const darb_plan &p, int wdtype, const void *values,
+                       const uint8_t *offsets, int xdtype, const void *x, float *y,
+                       hipStream_t s);
+hipError_t launch_spmm(const darb_plan &p, int wdtype, const void *values,
+                       const uint8_t *offsets, int xdtype, int64_t B, const void *X,
+                       int64_t ldx, float *Y, int64_t ldy, hipStream_t s);
+hipError_t launch_lstm_cell(int64_t H, int64_t batch, const float *G, const float *U,
+                            int64_t ldu, float *h, float *c, float *h_seq, int64_t ld_seq,
+                            hipStream_t s);
+hipError_t launch_stream_read(const void *buf, int64_t bytes, float *sink, hipStream_t s);
+hipError_t launch_stream_copy(void *dst, const void *src, int64_t bytes, hipStream_t s);
+
+}  // namespace darb

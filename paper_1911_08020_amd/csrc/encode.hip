@@ -1,0 +1,187 @@
+// BMWM encode on gfx950 (section 3.1 block-max weight masking, with the
+// per-row block size of section 3.2).
+//
+// Work unit: one wavefront handles one chunk of CHUNK consecutive columns of one
+// row.  CHUNK is a multiple of every block size (<= 128), so no block straddles
+// two waves.  Each lane loads VEC consecutive elements per 16-byte load, UNROLL
+// loads in flight per lane, all issued before any compare (the kernel is bound
+// by the HBM stream of the dense W).
+//
+// Selection: the magnitude key of an element is its bit pattern with the sign
+// cleared.  Within a lane the VEC elements are scanned in column order with a
+// strict ">" (earliest wins ties).  A block wider than VEC spans b/VEC
+// consecutive lanes; their candidates are packed as
+//     (magnitude << 8) | ((127 - j) << 1) | sign,     j = column within the block,
+// so one unsigned max over an xor butterfly picks the largest magnitude and,
+// among equal magnitudes, the smallest j; the sign travels along to rebuild the
+// value.  Columns past N (tail block) load as +0.0 with their own j, so they can
+// never beat a real column of the same block.
+#include "darb_internal.h"
+
+namespace darb {
+namespace {
+
+constexpr int kEncodeThreads = 256;
+constexpr int kEncodeWaves = kEncodeThreads / kWave;
+
+template <typename Bits> struct EncodeTraits;
+template <> struct EncodeTraits<uint32_t> {
+    static constexpr int VEC = 4;          // 16 bytes
+    static constexpr int UNROLL = 4;       // 64 B in flight per lane
+    static constexpr uint32_t MAG = 0x7FFFFFFFu;
+    static constexpr int SIGN_SHIFT = 31;
+    using Key = uint64_t;
+};
+template <> struct EncodeTraits<uint16_t> {
+    static constexpr int VEC = 8;          // 16 bytes
+    static constexpr int UNROLL = 4;
+    static constexpr uint32_t MAG = 0x7FFFu;
+    static constexpr int SIGN_SHIFT = 15;
+    using Key = uint32_t;
+};
+
+template <typename Bits>
+__device__ __forceinline__ typename EncodeTraits<Bits>::Key pack_key(Bits v, int j) {
+    using Tr = EncodeTraits<Bits>;
+    using Key = typename Tr::Key;
+    const uint32_t mag = uint32_t(v) & Tr::MAG;
+    const uint32_t sgn = uint32_t(v) >> Tr::SIGN_SHIFT;
+    return (Key(mag) << 8) | Key((127 - j) << 1) | Key(sgn);
+}
+
+template <typename Bits>
+__device__ __forceinline__ void unpack_key(typename EncodeTraits<Bits>::Key k, Bits &v, int &j) {
+    using Tr = EncodeTraits<Bits>;
+    const uint32_t mag = uint32_t(k >> 8);
+    const uint32_t sgn = uint32_t(k) & 1u;
+    v = Bits(mag | (sgn << Tr::SIGN_SHIFT));
+    j = 127 - int((uint32_t(k) >> 1) & 127u);
+}
+
+__device__ __forceinline__ uint64_t shfl_xor_key(uint64_t k, int m) {
+    const uint32_t lo = __shfl_xor(uint32_t(k), m, kWave);
+    const uint32_t hi = __shfl_xor(uint32_t(k >> 32), m, kWave);
+    return (uint64_t(hi) << 32) | lo;
+}
+__device__ __forceinline__ uint32_t shfl_xor_key(uint32_t k, int m) {
+    return __shfl_xor(k, m, kWave);
+}
+
+template <typename Bits, int VEC> struct alignas(16) Vec { Bits e[VEC]; };
+
+template <typename Bits, bool ALIGNED>
+__global__ __launch_bounds__(kEncodeThreads) void encode_kernel(
+    const Bits *__restrict__ W, int64_t ldw, int64_t N, int64_t M,
+    const int32_t *__restrict__ perm, BinTable bins, int64_t chunks_per_row,
+    Bits *__restrict__ values, uint8_t *__restrict__ offsets) {
+    using Tr = EncodeTraits<Bits>;
+    constexpr int VEC = Tr::VEC;
+    constexpr int UNROLL = Tr::UNROLL;
+    constexpr int64_t CHUNK = int64_t(kWave) * VEC * UNROLL;
+    using Key = typename Tr::Key;
+
+    const int lane = threadIdx.x & (kWave - 1);
+    const int64_t task = int64_t(blockIdx.x) * kEncodeWaves + (threadIdx.x / kWave);
+    const int64_t i = task / chunks_per_row;          // storage-order row
+    if (i >= M) return;                               // wave-uniform, no barrier below
+    const int64_t q = task - i * chunks_per_row;
+
+    int g = 0;
+    while (g + 1 < bins.nbins && i >= bins.first_row[g + 1]) ++g;
+    const int lb = bins.log2b[g];
+    const int64_t nblk = bins.nblk[g];
+    const int64_t out0 = bins.first_elem[g] + (i - bins.first_row[g]) * nblk;
+    const Bits *row = W + int64_t(perm[i]) * ldw;
+
+    // issue every load of this lane first
+    Vec<Bits, VEC> v[UNROLL];
+#pragma unroll
+    for (int u = 0; u < UNROLL; ++u) {
+        const int64_t c0 = q * CHUNK + int64_t(u) * (kWave * VEC) + int64_t(lane) * VEC;
+        if (ALIGNED && c0 + VEC <= N) {
+            v[u] = *reinterpret_cast<const Vec<Bits, VEC> *>(row + c0);
+        } else {
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) v[u].e[e] = (c0 + e < N) ? row[c0 + e] : Bits(0);
+        }
+    }
+
+    const int b = 1 << lb;
+#pragma unroll
+    for (int u = 0; u < UNROLL; ++u) {
+        const int64_t c0 = q * CHUNK + int64_t(u) * (kWave * VEC) + int64_t(lane) * VEC;
+        if (b <= VEC) {
+            // the lane holds VEC / b whole blocks
+            for (int s = 0; s < VEC; s += b) {
+                const int64_t k = (c0 + s) >> lb;
+                if (k >= nblk) break;
+                int best = 0;
+                uint32_t best_mag = uint32_t(v[u].e[s]) & Tr::MAG;
+                for (int j = 1; j < b; ++j) {
+                    const uint32_t mag = uint32_t(v[u].e[s + j]) & Tr::MAG;
+                    if (mag > best_mag) { best_mag = mag; best = j; }
+                }
+                values[out0 + k] = v[u].e[s + best];
+                offsets[out0 + k] = uint8_t(best);
+            }
+        } else {
+            // in-lane candidate, then a butterfly over the b / VEC lanes of the block
+            const int j0 = int(c0 & (b - 1));
+            int best = 0;
+            uint32_t best_mag = uint32_t(v[u].e[0]) & Tr::MAG;
+#pragma unroll
+            for (int e = 1; e < VEC; ++e) {
+                const uint32_t mag = uint32_t(v[u].e[e]) & Tr::MAG;
+                if (mag > best_mag) { best_mag = mag; best = e; }
+            }
+            Key key = pack_key<Bits>(v[u].e[best], j0 + best);
+            const int group = b / VEC;                 // 2 .. 32 lanes
+            for (int m = 1; m < group; m <<= 1) {
+                const Key other = shfl_xor_key(key, m);
+                key = other > key ? other : key;
+            }
+            const int64_t k = c0 >> lb;
+            if ((lane & (group - 1)) == 0 && k < nblk) {
+                Bits val;
+                int j;
+                unpack_key<Bits>(key, val, j);
+                values[out0 + k] = val;
+                offsets[out0 + k] = uint8_t(j);
+            }
+        }
+    }
+}
+
+template <typename Bits>
+hipError_t launch_encode_t(const darb_plan &p, const void *W, int64_t ldw, void *values,
+                           uint8_t *offsets, hipStream_t s) {
+    using Tr = EncodeTraits<Bits>;
+    constexpr int64_t CHUNK = int64_t(kWave) * Tr::VEC * Tr::UNROLL;
+    const int64_t chunks = (p.N + CHUNK - 1) / CHUNK;
+    const int64_t tasks = p.M * chunks;
+    const int64_t blocks = (tasks + kEncodeWaves - 1) / kEncodeWaves;
+    if (blocks > 0x7FFFFFFF) return hipErrorInvalidConfiguration;
+    const bool aligned = (reinterpret_cast<uintptr_t>(W) % 16 == 0) &&
+                         ((ldw * int64_t(sizeof(Bits))) % 16 == 0);
+    const Bits *w = static_cast<const Bits *>(W);
+    Bits *vals = static_cast<Bits *>(values);
+    if (aligned)
+        hipLaunchKernelGGL((encode_kernel<Bits, true>), dim3(unsigned(blocks)),
+                           dim3(kEncodeThreads), 0, s, w, ldw, p.N, p.M, p.d_perm, p.bins,
+                           chunks, vals, offsets);
+    else
+        hipLaunchKernelGGL((encode_kernel<Bits, false>), dim3(unsigned(blocks)),
+                           dim3(kEncodeThreads), 0, s, w, ldw, p.N, p.M, p.d_perm, p.bins,
+                           chunks, vals, offsets);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_encode(const darb_plan &p, int wdtype, const void *W, int64_t ldw,
+                         void *values, uint8_t *offsets, hipStream_t s) {
+    if (wdtype == DARB_F32) return launch_encode_t<uint32_t>(p, W, ldw, values, offsets, s);
+    return launch_encode_t<uint16_t>(p, W, ldw, values, offsets, s);
+}
+
+}  // namespace darb

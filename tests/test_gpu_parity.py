@@ -1,0 +1,294 @@
+"""GPU parity: the HIP kernels against the CPU oracle, through the C ABI.
+
+Encode, decode and the plan are compared bit for bit.  Products are compared
+per output with err = |y - y64| / sum_k |v_k x_k| (the scale of a dot
+product's rounding error; an output whose scale is 0 must be exactly 0),
+bounded by 1e-5 for fp32 weights and 2e-3 for fp16 weights.
+"""
+import functools
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+import workloads
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+TOL = {np.dtype(np.float32): 1e-5, np.dtype(np.float16): 2e-3}
+_TDT = {np.dtype(np.float32): torch.float32, np.dtype(np.float16): torch.float16}
+_UT = {np.dtype(np.float32): np.uint32, np.dtype(np.float16): np.uint16}
+
+
+def say(*a):
+    print(*a, flush=True, file=sys.stderr)
+
+
+@pytest.fixture(scope="module")
+def darb():
+    assert torch.cuda.is_available(), "GPU tests need a visible MI355X"
+    import paper_1911_08020_amd as d
+    return d
+
+
+def dev(a: np.ndarray):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def host(t) -> np.ndarray:
+    torch.cuda.synchronize()
+    return t.cpu().numpy()
+
+
+def check_product(Y, vals, offs, lay, X, wdtype, label=""):
+    ref = oracle.spmm(vals, offs, lay, X)
+    scale = oracle.spmm_absdot(vals, offs, lay, X)
+    Y = np.asarray(Y, dtype=np.float64).reshape(ref.shape)
+    err = np.abs(Y - ref)
+    zero = scale == 0
+    assert np.all(Y[zero] == 0.0), f"{label}: nonzero output where every term is 0"
+    rel = err[~zero] / scale[~zero]
+    worst = float(rel.max()) if rel.size else 0.0
+    say(f"  {label}: max rel err {worst:.3e} (tol {TOL[np.dtype(wdtype)]:.0e})")
+    assert worst <= TOL[np.dtype(wdtype)], label
+
+
+def encode_both(darb, W, d, D, mode, bmin, bmax, W_dev=None):
+    """Plan + encode on the GPU and in the oracle; assert bit-exact equality."""
+    M, N = W.shape
+    plan = darb.Plan(M, N, d, D, mode, bmin, bmax).upload()
+    lay = oracle.plan(N, d, D, mode, bmin, bmax)
+    log2b, row_start, perm = plan.export()
+    assert np.array_equal(log2b, lay.log2b) and np.array_equal(perm, lay.perm)
+    vals_ref, offs_ref = oracle.encode(W, lay)
+    Wd = dev(W) if W_dev is None else W_dev
+    v, o = plan.encode(Wd)
+    v, o = host(v), host(o)
+    ut = _UT[W.dtype]
+    assert np.array_equal(o, offs_ref), "offsets differ"
+    assert np.array_equal(v.view(ut), vals_ref.view(ut)), "values differ"
+    return plan, lay, vals_ref, offs_ref
+
+
+# --------------------------------------------------------------------------------
+# encode
+# --------------------------------------------------------------------------------
+
+@pytest.mark.parametrize("dtype", [np.float32, np.float16])
+@pytest.mark.parametrize("shape", [(1, 1), (3, 7), (37, 203), (130, 1030), (64, 4100), (9, 2049)])
+def test_encode_small_shapes_ties_and_tails(darb, dtype, shape):
+    M, N = shape
+    say(f"encode small {shape} {np.dtype(dtype).name}")
+    rng = np.random.default_rng(M * 1000 + N)
+    W = (rng.integers(-4, 5, size=(M, N)) * 0.5).astype(dtype)      # many ties
+    W[rng.random((M, N)) < 0.05] = -0.0
+    counts = rng.integers(0, N + 1, size=M)
+    for mode in (0, 1):
+        encode_both(darb, W, counts / float(N), float(counts.mean() / N), mode, 1, 128)
+
+
+@pytest.mark.parametrize("dtype", [np.float32, np.float16])
+def test_encode_special_values(darb, dtype):
+    say(f"encode special values {np.dtype(dtype).name}")
+    rng = np.random.default_rng(5)
+    M, N = 48, 517
+    W = rng.standard_normal((M, N)).astype(dtype)
+    specials = np.array([np.inf, -np.inf, 0.0, -0.0, np.finfo(dtype).tiny,
+                         np.finfo(dtype).max, -np.finfo(dtype).max], dtype=dtype)
+    sel = rng.random((M, N)) < 0.1
+    W[sel] = rng.choice(specials, size=int(sel.sum()))
+    W[::5] *= dtype(1e-30) if dtype == np.float32 else dtype(0)     # denormals / zeros
+    W[3, 10] = np.nan
+    W[7, 100:140] = np.nan
+    d = np.full(M, 0.01)
+    d[::3] = 0.3
+    encode_both(darb, W, d, 0.1, 0, 1, 128)
+
+
+def test_encode_strided_and_misaligned_rows(darb):
+    say("encode strided W (ldw > N, rows not 16-byte aligned)")
+    rng = np.random.default_rng(6)
+    M, N = 70, 999
+    big = rng.standard_normal((M, N + 3)).astype(np.float32)
+    W = big[:, :N]
+    d = rng.integers(0, N, size=M) / N
+    plan = darb.Plan(M, N, d, 0.05, 0, 2, 64).upload()
+    lay = oracle.plan(N, d, 0.05, 0, 2, 64)
+    vr, orf = oracle.encode(np.ascontiguousarray(W), lay)
+    Wd = dev(big)[:, :N]
+    assert Wd.stride(0) == N + 3
+    v, o = plan.encode(Wd)
+    assert np.array_equal(host(o), orf)
+    assert np.array_equal(host(v).view(np.uint32), vr.view(np.uint32))
+
+
+@functools.lru_cache(maxsize=None)
+def _config(name):
+    return workloads.make_config(name, seed=0)
+
+
+@pytest.mark.parametrize("name", ["lstm_tiny", "lstm_1024", "gru_1536", "fc_9216"])
+def test_config_encode_decode_spmv_spmm(darb, name):
+    cfg, mi, x, X = _config(name)
+    say(f"config {name}: encode {cfg.M}x{cfg.N} {cfg.wdtype}")
+    plan, lay, vals, offs = encode_both(darb, mi.W, mi.row_density, mi.matrix_density, 0,
+                                        cfg.b_min, cfg.b_max)
+    vd, od = dev(vals), dev(offs)
+    say(f"config {name}: decode")
+    Wm = host(plan.decode(vd, od))
+    ut = _UT[mi.W.dtype]
+    assert np.array_equal(Wm.view(ut), oracle.decode(vals, offs, lay).view(ut))
+    say(f"config {name}: spmv")
+    y = host(plan.spmv(vd, od, dev(x)))
+    check_product(y, vals, offs, lay, x, mi.W.dtype, f"{name} spmv")
+    say(f"config {name}: spmm B={X.shape[1]}")
+    Y = host(plan.spmm(vd, od, dev(X)))
+    check_product(Y, vals, offs, lay, X, mi.W.dtype, f"{name} spmm B={X.shape[1]}")
+
+
+def test_fc_spmm_and_spmv_deterministic(darb):
+    cfg, mi, x, X = _config("fc_9216")
+    say("fc_9216: repeat products, bitwise equal")
+    plan = darb.Plan(cfg.M, cfg.N, mi.row_density, mi.matrix_density, 0, cfg.b_min,
+                     cfg.b_max).upload()
+    v, o = plan.encode(dev(mi.W))
+    xd, Xd = dev(x), dev(X)
+    y1, y2 = host(plan.spmv(v, o, xd)), host(plan.spmv(v, o, xd))
+    Y1, Y2 = host(plan.spmm(v, o, Xd)), host(plan.spmm(v, o, Xd))
+    assert np.array_equal(y1.view(np.uint32), y2.view(np.uint32))
+    assert np.array_equal(Y1.view(np.uint32), Y2.view(np.uint32))
+
+
+# --------------------------------------------------------------------------------
+# products: batch sizes, strides, dtypes, degenerate layouts
+# --------------------------------------------------------------------------------
+
+@pytest.mark.parametrize("B", [1, 2, 3, 16, 33, 64, 65, 130])
+@pytest.mark.parametrize("wx", [("f32", "f32"), ("f16", "f16"), ("f16", "f32")])
+def test_spmm_batches(darb, B, wx):
+    wdt, xdt = {"f32": np.float32, "f16": np.float16}[wx[0]], {"f32": np.float32,
+                                                              "f16": np.float16}[wx[1]]
+    say(f"spmm B={B} w={wx[0]} x={wx[1]}")
+    rng = np.random.default_rng(B)
+    M, N = 300, 777
+    W = rng.standard_normal((M, N)).astype(wdt)
+    d = rng.integers(0, N // 3, size=M) / N
+    plan, lay, vals, offs = encode_both(darb, W, d, 0.1, 0, 1, 128)
+    X = rng.standard_normal((N, B)).astype(xdt)
+    # X and Y with leading dimensions larger than B
+    Xbig = np.zeros((N, B + 5), dtype=xdt)
+    Xbig[:, :B] = X
+    Xd = dev(Xbig)[:, :B]
+    Yd = torch.full((M, B + 3), float("nan"), device="cuda")[:, :B]
+    plan.spmm(dev(vals), dev(offs), Xd, Y=Yd)
+    check_product(host(Yd), vals, offs, lay, X, wdt, f"B={B}")
+    if B == 1:
+        y = plan.spmv(dev(vals), dev(offs), dev(X[:, 0].copy()))
+        check_product(host(y), vals, offs, lay, X[:, 0], wdt, "spmv")
+
+
+@pytest.mark.parametrize("case", ["all_empty_rows", "b_one", "b_wider_than_row", "one_row",
+                                  "wide_no_lds", "odd_nblk", "fp16_odd"])
+def test_product_edge_cases(darb, case):
+    say(f"edge case {case}")
+    rng = np.random.default_rng(len(case))
+    wdt = np.float16 if case == "fp16_odd" else np.float32
+    M, N, bmin, bmax = 50, 300, 1, 128
+    d = None
+    if case == "all_empty_rows":
+        d = np.zeros(M)
+    elif case == "b_one":
+        d, bmax = np.ones(M), 1
+    elif case == "b_wider_than_row":
+        M, N = 40, 50
+        d = np.zeros(M)
+    elif case == "one_row":
+        M, N = 1, 1000
+    elif case == "wide_no_lds":
+        M, N = 64, 20000                # x does not fit the LDS staging buffer
+    elif case == "odd_nblk":
+        M, N = 33, 333
+    elif case == "fp16_odd":
+        M, N = 29, 1001
+    W = rng.standard_normal((M, N)).astype(wdt)
+    if d is None:
+        d = rng.integers(0, N + 1, size=M) / N
+    plan, lay, vals, offs = encode_both(darb, W, d, float(np.mean(d)), 0, bmin, bmax)
+    x = rng.standard_normal(N).astype(wdt if wdt == np.float16 else np.float32)
+    y = host(plan.spmv(dev(vals), dev(offs), dev(x)))
+    check_product(y, vals, offs, lay, x, wdt, case + " spmv")
+    X = rng.standard_normal((N, 5)).astype(np.float32)
+    Y = host(plan.spmm(dev(vals), dev(offs), dev(X)))
+    check_product(Y, vals, offs, lay, X, wdt, case + " spmm")
+
+
+def test_spmv_misaligned_values_uses_scalar_path(darb):
+    say("spmv with values/offsets starting at an odd element")
+    rng = np.random.default_rng(12)
+    M, N = 77, 512
+    W = rng.standard_normal((M, N)).astype(np.float32)
+    d = rng.integers(0, N, size=M) / N
+    plan, lay, vals, offs = encode_both(darb, W, d, 0.1, 0, 4, 64)
+    vbig = dev(np.concatenate([[0.0], vals]).astype(np.float32))[1:]
+    obig = dev(np.concatenate([[0], offs]).astype(np.uint8))[1:]
+    x = rng.standard_normal(N).astype(np.float32)
+    y = host(plan.spmv(vbig, obig, dev(x)))
+    check_product(y, vals, offs, lay, x, np.float32, "misaligned spmv")
+
+
+def test_unit_vector_returns_masked_column(darb):
+    say("spmv(e_c) == column c of the masked matrix")
+    rng = np.random.default_rng(13)
+    M, N = 200, 640
+    W = rng.standard_normal((M, N)).astype(np.float32)
+    d = rng.integers(0, N, size=M) / N
+    plan, lay, vals, offs = encode_both(darb, W, d, 0.1, 0, 1, 128)
+    Wm = oracle.decode(vals, offs, lay)
+    X = np.zeros((N, 8), dtype=np.float32)
+    cols = [0, 1, 63, 64, 300, 511, 638, 639]
+    for j, c in enumerate(cols):
+        X[c, j] = 1.0
+    Y = host(plan.spmm(dev(vals), dev(offs), dev(X)))
+    assert np.array_equal(Y, Wm[:, cols])
+
+
+# --------------------------------------------------------------------------------
+# the recurrent workload
+# --------------------------------------------------------------------------------
+
+def _lstm_case(darb, hidden, seq_len, batch, layers, seed):
+    cfg, mats, xs, shp = workloads.make_lstm_inputs(seed=seed, seq_len=seq_len, batch=batch,
+                                                    hidden=hidden, layers=layers)
+    H, T, Bt = shp["hidden"], shp["seq_len"], shp["batch"]
+    masked, dev_layers = [], []
+    for (wih, whh) in mats:
+        pair_m, pair_d = [], []
+        for mi in (wih, whh):
+            plan, lay, vals, offs = encode_both(darb, mi.W, mi.row_density, mi.matrix_density,
+                                                0, cfg.b_min, cfg.b_max)
+            pair_m.append(oracle.decode(vals, offs, lay).astype(np.float64))
+            pair_d.append((plan, dev(vals), dev(offs)))
+        masked.append(tuple(pair_m))
+        dev_layers.append(tuple(pair_d))
+    ref, finals = oracle.lstm_forward(masked, xs, H, T, Bt)
+    inp = dev(xs)
+    for (wih, whh) in dev_layers:
+        inp, h, c = darb.lstm_layer(wih, whh, inp, H, T, Bt)
+    out = host(inp)
+    err = float(np.abs(out - ref).max())
+    say(f"  lstm H={H} T={T} B={Bt}: max abs err {err:.3e}")
+    assert err <= 2e-3
+    assert np.abs(host(c) - finals[-1][1]).max() <= 2e-3
+
+
+def test_lstm_small(darb):
+    say("lstm small")
+    _lstm_case(darb, hidden=64, seq_len=7, batch=3, layers=2, seed=1)
+
+
+def test_lstm_full_workload(darb):
+    say("lstm 2 layers, hidden 1024, T=200, batch 32")
+    _lstm_case(darb, hidden=None, seq_len=None, batch=None, layers=None, seed=0)
