@@ -57,6 +57,10 @@ class _Info(ctypes.Structure):
 
 
 def _load_library():
+    # torch carries its own HIP runtime (same soname as /opt/rocm's).  Loading it
+    # first makes libdarb.so bind to that one, so the process has a single HIP
+    # runtime and the library sees the devices and streams torch uses.
+    import torch  # noqa: F401
     if not os.path.exists(LIB_PATH):
         raise ImportError(
             f"DARB HIP library not built: {LIB_PATH} is missing. "
@@ -191,9 +195,10 @@ class Plan:
     def upload(self, device=None, stream=None):
         torch = _torch()
         dev = torch.device("cuda") if device is None else torch.device(device)
-        ws = torch.empty(self.workspace_bytes, dtype=torch.uint8, device=dev)
-        _check(_lib.darb_plan_upload(self._h, _ptr(ws), self.workspace_bytes,
-                                     _stream_ptr(stream)), "darb_plan_upload")
+        with torch.cuda.device(dev):
+            ws = torch.empty(self.workspace_bytes, dtype=torch.uint8, device=dev)
+            _check(_lib.darb_plan_upload(self._h, _ptr(ws), self.workspace_bytes,
+                                         _stream_ptr(stream)), "darb_plan_upload")
         self.workspace = ws
         return self
 

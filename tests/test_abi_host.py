@@ -154,3 +154,11 @@ def test_binding_rejects_host_tensors():
     p = darb.Plan(4, 16, np.full(4, 0.25), 0.25, 0, 1, 16)
     with pytest.raises(ValueError):
         p.encode(torch.zeros(4, 16))
+
+
+def test_single_hip_runtime_in_process():
+    # libdarb.so must share torch's HIP runtime, not load a second copy
+    import torch  # noqa: F401
+    maps = open("/proc/self/maps").read()
+    paths = {ln.split()[-1] for ln in maps.splitlines() if "libamdhip64" in ln}
+    assert len(paths) == 1, paths
