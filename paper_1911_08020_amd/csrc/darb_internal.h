@@ -26,14 +26,17 @@ struct BinTable {
     int64_t nblk[kMaxBins];        // retained weights per row
 };
 
-// Per-group work split of the product kernels: one wave handles `rows_per_wave`
-// rows of one group with `lanes_per_row` lanes each, `tiles` waves per group.
+// Per-launch work split of the product kernels.  Every workgroup belongs to one
+// block-size group g: blocks [block_begin[g], block_begin[g+1]).
 struct ProductSchedule {
     int32_t nbins;
-    int32_t vec[kMaxBins];            // elements per vector load (1 = scalar path)
-    int32_t lanes_per_row[kMaxBins];  // power of two, divides 64
-    int64_t tile_begin[kMaxBins + 1]; // prefix of wave tiles over groups
-    int64_t col_slabs;                // batch-column slabs (products with B > 1)
+    int32_t block_begin[kMaxBins + 1];
+    int32_t log2_lanes[kMaxBins];     // log2 of the lanes that share one row
+    int32_t vec[kMaxBins];            // SpMV: elements per vector load (1 = scalar path)
+    int32_t ksplit[kMaxBins];         // SpMM: waves that split one row group's weights
+    int32_t log2_kchunk[kMaxBins];    // SpMM: weights per row staged in LDS per round
+    int32_t col_slabs;                // SpMM: batch-column slabs per row block
+    int32_t stage_loads;              // SpMV: 16-byte loads per thread to stage x
 };
 
 }  // namespace darb

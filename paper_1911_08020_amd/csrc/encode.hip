@@ -69,28 +69,107 @@ __device__ __forceinline__ uint32_t shfl_xor_key(uint32_t k, int m) {
 
 template <typename Bits, int VEC> struct alignas(16) Vec { Bits e[VEC]; };
 
+// Blocks of b = 2^LB <= VEC elements: the lane's vector holds VEC / b whole blocks.
+template <typename Bits, int VEC, int LB>
+__device__ __forceinline__ void small_blocks(const Vec<Bits, VEC> &v, int64_t c0, int64_t nblk,
+                                             Bits *__restrict__ values,
+                                             uint8_t *__restrict__ offsets) {
+    using Tr = EncodeTraits<Bits>;
+    constexpr int b = 1 << LB;
+    if constexpr (b <= VEC) {
+#pragma unroll
+        for (int s = 0; s < VEC; s += b) {
+            const int64_t k = (c0 + s) >> LB;
+            Bits best_bits = v.e[s];
+            uint32_t best_mag = uint32_t(v.e[s]) & Tr::MAG;
+            int best = 0;
+#pragma unroll
+            for (int j = 1; j < b; ++j) {
+                const uint32_t mag = uint32_t(v.e[s + j]) & Tr::MAG;
+                const bool take = mag > best_mag;
+                best_mag = take ? mag : best_mag;
+                best_bits = take ? v.e[s + j] : best_bits;
+                best = take ? j : best;
+            }
+            if (k < nblk) {
+                values[k] = best_bits;
+                offsets[k] = uint8_t(best);
+            }
+        }
+    }
+}
+
+// Blocks wider than VEC: in-lane candidate, then an xor butterfly over the
+// b / VEC consecutive lanes that hold the block.
+template <typename Bits, int VEC>
+__device__ __forceinline__ void wide_block(const Vec<Bits, VEC> &v, int64_t c0, int lb, int lane,
+                                           int64_t nblk, Bits *__restrict__ values,
+                                           uint8_t *__restrict__ offsets) {
+    using Tr = EncodeTraits<Bits>;
+    using Key = typename Tr::Key;
+    const int b = 1 << lb;
+    const int j0 = int(c0 & (b - 1));
+    Bits best_bits = v.e[0];
+    uint32_t best_mag = uint32_t(v.e[0]) & Tr::MAG;
+    int best = 0;
+#pragma unroll
+    for (int e = 1; e < VEC; ++e) {
+        const uint32_t mag = uint32_t(v.e[e]) & Tr::MAG;
+        const bool take = mag > best_mag;
+        best_mag = take ? mag : best_mag;
+        best_bits = take ? v.e[e] : best_bits;
+        best = take ? e : best;
+    }
+    Key key = pack_key<Bits>(best_bits, j0 + best);
+    const int group = b / VEC;                         // 2 .. 32 lanes
+    for (int m = 1; m < group; m <<= 1) {
+        const Key other = shfl_xor_key(key, m);
+        key = other > key ? other : key;
+    }
+    const int64_t k = c0 >> lb;
+    if ((lane & (group - 1)) == 0 && k < nblk) {
+        Bits val;
+        int j;
+        unpack_key<Bits>(key, val, j);
+        values[k] = val;
+        offsets[k] = uint8_t(j);
+    }
+}
+
 template <typename Bits, bool ALIGNED>
 __global__ __launch_bounds__(kEncodeThreads) void encode_kernel(
-    const Bits *__restrict__ W, int64_t ldw, int64_t N, int64_t M,
-    const int32_t *__restrict__ perm, BinTable bins, int64_t chunks_per_row,
-    Bits *__restrict__ values, uint8_t *__restrict__ offsets) {
+    const Bits *__restrict__ W, int64_t ldw, int64_t N, const int32_t *__restrict__ perm,
+    BinTable bins, int64_t chunks_per_row, int cgroups, Bits *__restrict__ values,
+    uint8_t *__restrict__ offsets) {
     using Tr = EncodeTraits<Bits>;
     constexpr int VEC = Tr::VEC;
     constexpr int UNROLL = Tr::UNROLL;
     constexpr int64_t CHUNK = int64_t(kWave) * VEC * UNROLL;
-    using Key = typename Tr::Key;
 
-    const int lane = threadIdx.x & (kWave - 1);
-    const int64_t task = int64_t(blockIdx.x) * kEncodeWaves + (threadIdx.x / kWave);
-    const int64_t i = task / chunks_per_row;          // storage-order row
-    if (i >= M) return;                               // wave-uniform, no barrier below
-    const int64_t q = task - i * chunks_per_row;
+    // workgroup -> (storage-order row i, group of kEncodeWaves chunks); all uniform
+    const int i = int(blockIdx.x) / cgroups;
+    const int cg = int(blockIdx.x) - i * cgroups;
+    const int wave = __builtin_amdgcn_readfirstlane(int(threadIdx.x) / kWave);
+    const int lane = int(threadIdx.x) & (kWave - 1);
+    const int64_t q = int64_t(cg) * kEncodeWaves + wave;
+    if (q >= chunks_per_row) return;                  // wave-uniform, no barrier below
 
     int g = 0;
-    while (g + 1 < bins.nbins && i >= bins.first_row[g + 1]) ++g;
-    const int lb = bins.log2b[g];
-    const int64_t nblk = bins.nblk[g];
-    const int64_t out0 = bins.first_elem[g] + (i - bins.first_row[g]) * nblk;
+#pragma unroll
+    for (int b = 1; b < kMaxBins; ++b)
+        if (b < bins.nbins && i >= bins.first_row[b]) g = b;
+    int lb = bins.log2b[0];
+    int64_t nblk = bins.nblk[0], first_row = bins.first_row[0], first_elem = bins.first_elem[0];
+#pragma unroll
+    for (int b = 1; b < kMaxBins; ++b) {
+        if (b == g) {
+            lb = bins.log2b[b];
+            nblk = bins.nblk[b];
+            first_row = bins.first_row[b];
+            first_elem = bins.first_elem[b];
+        }
+    }
+    const int64_t out0 = first_elem + (i - first_row) * nblk;
     const Bits *row = W + int64_t(perm[i]) * ldw;
 
     // issue every load of this lane first
@@ -99,55 +178,32 @@ __global__ __launch_bounds__(kEncodeThreads) void encode_kernel(
     for (int u = 0; u < UNROLL; ++u) {
         const int64_t c0 = q * CHUNK + int64_t(u) * (kWave * VEC) + int64_t(lane) * VEC;
         if (ALIGNED && c0 + VEC <= N) {
-            v[u] = *reinterpret_cast<const Vec<Bits, VEC> *>(row + c0);
+            typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+            const u32x4 t = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(row + c0));
+            v[u] = __builtin_bit_cast(Vec<Bits, VEC>, t);
         } else {
 #pragma unroll
             for (int e = 0; e < VEC; ++e) v[u].e[e] = (c0 + e < N) ? row[c0 + e] : Bits(0);
         }
     }
 
-    const int b = 1 << lb;
 #pragma unroll
     for (int u = 0; u < UNROLL; ++u) {
         const int64_t c0 = q * CHUNK + int64_t(u) * (kWave * VEC) + int64_t(lane) * VEC;
-        if (b <= VEC) {
-            // the lane holds VEC / b whole blocks
-            for (int s = 0; s < VEC; s += b) {
-                const int64_t k = (c0 + s) >> lb;
-                if (k >= nblk) break;
-                int best = 0;
-                uint32_t best_mag = uint32_t(v[u].e[s]) & Tr::MAG;
-                for (int j = 1; j < b; ++j) {
-                    const uint32_t mag = uint32_t(v[u].e[s + j]) & Tr::MAG;
-                    if (mag > best_mag) { best_mag = mag; best = j; }
+        // block sizes up to VEC: the lane holds whole blocks (compile-time indices only,
+        // so the loaded vector stays in registers)
+        switch (lb) {
+            case 0: small_blocks<Bits, VEC, 0>(v[u], c0, nblk, values + out0, offsets + out0); break;
+            case 1: small_blocks<Bits, VEC, 1>(v[u], c0, nblk, values + out0, offsets + out0); break;
+            case 2: small_blocks<Bits, VEC, 2>(v[u], c0, nblk, values + out0, offsets + out0); break;
+            case 3:
+                if (VEC >= 8) {
+                    small_blocks<Bits, VEC, 3>(v[u], c0, nblk, values + out0, offsets + out0);
+                    break;
                 }
-                values[out0 + k] = v[u].e[s + best];
-                offsets[out0 + k] = uint8_t(best);
-            }
-        } else {
-            // in-lane candidate, then a butterfly over the b / VEC lanes of the block
-            const int j0 = int(c0 & (b - 1));
-            int best = 0;
-            uint32_t best_mag = uint32_t(v[u].e[0]) & Tr::MAG;
-#pragma unroll
-            for (int e = 1; e < VEC; ++e) {
-                const uint32_t mag = uint32_t(v[u].e[e]) & Tr::MAG;
-                if (mag > best_mag) { best_mag = mag; best = e; }
-            }
-            Key key = pack_key<Bits>(v[u].e[best], j0 + best);
-            const int group = b / VEC;                 // 2 .. 32 lanes
-            for (int m = 1; m < group; m <<= 1) {
-                const Key other = shfl_xor_key(key, m);
-                key = other > key ? other : key;
-            }
-            const int64_t k = c0 >> lb;
-            if ((lane & (group - 1)) == 0 && k < nblk) {
-                Bits val;
-                int j;
-                unpack_key<Bits>(key, val, j);
-                values[out0 + k] = val;
-                offsets[out0 + k] = uint8_t(j);
-            }
+                [[fallthrough]];
+            default:
+                wide_block<Bits, VEC>(v[u], c0, lb, lane, nblk, values + out0, offsets + out0);
         }
     }
 }
@@ -158,8 +214,8 @@ hipError_t launch_encode_t(const darb_plan &p, const void *W, int64_t ldw, void 
     using Tr = EncodeTraits<Bits>;
     constexpr int64_t CHUNK = int64_t(kWave) * Tr::VEC * Tr::UNROLL;
     const int64_t chunks = (p.N + CHUNK - 1) / CHUNK;
-    const int64_t tasks = p.M * chunks;
-    const int64_t blocks = (tasks + kEncodeWaves - 1) / kEncodeWaves;
+    const int64_t cgroups = (chunks + kEncodeWaves - 1) / kEncodeWaves;
+    const int64_t blocks = p.M * cgroups;
     if (blocks > 0x7FFFFFFF) return hipErrorInvalidConfiguration;
     const bool aligned = (reinterpret_cast<uintptr_t>(W) % 16 == 0) &&
                          ((ldw * int64_t(sizeof(Bits))) % 16 == 0);
@@ -167,12 +223,12 @@ hipError_t launch_encode_t(const darb_plan &p, const void *W, int64_t ldw, void 
     Bits *vals = static_cast<Bits *>(values);
     if (aligned)
         hipLaunchKernelGGL((encode_kernel<Bits, true>), dim3(unsigned(blocks)),
-                           dim3(kEncodeThreads), 0, s, w, ldw, p.N, p.M, p.d_perm, p.bins,
-                           chunks, vals, offsets);
+                           dim3(kEncodeThreads), 0, s, w, ldw, p.N, p.d_perm, p.bins, chunks,
+                           int(cgroups), vals, offsets);
     else
         hipLaunchKernelGGL((encode_kernel<Bits, false>), dim3(unsigned(blocks)),
-                           dim3(kEncodeThreads), 0, s, w, ldw, p.N, p.M, p.d_perm, p.bins,
-                           chunks, vals, offsets);
+                           dim3(kEncodeThreads), 0, s, w, ldw, p.N, p.d_perm, p.bins, chunks,
+                           int(cgroups), vals, offsets);
     return hipGetLastError();
 }
 

@@ -3,19 +3,24 @@
 // Only retained weights are read (section 2), and each retained weight's
 // in-block offset selects the one activation it multiplies (section 3.2):
 //     y[r] = sum_k v[r,k] * x[k * b_r + off[r,k]].
-// The grouped layout makes every block-size group a dense [rows x nblk] array,
-// so a group is streamed with plain coalesced vector loads.
+// The grouped layout makes every block-size group a dense [rows x nblk] array.
+// Every workgroup works inside one group, so the group's geometry is uniform:
+// it is read with scalar loads, and the per-lane work starts with the loads that
+// matter.  Loads are never placed under per-lane branches: addresses are clamped
+// into the buffer and the unused lanes' results are masked, so a wave issues all
+// of its loads back to back.
 //
-// SpMV: a wave owns `lanes_per_row` lanes per row and 64 / lanes_per_row rows of
-// one group; lanes stride over the row's vectors (16-byte value loads plus the
-// matching offset bytes).  The loads of the first chunk are issued before the
-// workgroup stages x into LDS, so HBM latency overlaps the staging; the gathers
-// then hit LDS.  Per-row sums are combined by an xor butterfly over the row's
-// lanes (fixed order, deterministic) and written to y in original row order.
+// SpMV: `lanes` lanes per row, 64 / lanes rows per wave; each lane holds up to
+// kVmax 16-byte vectors of values (plus their offset bytes) in registers.  The
+// workgroup stages x into LDS after issuing those loads, so HBM latency overlaps
+// the staging; the gathers then hit LDS.  A row's partial sums are combined by an
+// xor butterfly in a fixed order (deterministic) and written in original row order.
 //
 // SpMM: lanes map to batch columns (X is [N x B] row-major, so one weight's
-// activations X[c, :] are contiguous); a row's (value, column) pairs are loaded
-// one per lane and broadcast across the row's lanes with shuffles.
+// activations X[c, :] are contiguous), CPL columns per lane with 16-byte loads.
+// A workgroup stages the (value, column) pairs of its rows into LDS with
+// coalesced loads, then its waves split each row's weights (ksplit ways) and
+// gather X rows kSpmmBatch at a time; partial sums meet in LDS in a fixed order.
 #include <hip/hip_fp16.h>
 
 #include "darb_internal.h"
@@ -23,20 +28,55 @@
 namespace darb {
 namespace {
 
-constexpr int kThreads = 256;
-constexpr int kWaves = kThreads / kWave;
-constexpr int kVmax = 8;                         // vectors in flight per lane (SpMV)
-constexpr int64_t kLdsMaxFloats = 16384;         // x staged in LDS up to 64 KiB
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 template <typename T> __device__ __forceinline__ float to_f32(T v);
 template <> __device__ __forceinline__ float to_f32<float>(float v) { return v; }
 template <> __device__ __forceinline__ float to_f32<__half>(__half v) { return __half2float(v); }
 
-template <typename Tw> struct WVec;
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ float half_bits_to_f32(uint32_t h) {
+    return __half2float(__ushort_as_half(uint16_t(h & 0xFFFFu)));
+}
 
+__device__ __forceinline__ int wave_uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
+
+// Uniform selection of a per-group table entry (compile-time indices only, so the
+// table stays in scalar registers).
+template <typename T>
+__device__ __forceinline__ T pick(const T (&a)[kMaxBins], int g) {
+    T r = a[0];
+#pragma unroll
+    for (int b = 1; b < kMaxBins; ++b) r = (b == g) ? a[b] : r;
+    return r;
+}
+
+__device__ __forceinline__ int block_group(const ProductSchedule &s) {
+    int g = 0;
+#pragma unroll
+    for (int b = 1; b < kMaxBins; ++b)
+        if (b < s.nbins && int(blockIdx.x) >= s.block_begin[b]) g = b;
+    return g;
+}
+
+__device__ __forceinline__ int block_begin_of(const ProductSchedule &s, int g) {
+    int r = s.block_begin[0];
+#pragma unroll
+    for (int b = 1; b < kMaxBins; ++b) r = (b == g) ? s.block_begin[b] : r;
+    return r;
+}
+
+// ---------------------------------------------------------------------------------
+// SpMV
+// ---------------------------------------------------------------------------------
+
+constexpr int kSpmvThreads = 256;
+constexpr int kSpmvWaves = kSpmvThreads / kWave;
+constexpr int kVmax = 8;                         // vectors per lane per round
+constexpr int kLdsMaxFloats = 16384;             // x staged in LDS up to 64 KiB
+
+template <typename Tw> struct WVec;
 template <> struct WVec<float> {
     static constexpr int VEC = 4;
     using V = f32x4;        // 4 values, 16 bytes
@@ -49,8 +89,7 @@ template <> struct WVec<__half> {
     using O = u32x2;        // their 8 offset bytes
     __device__ static float get(const V &v, int i) {
         const uint32_t w = v[i >> 1];
-        const uint16_t h = (i & 1) ? uint16_t(w >> 16) : uint16_t(w & 0xFFFFu);
-        return __half2float(__ushort_as_half(h));
+        return half_bits_to_f32((i & 1) ? (w >> 16) : w);
     }
 };
 
@@ -59,216 +98,421 @@ __device__ __forceinline__ uint32_t off_byte(u32x2 o, int i) {
     return (o[i >> 2] >> (8 * (i & 3))) & 0xFFu;
 }
 
-__device__ __forceinline__ int find_group(const ProductSchedule &s, int64_t wtile) {
-    int g = 0;
-    while (g + 1 < s.nbins && wtile >= s.tile_begin[g + 1]) ++g;
-    return g;
+// Copy x (N elements) into LDS as fp32: SB 16-byte loads per thread in flight
+// (addresses clamped, stores masked), then the scalar tail.
+template <typename Tx, int SB>
+__device__ __forceinline__ void stage_x(float *xs, const Tx *__restrict__ x, int N) {
+    constexpr int E = 16 / int(sizeof(Tx));
+    const bool aligned = (reinterpret_cast<uintptr_t>(x) & 15) == 0;
+    const int nv = aligned ? N / E : 0;
+    const u32x4 *x4 = reinterpret_cast<const u32x4 *>(x);
+    for (int base = 0; base < nv; base += SB * kSpmvThreads) {
+        u32x4 t[SB];
+#pragma unroll
+        for (int u = 0; u < SB; ++u) {
+            const int i = base + u * kSpmvThreads + int(threadIdx.x);
+            t[u] = x4[i < nv ? i : nv - 1];
+        }
+#pragma unroll
+        for (int u = 0; u < SB; ++u) {
+            const int i = base + u * kSpmvThreads + int(threadIdx.x);
+            if (i < nv) {
+                if constexpr (sizeof(Tx) == 4) {
+                    *reinterpret_cast<u32x4 *>(xs + i * E) = t[u];
+                } else {
+#pragma unroll
+                    for (int h = 0; h < 4; ++h) {
+                        xs[i * E + 2 * h] = half_bits_to_f32(t[u][h]);
+                        xs[i * E + 2 * h + 1] = half_bits_to_f32(t[u][h] >> 16);
+                    }
+                }
+            }
+        }
+    }
+    for (int c = nv * E + int(threadIdx.x); c < N; c += kSpmvThreads) xs[c] = to_f32<Tx>(x[c]);
 }
 
-template <typename Tw, typename Tx, bool LDS>
-__global__ __launch_bounds__(kThreads) void spmv_kernel(
+template <typename Tw, typename Tx, bool LDS, int SB>
+__global__ __launch_bounds__(kSpmvThreads) void spmv_kernel(
     const Tw *__restrict__ values, const uint8_t *__restrict__ offsets,
     const Tx *__restrict__ x, float *__restrict__ y, const int32_t *__restrict__ perm,
-    int64_t N, BinTable bins, ProductSchedule sch) {
+    int N, BinTable bins, ProductSchedule sch) {
     using WV = WVec<Tw>;
     constexpr int VEC = WV::VEC;
     extern __shared__ float xs[];
 
-    const int lane = threadIdx.x & (kWave - 1);
-    const int64_t wtile = int64_t(blockIdx.x) * kWaves + threadIdx.x / kWave;
-    const bool active = wtile < sch.tile_begin[sch.nbins];
-    const int g = find_group(sch, active ? wtile : 0);
-    const int L = sch.lanes_per_row[g];
-    const int lb = bins.log2b[g];
-    const int64_t nblk = bins.nblk[g];
-    const int64_t row_in_group = (wtile - sch.tile_begin[g]) * (kWave / L) + lane / L;
-    const bool row_ok = active && row_in_group < bins.rows[g];
-    const int sub = lane & (L - 1);
-    const int64_t e0 = bins.first_elem[g] + row_in_group * nblk;
-    const bool vec_path = sch.vec[g] == VEC;
-    const int64_t nvec = vec_path ? nblk / VEC : nblk;
-    const int64_t stride = int64_t(L) * kVmax;
+    const int g = block_group(sch);
+    const int wave = wave_uniform(int(threadIdx.x) / kWave);
+    const int lane = int(threadIdx.x) & (kWave - 1);
+    const int lgL = pick(sch.log2_lanes, g);
+    const int L = 1 << lgL;
+    const int lb = pick(bins.log2b, g);
+    const int nblk = int(pick(bins.nblk, g));
+    const int64_t rows = pick(bins.rows, g);
+    const int64_t first_row = pick(bins.first_row, g);
+    const int64_t first_elem = pick(bins.first_elem, g);
+    const bool vec_path = pick(sch.vec, g) == VEC;
 
-    // first chunk of this lane's vectors, issued before x is staged
+    const int64_t tile = int64_t(int(blockIdx.x) - block_begin_of(sch, g)) * kSpmvWaves + wave;
+    const int64_t row = (tile << (6 - lgL)) + (lane >> lgL);
+    const bool row_ok = row < rows;
+    const int64_t row_c = row_ok ? row : rows - 1;
+    const int sub = lane & (L - 1);
+    const int64_t e0 = first_elem + row_c * nblk;
+    const int nvec = vec_path ? nblk / VEC : nblk;
+
+    // the first round of this lane's vectors, issued before x is staged
     typename WV::V wv[kVmax];
     typename WV::O ov[kVmax];
+    const typename WV::V *vrow = reinterpret_cast<const typename WV::V *>(values + e0);
+    const typename WV::O *orow = reinterpret_cast<const typename WV::O *>(offsets + e0);
     if (vec_path) {
 #pragma unroll
         for (int t = 0; t < kVmax; ++t) {
-            const int64_t vi = sub + int64_t(t) * L;
-            if (row_ok && vi < nvec) {
-                wv[t] = __builtin_nontemporal_load(
-                    reinterpret_cast<const typename WV::V *>(values + e0) + vi);
-                ov[t] = *(reinterpret_cast<const typename WV::O *>(offsets + e0) + vi);
-            }
+            const int vi = sub + t * L;
+            const int vc = vi < nvec ? vi : nvec - 1;
+            wv[t] = __builtin_nontemporal_load(vrow + vc);
+            ov[t] = orow[vc];
         }
     }
 
-    if (LDS) {
-        for (int64_t c = threadIdx.x; c < N; c += kThreads) xs[c] = to_f32<Tx>(x[c]);
+    if constexpr (LDS) {
+        stage_x<Tx, SB>(xs, x, N);
         __syncthreads();
     }
-    // offsets produced by the encode always give c < N; the global path clamps
-    // anyway so a malformed offset cannot read outside x
-    auto xat = [&](int64_t c) -> float {
-        return LDS ? xs[c] : to_f32<Tx>(x[c < N ? c : N - 1]);
+    auto xat = [&](int c) -> float {
+        // offsets from the encode always give c < N; the global path clamps anyway
+        // so a malformed offset cannot read outside x
+        if constexpr (LDS) return xs[c];
+        else return to_f32<Tx>(x[c < N ? c : N - 1]);
     };
 
     float acc = 0.0f;
     if (vec_path) {
-        for (int64_t base = 0;; base += stride) {
+        for (int base = 0;; base += L * kVmax) {
 #pragma unroll
             for (int t = 0; t < kVmax; ++t) {
-                const int64_t vi = base + sub + int64_t(t) * L;
-                if (row_ok && vi < nvec) {
+                const int vi = base + sub + t * L;
+                if (vi < nvec) {
 #pragma unroll
                     for (int q = 0; q < VEC; ++q) {
-                        const int64_t k = vi * VEC + q;
-                        const int64_t c = (k << lb) + off_byte(ov[t], q);
+                        const int c = ((vi * VEC + q) << lb) + int(off_byte(ov[t], q));
                         acc = fmaf(WV::get(wv[t], q), xat(c), acc);
                     }
                 }
             }
-            if (base + stride >= nvec) break;
+            if (base + L * kVmax >= nvec) break;
 #pragma unroll
             for (int t = 0; t < kVmax; ++t) {
-                const int64_t vi = base + stride + sub + int64_t(t) * L;
-                if (row_ok && vi < nvec) {
-                    wv[t] = __builtin_nontemporal_load(
-                        reinterpret_cast<const typename WV::V *>(values + e0) + vi);
-                    ov[t] = *(reinterpret_cast<const typename WV::O *>(offsets + e0) + vi);
-                }
+                const int vi = base + L * kVmax + sub + t * L;
+                const int vc = vi < nvec ? vi : nvec - 1;
+                wv[t] = __builtin_nontemporal_load(vrow + vc);
+                ov[t] = orow[vc];
             }
         }
-    } else if (row_ok) {
-        for (int64_t k = sub; k < nblk; k += L) {
-            const int64_t c = (k << lb) + offsets[e0 + k];
-            acc = fmaf(to_f32<Tw>(values[e0 + k]), xat(c), acc);
-        }
+    } else {
+        const Tw *vr = values + e0;
+        const uint8_t *orr = offsets + e0;
+        for (int k = sub; k < nblk; k += L)
+            acc = fmaf(to_f32<Tw>(vr[k]), xat((k << lb) + int(orr[k])), acc);
     }
 
     for (int m = L >> 1; m >= 1; m >>= 1) acc += __shfl_xor(acc, m, kWave);
-    if (row_ok && sub == 0) y[perm[bins.first_row[g] + row_in_group]] = acc;
+    if (row_ok && sub == 0) y[perm[first_row + row]] = acc;
 }
 
-template <typename Tw, typename Tx>
-__global__ __launch_bounds__(kThreads) void spmm_kernel(
+// ---------------------------------------------------------------------------------
+// SpMM
+// ---------------------------------------------------------------------------------
+
+constexpr int kSpmmThreads = 512;
+constexpr int kSpmmWaves = kSpmmThreads / kWave;
+constexpr int kSpmmBatch = 16;        // X rows in flight per lane
+constexpr int kPairsMax = 4096;       // (value, column) pairs staged per round
+constexpr int kStageRounds = 8;       // pair loads per thread in flight while staging
+
+// CPL consecutive batch columns of one X row, loaded at once (16 bytes when CPL > 1).
+template <typename Tx, int CPL> struct XLoad;
+template <typename Tx> struct XLoad<Tx, 1> {
+    using V = Tx;
+    __device__ static V load(const Tx *p) { return *p; }
+    __device__ static float get(const V &v, int) { return to_f32<Tx>(v); }
+};
+template <> struct XLoad<float, 4> {
+    using V = f32x4;
+    __device__ static V load(const float *p) { return *reinterpret_cast<const f32x4 *>(p); }
+    __device__ static float get(const V &v, int i) { return v[i]; }
+};
+template <> struct XLoad<__half, 8> {
+    using V = u32x4;
+    __device__ static V load(const __half *p) { return *reinterpret_cast<const u32x4 *>(p); }
+    __device__ static float get(const V &v, int i) {
+        const uint32_t w = v[i >> 1];
+        return half_bits_to_f32((i & 1) ? (w >> 16) : w);
+    }
+};
+
+struct Pair {
+    float v;
+    int c;
+};
+
+template <typename Tw, typename Tx, int CPL>
+__global__ __launch_bounds__(kSpmmThreads) void spmm_kernel(
     const Tw *__restrict__ values, const uint8_t *__restrict__ offsets,
     const Tx *__restrict__ X, int64_t ldx, int64_t B, float *__restrict__ Y, int64_t ldy,
-    const int32_t *__restrict__ perm, int64_t N, BinTable bins, ProductSchedule sch) {
-    const int lane = threadIdx.x & (kWave - 1);
-    const int64_t wtile = int64_t(blockIdx.x) * kWaves + threadIdx.x / kWave;
-    if (wtile >= sch.tile_begin[sch.nbins]) return;   // wave-uniform
-    const int g = find_group(sch, wtile);
-    const int L = sch.lanes_per_row[g];
-    const int lb = bins.log2b[g];
-    const int64_t nblk = bins.nblk[g];
-    const int64_t t_in_group = wtile - sch.tile_begin[g];
-    const int64_t row_tile = t_in_group / sch.col_slabs;
-    const int64_t slab = t_in_group - row_tile * sch.col_slabs;
-    const int64_t row_in_group = row_tile * (kWave / L) + lane / L;
-    const bool row_ok = row_in_group < bins.rows[g];
-    const int sub = lane & (L - 1);
-    const int64_t col = slab * L + sub;
-    const bool col_ok = col < B;
-    const int64_t e0 = bins.first_elem[g] + row_in_group * nblk;
+    const int32_t *__restrict__ perm, int N, BinTable bins, ProductSchedule sch) {
+    using XL = XLoad<Tx, CPL>;
+    extern __shared__ __align__(16) unsigned char smem[];
+    Pair *pairs = reinterpret_cast<Pair *>(smem);
+    float *part = reinterpret_cast<float *>(smem + kPairsMax * sizeof(Pair));
 
-    float acc = 0.0f;
-    for (int64_t kb = 0; kb < nblk; kb += L) {
-        const int64_t k = kb + sub;
-        float v_l = 0.0f;
-        int c_l = 0;
-        if (row_ok && k < nblk) {
-            v_l = to_f32<Tw>(values[e0 + k]);
-            c_l = int((k << lb) + offsets[e0 + k]);
+    const int g = block_group(sch);
+    const int wave = wave_uniform(int(threadIdx.x) / kWave);
+    const int lane = int(threadIdx.x) & (kWave - 1);
+    const int lgL = pick(sch.log2_lanes, g);
+    const int L = 1 << lgL;
+    const int R = kWave >> lgL;                  // rows per row group
+    const int KS = pick(sch.ksplit, g);          // waves per row group
+    const int rows_pb = R * (kSpmmWaves / KS);   // rows per workgroup
+    const int lgKC = pick(sch.log2_kchunk, g);
+    const int KC = 1 << lgKC;
+    const int lb = pick(bins.log2b, g);
+    const int nblk = int(pick(bins.nblk, g));
+    const int64_t rows = pick(bins.rows, g);
+    const int64_t first_row = pick(bins.first_row, g);
+    const int64_t first_elem = pick(bins.first_elem, g);
+
+    const int local = int(blockIdx.x) - block_begin_of(sch, g);
+    const int row_blk = local / sch.col_slabs;
+    const int slab = local - row_blk * sch.col_slabs;
+    const int64_t row0 = int64_t(row_blk) * rows_pb;
+    const int rows_here = int(rows - row0 < rows_pb ? rows - row0 : rows_pb);
+    const Tw *vb = values + first_elem + row0 * nblk;
+    const uint8_t *ob = offsets + first_elem + row0 * nblk;
+
+    const int rg = wave / KS, ks = wave - (wave / KS) * KS;
+    const int rl = rg * R + (lane >> lgL);       // row of this lane inside the block
+    const bool row_ok = rl < rows_here;
+    const int rl_c = row_ok ? rl : 0;
+    const int sub = lane & (L - 1);
+    const int64_t col0 = (int64_t(slab) * L + sub) * CPL;
+    const bool col_ok = col0 < B;                // CPL > 1 only when CPL divides B
+    const int64_t col_c = col_ok ? col0 : 0;
+    const int per_wave = KC / KS;
+
+    float acc[CPL];
+#pragma unroll
+    for (int q = 0; q < CPL; ++q) acc[q] = 0.0f;
+
+    for (int k0 = 0; k0 < nblk; k0 += KC) {
+        const int kc = nblk - k0 < KC ? nblk - k0 : KC;
+        // stage this round's pairs: rows_pb x KC slots, coalesced along each row
+        const int total = rows_pb << lgKC;
+        for (int base = 0; base < total; base += kStageRounds * kSpmmThreads) {
+            float v[kStageRounds];
+            uint32_t o[kStageRounds];
+#pragma unroll
+            for (int u = 0; u < kStageRounds; ++u) {
+                const int idx = base + u * kSpmmThreads + int(threadIdx.x);
+                const int r = idx >> lgKC, kk = idx & (KC - 1);
+                const bool ok = idx < total && r < rows_here && kk < kc;
+                const int64_t e = ok ? int64_t(r) * nblk + k0 + kk : 0;
+                v[u] = to_f32<Tw>(vb[e]);
+                o[u] = ob[e];
+            }
+#pragma unroll
+            for (int u = 0; u < kStageRounds; ++u) {
+                const int idx = base + u * kSpmmThreads + int(threadIdx.x);
+                if (idx < total) {
+                    const int r = idx >> lgKC, kk = idx & (KC - 1);
+                    const bool ok = r < rows_here && kk < kc;
+                    Pair p;
+                    p.v = ok ? v[u] : 0.0f;
+                    const int c = ((k0 + kk) << lb) + int(o[u]);
+                    p.c = ok ? (c < N ? c : N - 1) : -1;   // -1 marks an empty slot
+                    pairs[idx] = p;
+                }
+            }
         }
-        const int cnt = int(nblk - kb < L ? nblk - kb : L);
-        for (int t = 0; t < cnt; ++t) {
-            const float v = __shfl(v_l, t, L);
-            int c = __shfl(c_l, t, L);
-            c = c < N ? c : N - 1;                 // see the note in spmv_kernel
-            if (row_ok && col_ok) acc = fmaf(v, to_f32<Tx>(X[int64_t(c) * ldx + col]), acc);
+        __syncthreads();
+
+        // this wave's share of the round: slots [ks*per_wave, (ks+1)*per_wave) of its rows
+        const int kbeg = ks * per_wave;
+        const int kend = kbeg + per_wave < kc ? kbeg + per_wave : kc;
+        const Pair *prow = pairs + (rl_c << lgKC);
+        for (int kk = kbeg; kk < kend; kk += kSpmmBatch) {
+            Pair p[kSpmmBatch];
+#pragma unroll
+            for (int u = 0; u < kSpmmBatch; ++u) {
+                const int s = kk + u < kend ? kk + u : kend - 1;
+                p[u] = prow[s];
+            }
+            typename XL::V xv[kSpmmBatch];
+#pragma unroll
+            for (int u = 0; u < kSpmmBatch; ++u) {
+                const int64_t c = p[u].c >= 0 ? p[u].c : 0;
+                xv[u] = XL::load(X + c * ldx + col_c);
+            }
+#pragma unroll
+            for (int u = 0; u < kSpmmBatch; ++u) {
+                if (kk + u < kend && p[u].c >= 0) {
+#pragma unroll
+                    for (int q = 0; q < CPL; ++q) acc[q] = fmaf(p[u].v, XL::get(xv[u], q), acc[q]);
+                }
+            }
+        }
+        __syncthreads();
+    }
+
+    // combine the KS partial sums of each row group in a fixed order
+    if (KS > 1) {
+#pragma unroll
+        for (int q = 0; q < CPL; ++q) part[(wave * kWave + lane) * CPL + q] = acc[q];
+        __syncthreads();
+        if (ks == 0) {
+            for (int s = 1; s < KS; ++s) {
+#pragma unroll
+                for (int q = 0; q < CPL; ++q) acc[q] += part[((wave + s) * kWave + lane) * CPL + q];
+            }
         }
     }
-    if (row_ok && col_ok) Y[int64_t(perm[bins.first_row[g] + row_in_group]) * ldy + col] = acc;
+    if (ks == 0 && row_ok && col_ok) {
+        float *yrow = Y + int64_t(perm[first_row + row0 + rl]) * ldy + col0;
+#pragma unroll
+        for (int q = 0; q < CPL; ++q) yrow[q] = acc[q];
+    }
+}
+
+// ---------------------------------------------------------------------------------
+// host-side schedules and launches
+// ---------------------------------------------------------------------------------
+
+int ilog2_floor(int64_t v) {
+    int l = 0;
+    while ((int64_t(2) << l) <= v) ++l;
+    return l;
+}
+int ilog2_ceil(int64_t v) {
+    int l = 0;
+    while ((int64_t(1) << l) < v) ++l;
+    return l;
 }
 
 template <typename Tw>
-ProductSchedule spmv_schedule(const darb_plan &p, const void *values, const uint8_t *offsets) {
+bool spmv_schedule(const darb_plan &p, const void *values, const uint8_t *offsets,
+                   ProductSchedule &s) {
     constexpr int VEC = WVec<Tw>::VEC;
-    ProductSchedule s{};
+    s = ProductSchedule{};
     s.nbins = p.bins.nbins;
     s.col_slabs = 1;
-    int64_t tiles = 0;
     const bool ptr_ok = (reinterpret_cast<uintptr_t>(values) % 16 == 0) &&
                         (reinterpret_cast<uintptr_t>(offsets) % VEC == 0);
+    int64_t blocks = 0;
     for (int g = 0; g < s.nbins; ++g) {
         const int64_t nblk = p.bins.nblk[g];
         const bool vec = ptr_ok && nblk % VEC == 0 && p.bins.first_elem[g] % VEC == 0;
         s.vec[g] = vec ? VEC : 1;
         const int64_t nvec = vec ? nblk / VEC : nblk;
-        int L = 1;
-        while (L < kWave && (nvec + L - 1) / L > kVmax) L <<= 1;
-        s.lanes_per_row[g] = L;
-        s.tile_begin[g] = tiles;
-        const int64_t rpw = kWave / L;
-        tiles += (p.bins.rows[g] + rpw - 1) / rpw;
+        int lgL = 0;     // fewest lanes per row that keep each lane within kVmax vectors
+        while (lgL < 6 && ((nvec + (int64_t(1) << lgL) - 1) >> lgL) > kVmax) ++lgL;
+        s.log2_lanes[g] = lgL;
+        s.block_begin[g] = int32_t(blocks);
+        const int64_t rows_per_wave = int64_t(kWave) >> lgL;
+        const int64_t tiles = (p.bins.rows[g] + rows_per_wave - 1) / rows_per_wave;
+        blocks += (tiles + kSpmvWaves - 1) / kSpmvWaves;
+        if (blocks > 0x7FFFFFFF) return false;
     }
-    s.tile_begin[s.nbins] = tiles;
-    return s;
-}
-
-ProductSchedule spmm_schedule(const darb_plan &p, int64_t B) {
-    ProductSchedule s{};
-    s.nbins = p.bins.nbins;
-    int L = 1;
-    while (L < kWave && L < B) L <<= 1;
-    s.col_slabs = (B + L - 1) / L;
-    int64_t tiles = 0;
-    for (int g = 0; g < s.nbins; ++g) {
-        s.vec[g] = 1;
-        s.lanes_per_row[g] = L;
-        s.tile_begin[g] = tiles;
-        const int64_t rpw = kWave / L;
-        tiles += (p.bins.rows[g] + rpw - 1) / rpw * s.col_slabs;
-    }
-    s.tile_begin[s.nbins] = tiles;
-    return s;
+    s.block_begin[s.nbins] = int32_t(blocks);
+    return true;
 }
 
 template <typename Tw, typename Tx>
 hipError_t launch_spmv_t(const darb_plan &p, const void *values, const uint8_t *offsets,
                          const void *x, float *y, hipStream_t st) {
-    const ProductSchedule s = spmv_schedule<Tw>(p, values, offsets);
-    const int64_t tiles = s.tile_begin[s.nbins];
-    const int64_t blocks = (tiles + kWaves - 1) / kWaves;
+    ProductSchedule s;
+    if (!spmv_schedule<Tw>(p, values, offsets, s)) return hipErrorInvalidConfiguration;
+    const int blocks = s.block_begin[s.nbins];
     if (blocks == 0) return hipSuccess;
-    if (blocks > 0x7FFFFFFF) return hipErrorInvalidConfiguration;
     const Tw *v = static_cast<const Tw *>(values);
     const Tx *xx = static_cast<const Tx *>(x);
+    const int N = int(p.N);
     if (p.N <= kLdsMaxFloats) {
         const size_t lds = size_t(p.N) * sizeof(float);
-        hipLaunchKernelGGL((spmv_kernel<Tw, Tx, true>), dim3(unsigned(blocks)), dim3(kThreads),
-                           lds, st, v, offsets, xx, y, p.d_perm, p.N, p.bins, s);
+        const int64_t nv = p.N / (16 / int64_t(sizeof(Tx)));
+        const int64_t per_thread = (nv + kSpmvThreads - 1) / kSpmvThreads;
+#define DARB_SPMV_LDS(SB)                                                                       \
+    hipLaunchKernelGGL((spmv_kernel<Tw, Tx, true, SB>), dim3(blocks), dim3(kSpmvThreads), lds, \
+                       st, v, offsets, xx, y, p.d_perm, N, p.bins, s)
+        if (per_thread <= 1) DARB_SPMV_LDS(1);
+        else if (per_thread <= 2) DARB_SPMV_LDS(2);
+        else if (per_thread <= 4) DARB_SPMV_LDS(4);
+        else if (per_thread <= 8) DARB_SPMV_LDS(8);
+        else DARB_SPMV_LDS(16);
+#undef DARB_SPMV_LDS
     } else {
-        hipLaunchKernelGGL((spmv_kernel<Tw, Tx, false>), dim3(unsigned(blocks)), dim3(kThreads),
-                           0, st, v, offsets, xx, y, p.d_perm, p.N, p.bins, s);
+        hipLaunchKernelGGL((spmv_kernel<Tw, Tx, false, 1>), dim3(blocks), dim3(kSpmvThreads), 0,
+                           st, v, offsets, xx, y, p.d_perm, N, p.bins, s);
     }
     return hipGetLastError();
+}
+
+bool spmm_schedule(const darb_plan &p, int64_t B, int cpl, ProductSchedule &s) {
+    s = ProductSchedule{};
+    s.nbins = p.bins.nbins;
+    const int64_t lanes = (B + cpl - 1) / cpl;        // lanes needed for all columns
+    const int lgL = lanes >= kWave ? 6 : ilog2_ceil(lanes);
+    const int64_t slabs = (lanes + (int64_t(1) << lgL) - 1) >> lgL;
+    if (slabs > 0x7FFFFFFF) return false;
+    s.col_slabs = int32_t(slabs);
+    const int R = kWave >> lgL;
+    int64_t blocks = 0;
+    for (int g = 0; g < s.nbins; ++g) {
+        const int64_t nblk = p.bins.nblk[g];
+        // split a row group's weights over up to 8 waves, ~128 weights per wave
+        int lgKS = ilog2_ceil((nblk + 127) / 128);
+        if (lgKS > 3) lgKS = 3;
+        const int KS = 1 << lgKS;
+        const int rows_pb = R * (kSpmmWaves / KS);
+        int lgKC = ilog2_floor(kPairsMax / rows_pb);  // pairs per round fit the LDS buffer
+        const int lgN = ilog2_ceil(nblk);
+        if (lgKC > lgN) lgKC = lgN;
+        if (lgKC < lgKS) lgKC = lgKS;                 // at least one slot per wave
+        s.log2_lanes[g] = lgL;
+        s.ksplit[g] = KS;
+        s.log2_kchunk[g] = lgKC;
+        s.vec[g] = cpl;
+        s.block_begin[g] = int32_t(blocks);
+        blocks += (p.bins.rows[g] + rows_pb - 1) / rows_pb * slabs;
+        if (blocks > 0x7FFFFFFF) return false;
+    }
+    s.block_begin[s.nbins] = int32_t(blocks);
+    return true;
 }
 
 template <typename Tw, typename Tx>
 hipError_t launch_spmm_t(const darb_plan &p, const void *values, const uint8_t *offsets,
                          int64_t B, const void *X, int64_t ldx, float *Y, int64_t ldy,
                          hipStream_t st) {
-    const ProductSchedule s = spmm_schedule(p, B);
-    const int64_t tiles = s.tile_begin[s.nbins];
-    const int64_t blocks = (tiles + kWaves - 1) / kWaves;
+    constexpr int CPL = 16 / int(sizeof(Tx));
+    const bool vec = (reinterpret_cast<uintptr_t>(X) % 16 == 0) &&
+                     ((ldx * int64_t(sizeof(Tx))) % 16 == 0) && (B % CPL == 0);
+    ProductSchedule s;
+    if (!spmm_schedule(p, B, vec ? CPL : 1, s)) return hipErrorInvalidConfiguration;
+    const int blocks = s.block_begin[s.nbins];
     if (blocks == 0) return hipSuccess;
-    if (blocks > 0x7FFFFFFF) return hipErrorInvalidConfiguration;
-    hipLaunchKernelGGL((spmm_kernel<Tw, Tx>), dim3(unsigned(blocks)), dim3(kThreads), 0, st,
-                       static_cast<const Tw *>(values), offsets, static_cast<const Tx *>(X), ldx,
-                       B, Y, ldy, p.d_perm, p.N, p.bins, s);
+    const Tw *v = static_cast<const Tw *>(values);
+    const Tx *x = static_cast<const Tx *>(X);
+    const int N = int(p.N);
+    if (vec) {
+        const size_t lds = kPairsMax * sizeof(Pair) + size_t(kSpmmThreads) * CPL * sizeof(float);
+        hipLaunchKernelGGL((spmm_kernel<Tw, Tx, CPL>), dim3(blocks), dim3(kSpmmThreads), lds, st,
+                           v, offsets, x, ldx, B, Y, ldy, p.d_perm, N, p.bins, s);
+    } else {
+        const size_t lds = kPairsMax * sizeof(Pair) + size_t(kSpmmThreads) * sizeof(float);
+        hipLaunchKernelGGL((spmm_kernel<Tw, Tx, 1>), dim3(blocks), dim3(kSpmmThreads), lds, st, v,
+                           offsets, x, ldx, B, Y, ldy, p.d_perm, N, p.bins, s);
+    }
     return hipGetLastError();
 }
 
