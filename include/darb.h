@@ -112,11 +112,13 @@ int darb_plan_info(const darb_plan *plan, darb_plan_info_t *info);
 int darb_plan_export(const darb_plan *plan, uint8_t *log2b, int64_t *row_start, int32_t *perm);
 
 /*
- * Enqueue the copy of the plan's device metadata into a caller-owned device
- * workspace of at least info.workspace_bytes bytes (256-byte aligned), and
- * remember it for later device calls.  The workspace must stay allocated and
- * unmodified while the plan is used on the device.  Re-uploading to another
- * workspace is allowed.  Errors: DARB_E_INVALID, DARB_E_WORKSPACE, DARB_E_HIP.
+ * Copy the plan's device metadata (the storage order and a per-row table of
+ * first slot and block size) into a caller-owned device workspace of at least
+ * info.workspace_bytes bytes (256-byte aligned) on `stream`, wait for the copy
+ * to finish, and remember the workspace for later device calls on the current
+ * device.  The workspace must stay allocated and unmodified while the plan is
+ * used on the device.  Re-uploading to another workspace is allowed.
+ * Errors: DARB_E_INVALID, DARB_E_WORKSPACE, DARB_E_NOMEM, DARB_E_HIP.
  */
 int darb_plan_upload(darb_plan *plan, void *workspace, int64_t workspace_bytes, void *stream);
 

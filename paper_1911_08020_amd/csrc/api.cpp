@@ -20,6 +20,9 @@ void clear_error() { g_last_error.clear(); }
 
 static bool is_pow2(int64_t v) { return v > 0 && (v & (v - 1)) == 0; }
 
+// workspace layout: perm (int32 [M]) padded to 256 bytes, then rowinfo (int64 [M])
+static int64_t perm_bytes(int64_t M) { return (M * int64_t(sizeof(int32_t)) + 255) / 256 * 256; }
+
 static int log2_exact(int64_t v) {
     int l = 0;
     while ((int64_t(1) << l) != v) ++l;
@@ -138,7 +141,7 @@ int darb_plan_create(int64_t M, int64_t N, const double *row_density, double mat
         p->row_start[r] = group_elem[l];
         group_elem[l] += nblk;
     }
-    p->workspace_bytes = ((M * int64_t(sizeof(int32_t))) + 255) / 256 * 256;
+    p->workspace_bytes = perm_bytes(M) + M * int64_t(sizeof(int64_t));
     *out = p;
     return DARB_OK;
 }
@@ -182,11 +185,26 @@ int darb_plan_upload(darb_plan *p, void *workspace, int64_t workspace_bytes, voi
     int dev = -1;
     hipError_t e = hipGetDevice(&dev);
     if (e != hipSuccess) return fail(DARB_E_HIP, std::string("hipGetDevice: ") + hipGetErrorString(e));
+    std::vector<int64_t> rowinfo;
+    try {
+        rowinfo.resize(p->M);
+    } catch (const std::bad_alloc &) {
+        return fail(DARB_E_NOMEM, "rowinfo");
+    }
+    for (int64_t r = 0; r < p->M; ++r) rowinfo[r] = (p->row_start[r] << 8) | p->log2b[r];
     int32_t *d_perm = static_cast<int32_t *>(workspace);
-    e = hipMemcpyAsync(d_perm, p->perm.data(), p->M * sizeof(int32_t), hipMemcpyHostToDevice,
-                       static_cast<hipStream_t>(stream));
-    if (e != hipSuccess) return fail(DARB_E_HIP, std::string("hipMemcpyAsync: ") + hipGetErrorString(e));
+    int64_t *d_rowinfo = reinterpret_cast<int64_t *>(static_cast<char *>(workspace) +
+                                                     perm_bytes(p->M));
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    e = hipMemcpyAsync(d_perm, p->perm.data(), p->M * sizeof(int32_t), hipMemcpyHostToDevice, s);
+    if (e == hipSuccess)
+        e = hipMemcpyAsync(d_rowinfo, rowinfo.data(), p->M * sizeof(int64_t),
+                           hipMemcpyHostToDevice, s);
+    // the host vector dies on return: make sure the copies have consumed it
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return fail(DARB_E_HIP, std::string("plan upload: ") + hipGetErrorString(e));
     p->d_perm = d_perm;
+    p->d_rowinfo = d_rowinfo;
     p->device = dev;
     return DARB_OK;
 }

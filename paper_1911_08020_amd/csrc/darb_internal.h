@@ -49,8 +49,9 @@ struct darb_plan {
     std::vector<int32_t> perm;
     darb::BinTable bins{};
     int64_t workspace_bytes = 0;
-    // device side
-    int32_t *d_perm = nullptr;
+    // device side (inside the caller's workspace)
+    int32_t *d_perm = nullptr;      // [M] original row stored i-th
+    int64_t *d_rowinfo = nullptr;   // [M] (row_start[r] << 8) | log2b[r], original order
     int device = -1;
 };
 

@@ -138,39 +138,25 @@ __device__ __forceinline__ void wide_block(const Vec<Bits, VEC> &v, int64_t c0, 
 
 template <typename Bits, bool ALIGNED>
 __global__ __launch_bounds__(kEncodeThreads) void encode_kernel(
-    const Bits *__restrict__ W, int64_t ldw, int64_t N, const int32_t *__restrict__ perm,
-    BinTable bins, int64_t chunks_per_row, int cgroups, Bits *__restrict__ values,
+    const Bits *__restrict__ W, int64_t ldw, int64_t N, const int64_t *__restrict__ rowinfo,
+    int64_t chunks_per_row, int cgroups, Bits *__restrict__ values,
     uint8_t *__restrict__ offsets) {
     using Tr = EncodeTraits<Bits>;
     constexpr int VEC = Tr::VEC;
     constexpr int UNROLL = Tr::UNROLL;
     constexpr int64_t CHUNK = int64_t(kWave) * VEC * UNROLL;
 
-    // workgroup -> (storage-order row i, group of kEncodeWaves chunks); all uniform
-    const int i = int(blockIdx.x) / cgroups;
-    const int cg = int(blockIdx.x) - i * cgroups;
+    // workgroup -> (original row r, group of kEncodeWaves chunks); all uniform.  The
+    // W loads depend on nothing but r, so they issue first; the row's block size and
+    // first output slot arrive from the per-row table while they are in flight.
+    const int r = int(blockIdx.x) / cgroups;
+    const int cg = int(blockIdx.x) - r * cgroups;
     const int wave = __builtin_amdgcn_readfirstlane(int(threadIdx.x) / kWave);
     const int lane = int(threadIdx.x) & (kWave - 1);
     const int64_t q = int64_t(cg) * kEncodeWaves + wave;
     if (q >= chunks_per_row) return;                  // wave-uniform, no barrier below
-
-    int g = 0;
-#pragma unroll
-    for (int b = 1; b < kMaxBins; ++b)
-        if (b < bins.nbins && i >= bins.first_row[b]) g = b;
-    int lb = bins.log2b[0];
-    int64_t nblk = bins.nblk[0], first_row = bins.first_row[0], first_elem = bins.first_elem[0];
-#pragma unroll
-    for (int b = 1; b < kMaxBins; ++b) {
-        if (b == g) {
-            lb = bins.log2b[b];
-            nblk = bins.nblk[b];
-            first_row = bins.first_row[b];
-            first_elem = bins.first_elem[b];
-        }
-    }
-    const int64_t out0 = first_elem + (i - first_row) * nblk;
-    const Bits *row = W + int64_t(perm[i]) * ldw;
+    const Bits *row = W + int64_t(r) * ldw;
+    const int64_t info = rowinfo[r];
 
     // issue every load of this lane first
     Vec<Bits, VEC> v[UNROLL];
@@ -187,6 +173,9 @@ __global__ __launch_bounds__(kEncodeThreads) void encode_kernel(
         }
     }
 
+    const int lb = int(info & 0xFF);
+    const int64_t nblk = (N + (int64_t(1) << lb) - 1) >> lb;
+    const int64_t out0 = info >> 8;
 #pragma unroll
     for (int u = 0; u < UNROLL; ++u) {
         const int64_t c0 = q * CHUNK + int64_t(u) * (kWave * VEC) + int64_t(lane) * VEC;
@@ -223,11 +212,11 @@ hipError_t launch_encode_t(const darb_plan &p, const void *W, int64_t ldw, void 
     Bits *vals = static_cast<Bits *>(values);
     if (aligned)
         hipLaunchKernelGGL((encode_kernel<Bits, true>), dim3(unsigned(blocks)),
-                           dim3(kEncodeThreads), 0, s, w, ldw, p.N, p.d_perm, p.bins, chunks,
+                           dim3(kEncodeThreads), 0, s, w, ldw, p.N, p.d_rowinfo, chunks,
                            int(cgroups), vals, offsets);
     else
         hipLaunchKernelGGL((encode_kernel<Bits, false>), dim3(unsigned(blocks)),
-                           dim3(kEncodeThreads), 0, s, w, ldw, p.N, p.d_perm, p.bins, chunks,
+                           dim3(kEncodeThreads), 0, s, w, ldw, p.N, p.d_rowinfo, chunks,
                            int(cgroups), vals, offsets);
     return hipGetLastError();
 }

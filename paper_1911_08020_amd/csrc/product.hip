@@ -161,7 +161,9 @@ __global__ __launch_bounds__(kSpmvThreads) void spmv_kernel(
     const int64_t e0 = first_elem + row_c * nblk;
     const int nvec = vec_path ? nblk / VEC : nblk;
 
-    // the first round of this lane's vectors, issued before x is staged
+    // the destination row and the first round of this lane's vectors, issued
+    // before x is staged
+    const int32_t dest = perm[first_row + row_c];
     typename WV::V wv[kVmax];
     typename WV::O ov[kVmax];
     const typename WV::V *vrow = reinterpret_cast<const typename WV::V *>(values + e0);
@@ -218,7 +220,7 @@ __global__ __launch_bounds__(kSpmvThreads) void spmv_kernel(
     }
 
     for (int m = L >> 1; m >= 1; m >>= 1) acc += __shfl_xor(acc, m, kWave);
-    if (row_ok && sub == 0) y[perm[first_row + row]] = acc;
+    if (row_ok && sub == 0) y[dest] = acc;
 }
 
 // ---------------------------------------------------------------------------------
