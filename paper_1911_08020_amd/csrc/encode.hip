@@ -99,41 +99,68 @@ __device__ __forceinline__ void small_blocks(const Vec<Bits, VEC> &v, int64_t c0
     }
 }
 
-// Blocks wider than VEC: in-lane candidate, then an xor butterfly over the
-// b / VEC consecutive lanes that hold the block.
-template <typename Bits, int VEC>
-__device__ __forceinline__ void wide_block(const Vec<Bits, VEC> &v, int64_t c0, int lb, int lane,
-                                           int64_t nblk, Bits *__restrict__ values,
-                                           uint8_t *__restrict__ offsets) {
+// Blocks wider than VEC: each lane's candidate, then an xor butterfly over the
+// b / VEC consecutive lanes that hold the block.  The UNROLL vectors of a lane are
+// independent, so every butterfly step shuffles all of them at once and their
+// latencies overlap.
+template <typename Bits, int VEC, int UNROLL>
+__device__ __forceinline__ void wide_blocks(const Vec<Bits, VEC> (&v)[UNROLL], int64_t cbase,
+                                            int lb, int lane, int64_t nblk,
+                                            Bits *__restrict__ values,
+                                            uint8_t *__restrict__ offsets) {
     using Tr = EncodeTraits<Bits>;
     using Key = typename Tr::Key;
     const int b = 1 << lb;
-    const int j0 = int(c0 & (b - 1));
-    Bits best_bits = v.e[0];
-    uint32_t best_mag = uint32_t(v.e[0]) & Tr::MAG;
-    int best = 0;
+    Key key[UNROLL];
 #pragma unroll
-    for (int e = 1; e < VEC; ++e) {
-        const uint32_t mag = uint32_t(v.e[e]) & Tr::MAG;
-        const bool take = mag > best_mag;
-        best_mag = take ? mag : best_mag;
-        best_bits = take ? v.e[e] : best_bits;
-        best = take ? e : best;
+    for (int u = 0; u < UNROLL; ++u) {
+        const int64_t c0 = cbase + int64_t(u) * (kWave * VEC) + int64_t(lane) * VEC;
+        Bits best_bits = v[u].e[0];
+        uint32_t best_mag = uint32_t(v[u].e[0]) & Tr::MAG;
+        int best = 0;
+#pragma unroll
+        for (int e = 1; e < VEC; ++e) {
+            const uint32_t mag = uint32_t(v[u].e[e]) & Tr::MAG;
+            const bool take = mag > best_mag;
+            best_mag = take ? mag : best_mag;
+            best_bits = take ? v[u].e[e] : best_bits;
+            best = take ? e : best;
+        }
+        key[u] = pack_key<Bits>(best_bits, int(c0 & (b - 1)) + best);
     }
-    Key key = pack_key<Bits>(best_bits, j0 + best);
     const int group = b / VEC;                         // 2 .. 32 lanes
     for (int m = 1; m < group; m <<= 1) {
-        const Key other = shfl_xor_key(key, m);
-        key = other > key ? other : key;
+#pragma unroll
+        for (int u = 0; u < UNROLL; ++u) {
+            const Key other = shfl_xor_key(key[u], m);
+            key[u] = other > key[u] ? other : key[u];
+        }
     }
-    const int64_t k = c0 >> lb;
-    if ((lane & (group - 1)) == 0 && k < nblk) {
-        Bits val;
-        int j;
-        unpack_key<Bits>(key, val, j);
-        values[k] = val;
-        offsets[k] = uint8_t(j);
+    if ((lane & (group - 1)) == 0) {
+#pragma unroll
+        for (int u = 0; u < UNROLL; ++u) {
+            const int64_t k = (cbase + int64_t(u) * (kWave * VEC) + int64_t(lane) * VEC) >> lb;
+            if (k < nblk) {
+                Bits val;
+                int j;
+                unpack_key<Bits>(key[u], val, j);
+                values[k] = val;
+                offsets[k] = uint8_t(j);
+            }
+        }
     }
+}
+
+// Blocks of b <= VEC for all UNROLL vectors of the lane.
+template <typename Bits, int VEC, int UNROLL, int LB>
+__device__ __forceinline__ void small_blocks_all(const Vec<Bits, VEC> (&v)[UNROLL], int64_t cbase,
+                                                 int lane, int64_t nblk,
+                                                 Bits *__restrict__ values,
+                                                 uint8_t *__restrict__ offsets) {
+#pragma unroll
+    for (int u = 0; u < UNROLL; ++u)
+        small_blocks<Bits, VEC, LB>(v[u], cbase + int64_t(u) * (kWave * VEC) + int64_t(lane) * VEC,
+                                    nblk, values, offsets);
 }
 
 template <typename Bits, bool ALIGNED>
@@ -176,24 +203,21 @@ __global__ __launch_bounds__(kEncodeThreads) void encode_kernel(
     const int lb = int(info & 0xFF);
     const int64_t nblk = (N + (int64_t(1) << lb) - 1) >> lb;
     const int64_t out0 = info >> 8;
-#pragma unroll
-    for (int u = 0; u < UNROLL; ++u) {
-        const int64_t c0 = q * CHUNK + int64_t(u) * (kWave * VEC) + int64_t(lane) * VEC;
-        // block sizes up to VEC: the lane holds whole blocks (compile-time indices only,
-        // so the loaded vector stays in registers)
-        switch (lb) {
-            case 0: small_blocks<Bits, VEC, 0>(v[u], c0, nblk, values + out0, offsets + out0); break;
-            case 1: small_blocks<Bits, VEC, 1>(v[u], c0, nblk, values + out0, offsets + out0); break;
-            case 2: small_blocks<Bits, VEC, 2>(v[u], c0, nblk, values + out0, offsets + out0); break;
-            case 3:
-                if (VEC >= 8) {
-                    small_blocks<Bits, VEC, 3>(v[u], c0, nblk, values + out0, offsets + out0);
-                    break;
-                }
-                [[fallthrough]];
-            default:
-                wide_block<Bits, VEC>(v[u], c0, lb, lane, nblk, values + out0, offsets + out0);
-        }
+    const int64_t cbase = q * CHUNK;
+    Bits *vo = values + out0;
+    uint8_t *oo = offsets + out0;
+    // one wave-uniform branch on the block size, straight-line code inside
+    switch (lb) {
+        case 0: small_blocks_all<Bits, VEC, UNROLL, 0>(v, cbase, lane, nblk, vo, oo); break;
+        case 1: small_blocks_all<Bits, VEC, UNROLL, 1>(v, cbase, lane, nblk, vo, oo); break;
+        case 2: small_blocks_all<Bits, VEC, UNROLL, 2>(v, cbase, lane, nblk, vo, oo); break;
+        case 3:
+            if (VEC >= 8) {
+                small_blocks_all<Bits, VEC, UNROLL, 3>(v, cbase, lane, nblk, vo, oo);
+                break;
+            }
+            [[fallthrough]];
+        default: wide_blocks<Bits, VEC, UNROLL>(v, cbase, lb, lane, nblk, vo, oo);
     }
 }
 

@@ -110,8 +110,10 @@ __device__ __forceinline__ void stage_x(float *xs, const Tx *__restrict__ x, int
         u32x4 t[SB];
 #pragma unroll
         for (int u = 0; u < SB; ++u) {
-            const int i = base + u * kSpmvThreads + int(threadIdx.x);
-            t[u] = x4[i < nv ? i : nv - 1];
+            if (base + u * kSpmvThreads < nv) {          // wave-uniform: skip empty rounds
+                const int i = base + u * kSpmvThreads + int(threadIdx.x);
+                t[u] = x4[i < nv ? i : nv - 1];
+            }
         }
 #pragma unroll
         for (int u = 0; u < SB; ++u) {
@@ -171,10 +173,12 @@ __global__ __launch_bounds__(kSpmvThreads) void spmv_kernel(
     if (vec_path) {
 #pragma unroll
         for (int t = 0; t < kVmax; ++t) {
-            const int vi = sub + t * L;
-            const int vc = vi < nvec ? vi : nvec - 1;
-            wv[t] = __builtin_nontemporal_load(vrow + vc);
-            ov[t] = orow[vc];
+            if (t * L < nvec) {                          // wave-uniform
+                const int vi = sub + t * L;
+                const int vc = vi < nvec ? vi : nvec - 1;
+                wv[t] = __builtin_nontemporal_load(vrow + vc);
+                ov[t] = orow[vc];
+            }
         }
     }
 
@@ -206,10 +210,12 @@ __global__ __launch_bounds__(kSpmvThreads) void spmv_kernel(
             if (base + L * kVmax >= nvec) break;
 #pragma unroll
             for (int t = 0; t < kVmax; ++t) {
-                const int vi = base + L * kVmax + sub + t * L;
-                const int vc = vi < nvec ? vi : nvec - 1;
-                wv[t] = __builtin_nontemporal_load(vrow + vc);
-                ov[t] = orow[vc];
+                if (base + L * kVmax + t * L < nvec) {   // wave-uniform
+                    const int vi = base + L * kVmax + sub + t * L;
+                    const int vc = vi < nvec ? vi : nvec - 1;
+                    wv[t] = __builtin_nontemporal_load(vrow + vc);
+                    ov[t] = orow[vc];
+                }
             }
         }
     } else {
@@ -471,8 +477,9 @@ bool spmm_schedule(const darb_plan &p, int64_t B, int cpl, ProductSchedule &s) {
     int64_t blocks = 0;
     for (int g = 0; g < s.nbins; ++g) {
         const int64_t nblk = p.bins.nblk[g];
-        // split a row group's weights over up to 8 waves, ~128 weights per wave
-        int lgKS = ilog2_ceil((nblk + 127) / 128);
+        // split a row group's weights over up to 8 waves, >= ~16 weights per wave: many
+        // small workgroups keep every CU's share of the gathers even
+        int lgKS = ilog2_ceil((nblk + 15) / 16);
         if (lgKS > 3) lgKS = 3;
         const int KS = 1 << lgKS;
         const int rows_pb = R * (kSpmmWaves / KS);
