@@ -235,7 +235,7 @@ __global__ __launch_bounds__(kSpmvThreads) void spmv_kernel(
 
 constexpr int kSpmmThreads = 512;
 constexpr int kSpmmWaves = kSpmmThreads / kWave;
-constexpr int kSpmmBatch = 16;        // X rows in flight per lane
+constexpr int kSpmmBatch = 8;         // X rows in flight per lane (more waves beat deeper batches)
 constexpr int kPairsMax = 4096;       // (value, column) pairs staged per round
 constexpr int kStageRounds = 8;       // pair loads per thread in flight while staging
 
