@@ -34,7 +34,6 @@ struct ProductSchedule {
     int32_t log2_lanes[kMaxBins];     // log2 of the lanes that share one row
     int32_t vec[kMaxBins];            // SpMV: elements per vector load (1 = scalar path)
     int32_t ksplit[kMaxBins];         // SpMM: waves that split one row group's weights
-    int32_t log2_kchunk[kMaxBins];    // SpMM: weights per row staged in LDS per round
     int32_t col_slabs;                // SpMM: batch-column slabs per row block
     int32_t stage_loads;              // SpMV: 16-byte loads per thread to stage x
 };

@@ -18,10 +18,13 @@
 //
 // SpMM: lanes map to batch columns (X is [N x B] row-major, so one weight's
 // activations X[c, :] are contiguous), CPL columns per lane with 16-byte loads.
-// A workgroup stages the (value, column) pairs of its rows into LDS with
-// coalesced loads, then its waves split each row's weights (ksplit ways) and
-// gather X rows kSpmmBatch at a time; partial sums meet in LDS in a fixed order.
+// Each wave loads its rows' (value, column) pairs with coalesced loads and
+// broadcasts them across a row's lanes register to register (DPP, swizzle or
+// readlane), gathering X rows kSpmmBatch at a time; up to 8 waves split a row
+// group's weights and their partial sums meet in LDS in a fixed order.
 #include <hip/hip_fp16.h>
+
+#include <utility>
 
 #include "darb_internal.h"
 
@@ -236,8 +239,6 @@ __global__ __launch_bounds__(kSpmvThreads) void spmv_kernel(
 constexpr int kSpmmThreads = 512;
 constexpr int kSpmmWaves = kSpmmThreads / kWave;
 constexpr int kSpmmBatch = 8;         // X rows in flight per lane (more waves beat deeper batches)
-constexpr int kPairsMax = 4096;       // (value, column) pairs staged per round
-constexpr int kStageRounds = 8;       // pair loads per thread in flight while staging
 
 // CPL consecutive batch columns of one X row, loaded at once (16 bytes when CPL > 1).
 template <typename Tx, int CPL> struct XLoad;
@@ -260,31 +261,59 @@ template <> struct XLoad<__half, 8> {
     }
 };
 
-struct Pair {
-    float v;
-    int c;
-};
+template <int Base, typename F, int... Is>
+__device__ __forceinline__ void static_for_impl(F &&f, std::integer_sequence<int, Is...>) {
+    (f(std::integral_constant<int, Base + Is>{}), ...);
+}
+// f(integral_constant<int, i>) for i = Base .. Base + Count - 1, unrolled at compile time
+template <int Base, int Count, typename F> __device__ __forceinline__ void static_for(F &&f) {
+    static_for_impl<Base>(f, std::make_integer_sequence<int, Count>{});
+}
 
-template <typename Tw, typename Tx, int CPL>
+// Value of lane T of the caller's group of 2^LGL consecutive lanes, for every lane
+// of the group (T is a compile-time lane index inside the group).
+template <int LGL, int T> __device__ __forceinline__ int group_bcast(int v) {
+    if constexpr (LGL == 0) {
+        return v;
+    } else if constexpr (LGL == 1) {                      // DPP quad_perm [T, T, 2+T, 2+T]
+        return __builtin_amdgcn_update_dpp(0, v, T | (T << 2) | ((2 + T) << 4) | ((2 + T) << 6),
+                                           0xF, 0xF, false);
+    } else if constexpr (LGL == 2) {                      // DPP quad_perm [T, T, T, T]
+        return __builtin_amdgcn_update_dpp(0, v, T * 0x55, 0xF, 0xF, false);
+    } else if constexpr (LGL == 4) {                      // DPP row_newbcast:T (16-lane rows)
+        return __builtin_amdgcn_update_dpp(0, v, 0x150 + T, 0xF, 0xF, false);
+    } else if constexpr (LGL == 6) {                      // whole wave: through a scalar register
+        return __builtin_amdgcn_readlane(v, T);
+    } else {                                              // 8 or 32 lanes: ds_swizzle bitmask mode
+        constexpr int and_mask = 0x1F & ~((1 << LGL) - 1);
+        return __builtin_amdgcn_ds_swizzle(v, (T << 5) | and_mask);
+    }
+}
+
+// Lanes map to batch columns (CPL per lane, 2^LGL lanes per matrix row, 64 >> LGL
+// rows per wave).  A wave owns a contiguous share [kbeg, kend) of its rows' weights
+// (KS waves split a row group).  The lanes of a row load S = max(2^LGL, 16) of the
+// row's (value, column) pairs per step, one pair per lane and group, straight from
+// HBM with coalesced loads, then broadcast each pair to the row's lanes with a
+// register-to-register exchange and gather its X row; kSpmmBatch gathers are in
+// flight per lane.  Partial sums of the KS waves meet in LDS in a fixed order.
+template <typename Tw, typename Tx, int CPL, int LGL>
 __global__ __launch_bounds__(kSpmmThreads) void spmm_kernel(
     const Tw *__restrict__ values, const uint8_t *__restrict__ offsets,
     const Tx *__restrict__ X, int64_t ldx, int64_t B, float *__restrict__ Y, int64_t ldy,
     const int32_t *__restrict__ perm, int N, BinTable bins, ProductSchedule sch) {
     using XL = XLoad<Tx, CPL>;
-    extern __shared__ __align__(16) unsigned char smem[];
-    Pair *pairs = reinterpret_cast<Pair *>(smem);
-    float *part = reinterpret_cast<float *>(smem + kPairsMax * sizeof(Pair));
+    constexpr int L = 1 << LGL;
+    constexpr int R = kWave >> LGL;                       // rows per wave
+    constexpr int GM = L >= 16 ? 1 : 16 / L;              // pair groups per lane per step
+    constexpr int S = L * GM;                             // weights per row per step
+    __shared__ float part[kSpmmThreads * CPL];
 
     const int g = block_group(sch);
     const int wave = wave_uniform(int(threadIdx.x) / kWave);
     const int lane = int(threadIdx.x) & (kWave - 1);
-    const int lgL = pick(sch.log2_lanes, g);
-    const int L = 1 << lgL;
-    const int R = kWave >> lgL;                  // rows per row group
-    const int KS = pick(sch.ksplit, g);          // waves per row group
-    const int rows_pb = R * (kSpmmWaves / KS);   // rows per workgroup
-    const int lgKC = pick(sch.log2_kchunk, g);
-    const int KC = 1 << lgKC;
+    const int KS = pick(sch.ksplit, g);
+    const int rows_pb = R * (kSpmmWaves / KS);
     const int lb = pick(bins.log2b, g);
     const int nblk = int(pick(bins.nblk, g));
     const int64_t rows = pick(bins.rows, g);
@@ -296,81 +325,59 @@ __global__ __launch_bounds__(kSpmmThreads) void spmm_kernel(
     const int slab = local - row_blk * sch.col_slabs;
     const int64_t row0 = int64_t(row_blk) * rows_pb;
     const int rows_here = int(rows - row0 < rows_pb ? rows - row0 : rows_pb);
-    const Tw *vb = values + first_elem + row0 * nblk;
-    const uint8_t *ob = offsets + first_elem + row0 * nblk;
 
     const int rg = wave / KS, ks = wave - (wave / KS) * KS;
-    const int rl = rg * R + (lane >> lgL);       // row of this lane inside the block
+    const int rl = rg * R + (lane >> LGL);                // row of this lane in the block
     const bool row_ok = rl < rows_here;
-    const int rl_c = row_ok ? rl : 0;
     const int sub = lane & (L - 1);
     const int64_t col0 = (int64_t(slab) * L + sub) * CPL;
-    const bool col_ok = col0 < B;                // CPL > 1 only when CPL divides B
+    const bool col_ok = col0 < B;                         // CPL > 1 only when CPL divides B
     const int64_t col_c = col_ok ? col0 : 0;
-    const int per_wave = KC / KS;
+    const int share = (nblk + KS - 1) / KS;
+    const int kbeg = ks * share;
+    const int kend = kbeg + share < nblk ? kbeg + share : nblk;
+    const int64_t re = first_elem + (row0 + (row_ok ? rl : 0)) * nblk;
+    const Tw *vr = values + re;
+    const uint8_t *orr = offsets + re;
 
     float acc[CPL];
 #pragma unroll
     for (int q = 0; q < CPL; ++q) acc[q] = 0.0f;
 
-    for (int k0 = 0; k0 < nblk; k0 += KC) {
-        const int kc = nblk - k0 < KC ? nblk - k0 : KC;
-        // stage this round's pairs: rows_pb x KC slots, coalesced along each row
-        const int total = rows_pb << lgKC;
-        for (int base = 0; base < total; base += kStageRounds * kSpmmThreads) {
-            float v[kStageRounds];
-            uint32_t o[kStageRounds];
+    for (int k0 = kbeg; k0 < kend; k0 += S) {
+        // this step's pairs: lane `sub` of the row holds weights k0 + gi*L + sub
+        float vl[GM];
+        int cl[GM];
 #pragma unroll
-            for (int u = 0; u < kStageRounds; ++u) {
-                const int idx = base + u * kSpmmThreads + int(threadIdx.x);
-                const int r = idx >> lgKC, kk = idx & (KC - 1);
-                const bool ok = idx < total && r < rows_here && kk < kc;
-                const int64_t e = ok ? int64_t(r) * nblk + k0 + kk : 0;
-                v[u] = to_f32<Tw>(vb[e]);
-                o[u] = ob[e];
-            }
-#pragma unroll
-            for (int u = 0; u < kStageRounds; ++u) {
-                const int idx = base + u * kSpmmThreads + int(threadIdx.x);
-                if (idx < total) {
-                    const int r = idx >> lgKC, kk = idx & (KC - 1);
-                    const bool ok = r < rows_here && kk < kc;
-                    Pair p;
-                    p.v = ok ? v[u] : 0.0f;
-                    const int c = ((k0 + kk) << lb) + int(o[u]);
-                    p.c = ok ? (c < N ? c : N - 1) : -1;   // -1 marks an empty slot
-                    pairs[idx] = p;
-                }
-            }
+        for (int gi = 0; gi < GM; ++gi) {
+            const int k = k0 + gi * L + sub;
+            const bool ok = row_ok && k < kend;
+            const int kc = ok ? k : kbeg;
+            vl[gi] = ok ? to_f32<Tw>(vr[kc]) : 0.0f;
+            const int c = (kc << lb) + int(orr[kc]);
+            cl[gi] = ok ? (c < N ? c : N - 1) : -1;   // the encode gives c < N; clamp anyway
         }
-        __syncthreads();
-
-        // this wave's share of the round: slots [ks*per_wave, (ks+1)*per_wave) of its rows
-        const int kbeg = ks * per_wave;
-        const int kend = kbeg + per_wave < kc ? kbeg + per_wave : kc;
-        const Pair *prow = pairs + (rl_c << lgKC);
-        for (int kk = kbeg; kk < kend; kk += kSpmmBatch) {
-            Pair p[kSpmmBatch];
-#pragma unroll
-            for (int u = 0; u < kSpmmBatch; ++u) {
-                const int s = kk + u < kend ? kk + u : kend - 1;
-                p[u] = prow[s];
-            }
+        static_for<0, S / kSpmmBatch>([&](auto bc) {
+            constexpr int b0 = decltype(bc)::value * kSpmmBatch;
+            float vv[kSpmmBatch];
+            int cc[kSpmmBatch];
             typename XL::V xv[kSpmmBatch];
+            static_for<0, kSpmmBatch>([&](auto uc) {
+                constexpr int f = b0 + decltype(uc)::value;   // weight k0 + f of every row
+                vv[f - b0] = __builtin_bit_cast(
+                    float, group_bcast<LGL, f % L>(__builtin_bit_cast(int, vl[f / L])));
+                cc[f - b0] = group_bcast<LGL, f % L>(cl[f / L]);
+                const int64_t c = cc[f - b0] >= 0 ? cc[f - b0] : 0;
+                xv[f - b0] = XL::load(X + c * ldx + col_c);
+            });
 #pragma unroll
             for (int u = 0; u < kSpmmBatch; ++u) {
-                const int64_t c = p[u].c >= 0 ? p[u].c : 0;
-                xv[u] = XL::load(X + c * ldx + col_c);
-            }
+                if (cc[u] >= 0 && col_ok) {
 #pragma unroll
-            for (int u = 0; u < kSpmmBatch; ++u) {
-                if (kk + u < kend && p[u].c >= 0) {
-#pragma unroll
-                    for (int q = 0; q < CPL; ++q) acc[q] = fmaf(p[u].v, XL::get(xv[u], q), acc[q]);
+                    for (int q = 0; q < CPL; ++q) acc[q] = fmaf(vv[u], XL::get(xv[u], q), acc[q]);
                 }
             }
-        }
-        __syncthreads();
+        });
     }
 
     // combine the KS partial sums of each row group in a fixed order
@@ -379,9 +386,10 @@ __global__ __launch_bounds__(kSpmmThreads) void spmm_kernel(
         for (int q = 0; q < CPL; ++q) part[(wave * kWave + lane) * CPL + q] = acc[q];
         __syncthreads();
         if (ks == 0) {
-            for (int s = 1; s < KS; ++s) {
+            for (int s2 = 1; s2 < KS; ++s2) {
 #pragma unroll
-                for (int q = 0; q < CPL; ++q) acc[q] += part[((wave + s) * kWave + lane) * CPL + q];
+                for (int q = 0; q < CPL; ++q)
+                    acc[q] += part[((wave + s2) * kWave + lane) * CPL + q];
             }
         }
     }
@@ -483,13 +491,8 @@ bool spmm_schedule(const darb_plan &p, int64_t B, int cpl, ProductSchedule &s) {
         if (lgKS > 3) lgKS = 3;
         const int KS = 1 << lgKS;
         const int rows_pb = R * (kSpmmWaves / KS);
-        int lgKC = ilog2_floor(kPairsMax / rows_pb);  // pairs per round fit the LDS buffer
-        const int lgN = ilog2_ceil(nblk);
-        if (lgKC > lgN) lgKC = lgN;
-        if (lgKC < lgKS) lgKC = lgKS;                 // at least one slot per wave
         s.log2_lanes[g] = lgL;
         s.ksplit[g] = KS;
-        s.log2_kchunk[g] = lgKC;
         s.vec[g] = cpl;
         s.block_begin[g] = int32_t(blocks);
         blocks += (p.bins.rows[g] + rows_pb - 1) / rows_pb * slabs;
@@ -497,6 +500,28 @@ bool spmm_schedule(const darb_plan &p, int64_t B, int cpl, ProductSchedule &s) {
     }
     s.block_begin[s.nbins] = int32_t(blocks);
     return true;
+}
+
+template <typename Tw, typename Tx, int CPL>
+hipError_t launch_spmm_cpl(const darb_plan &p, const ProductSchedule &s, const Tw *v,
+                           const uint8_t *offsets, int64_t B, const Tx *x, int64_t ldx, float *Y,
+                           int64_t ldy, hipStream_t st) {
+    const int blocks = s.block_begin[s.nbins];
+    const int N = int(p.N);
+#define DARB_SPMM(LGL)                                                                          \
+    hipLaunchKernelGGL((spmm_kernel<Tw, Tx, CPL, LGL>), dim3(blocks), dim3(kSpmmThreads), 0, st, \
+                       v, offsets, x, ldx, B, Y, ldy, p.d_perm, N, p.bins, s)
+    switch (s.log2_lanes[0]) {
+        case 0: DARB_SPMM(0); break;
+        case 1: DARB_SPMM(1); break;
+        case 2: DARB_SPMM(2); break;
+        case 3: DARB_SPMM(3); break;
+        case 4: DARB_SPMM(4); break;
+        case 5: DARB_SPMM(5); break;
+        default: DARB_SPMM(6); break;
+    }
+#undef DARB_SPMM
+    return hipGetLastError();
 }
 
 template <typename Tw, typename Tx>
@@ -508,21 +533,11 @@ hipError_t launch_spmm_t(const darb_plan &p, const void *values, const uint8_t *
                      ((ldx * int64_t(sizeof(Tx))) % 16 == 0) && (B % CPL == 0);
     ProductSchedule s;
     if (!spmm_schedule(p, B, vec ? CPL : 1, s)) return hipErrorInvalidConfiguration;
-    const int blocks = s.block_begin[s.nbins];
-    if (blocks == 0) return hipSuccess;
+    if (s.block_begin[s.nbins] == 0) return hipSuccess;
     const Tw *v = static_cast<const Tw *>(values);
     const Tx *x = static_cast<const Tx *>(X);
-    const int N = int(p.N);
-    if (vec) {
-        const size_t lds = kPairsMax * sizeof(Pair) + size_t(kSpmmThreads) * CPL * sizeof(float);
-        hipLaunchKernelGGL((spmm_kernel<Tw, Tx, CPL>), dim3(blocks), dim3(kSpmmThreads), lds, st,
-                           v, offsets, x, ldx, B, Y, ldy, p.d_perm, N, p.bins, s);
-    } else {
-        const size_t lds = kPairsMax * sizeof(Pair) + size_t(kSpmmThreads) * sizeof(float);
-        hipLaunchKernelGGL((spmm_kernel<Tw, Tx, 1>), dim3(blocks), dim3(kSpmmThreads), lds, st, v,
-                           offsets, x, ldx, B, Y, ldy, p.d_perm, N, p.bins, s);
-    }
-    return hipGetLastError();
+    if (vec) return launch_spmm_cpl<Tw, Tx, CPL>(p, s, v, offsets, B, x, ldx, Y, ldy, st);
+    return launch_spmm_cpl<Tw, Tx, 1>(p, s, v, offsets, B, x, ldx, Y, ldy, st);
 }
 
 }  // namespace
