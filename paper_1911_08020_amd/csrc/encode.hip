@@ -15,7 +15,10 @@
 // so one unsigned max over an xor butterfly picks the largest magnitude and,
 // among equal magnitudes, the smallest j; the sign travels along to rebuild the
 // value.  Columns past N (tail block) load as +0.0 with their own j, so they can
-// never beat a real column of the same block.
+// never beat a real column of the same block.  The butterfly's lane exchanges are
+// DPP / swizzle register moves chosen at compile time per block size.
+#include <type_traits>
+
 #include "darb_internal.h"
 
 namespace darb {
@@ -58,14 +61,28 @@ __device__ __forceinline__ void unpack_key(typename EncodeTraits<Bits>::Key k, B
     j = 127 - int((uint32_t(k) >> 1) & 127u);
 }
 
-__device__ __forceinline__ uint64_t shfl_xor_key(uint64_t k, int m) {
-    const uint32_t lo = __shfl_xor(uint32_t(k), m, kWave);
-    const uint32_t hi = __shfl_xor(uint32_t(k >> 32), m, kWave);
-    return (uint64_t(hi) << 32) | lo;
+// Partner exchange of a max-butterfly that merges the two halves (M lanes each) of
+// every aligned group of 2M lanes.  Any pairing across the two halves works for a
+// max-reduction: quad_perm swaps for M = 1, 2, the 8- and 16-lane mirrors for
+// M = 4, 8 (all DPP, plain VALU), a swizzle swapping 16-lane halves for M = 16.
+template <int M> __device__ __forceinline__ uint32_t xchg(uint32_t v) {
+    if constexpr (M == 1) {
+        return uint32_t(__builtin_amdgcn_update_dpp(0, int(v), 0xB1, 0xF, 0xF, false));
+    } else if constexpr (M == 2) {
+        return uint32_t(__builtin_amdgcn_update_dpp(0, int(v), 0x4E, 0xF, 0xF, false));
+    } else if constexpr (M == 4) {
+        return uint32_t(__builtin_amdgcn_update_dpp(0, int(v), 0x141, 0xF, 0xF, false));
+    } else if constexpr (M == 8) {
+        return uint32_t(__builtin_amdgcn_update_dpp(0, int(v), 0x140, 0xF, 0xF, false));
+    } else {
+        static_assert(M == 16, "blocks span at most 32 lanes");
+        return uint32_t(__builtin_amdgcn_ds_swizzle(int(v), (0x10 << 10) | 0x1F));
+    }
 }
-__device__ __forceinline__ uint32_t shfl_xor_key(uint32_t k, int m) {
-    return __shfl_xor(k, m, kWave);
+template <int M> __device__ __forceinline__ uint64_t xchg_key(uint64_t k) {
+    return (uint64_t(xchg<M>(uint32_t(k >> 32))) << 32) | xchg<M>(uint32_t(k));
 }
+template <int M> __device__ __forceinline__ uint32_t xchg_key(uint32_t k) { return xchg<M>(k); }
 
 template <typename Bits, int VEC> struct alignas(16) Vec { Bits e[VEC]; };
 
@@ -103,49 +120,58 @@ __device__ __forceinline__ void small_blocks(const Vec<Bits, VEC> &v, int64_t c0
 // b / VEC consecutive lanes that hold the block.  The UNROLL vectors of a lane are
 // independent, so every butterfly step shuffles all of them at once and their
 // latencies overlap.
-template <typename Bits, int VEC, int UNROLL>
+template <typename Bits, int VEC, int UNROLL, int LB>
 __device__ __forceinline__ void wide_blocks(const Vec<Bits, VEC> (&v)[UNROLL], int64_t cbase,
-                                            int lb, int lane, int64_t nblk,
-                                            Bits *__restrict__ values,
+                                            int lane, int64_t nblk, Bits *__restrict__ values,
                                             uint8_t *__restrict__ offsets) {
     using Tr = EncodeTraits<Bits>;
     using Key = typename Tr::Key;
-    const int b = 1 << lb;
-    Key key[UNROLL];
-#pragma unroll
-    for (int u = 0; u < UNROLL; ++u) {
-        const int64_t c0 = cbase + int64_t(u) * (kWave * VEC) + int64_t(lane) * VEC;
-        Bits best_bits = v[u].e[0];
-        uint32_t best_mag = uint32_t(v[u].e[0]) & Tr::MAG;
-        int best = 0;
-#pragma unroll
-        for (int e = 1; e < VEC; ++e) {
-            const uint32_t mag = uint32_t(v[u].e[e]) & Tr::MAG;
-            const bool take = mag > best_mag;
-            best_mag = take ? mag : best_mag;
-            best_bits = take ? v[u].e[e] : best_bits;
-            best = take ? e : best;
-        }
-        key[u] = pack_key<Bits>(best_bits, int(c0 & (b - 1)) + best);
-    }
-    const int group = b / VEC;                         // 2 .. 32 lanes
-    for (int m = 1; m < group; m <<= 1) {
+    constexpr int b = 1 << LB;
+    constexpr int group = b / VEC;                     // 2 .. 32 lanes hold one block
+    if constexpr (group >= 2) {
+        Key key[UNROLL];
 #pragma unroll
         for (int u = 0; u < UNROLL; ++u) {
-            const Key other = shfl_xor_key(key[u], m);
-            key[u] = other > key[u] ? other : key[u];
-        }
-    }
-    if ((lane & (group - 1)) == 0) {
+            const int64_t c0 = cbase + int64_t(u) * (kWave * VEC) + int64_t(lane) * VEC;
+            Bits best_bits = v[u].e[0];
+            uint32_t best_mag = uint32_t(v[u].e[0]) & Tr::MAG;
+            int best = 0;
 #pragma unroll
-        for (int u = 0; u < UNROLL; ++u) {
-            const int64_t k = (cbase + int64_t(u) * (kWave * VEC) + int64_t(lane) * VEC) >> lb;
-            if (k < nblk) {
-                Bits val;
-                int j;
-                unpack_key<Bits>(key[u], val, j);
-                values[k] = val;
-                offsets[k] = uint8_t(j);
+            for (int e = 1; e < VEC; ++e) {
+                const uint32_t mag = uint32_t(v[u].e[e]) & Tr::MAG;
+                const bool take = mag > best_mag;
+                best_mag = take ? mag : best_mag;
+                best_bits = take ? v[u].e[e] : best_bits;
+                best = take ? e : best;
+            }
+            key[u] = pack_key<Bits>(best_bits, int(c0 & (b - 1)) + best);
+        }
+        auto step = [&](auto mc) {
+            constexpr int M = decltype(mc)::value;
+            if constexpr (M < group) {
+#pragma unroll
+                for (int u = 0; u < UNROLL; ++u) {
+                    const Key other = xchg_key<M>(key[u]);
+                    key[u] = other > key[u] ? other : key[u];
+                }
+            }
+        };
+        step(std::integral_constant<int, 1>{});
+        step(std::integral_constant<int, 2>{});
+        step(std::integral_constant<int, 4>{});
+        step(std::integral_constant<int, 8>{});
+        step(std::integral_constant<int, 16>{});
+        if ((lane & (group - 1)) == 0) {
+#pragma unroll
+            for (int u = 0; u < UNROLL; ++u) {
+                const int64_t k = (cbase + int64_t(u) * (kWave * VEC) + int64_t(lane) * VEC) >> LB;
+                if (k < nblk) {
+                    Bits val;
+                    int j;
+                    unpack_key<Bits>(key[u], val, j);
+                    values[k] = val;
+                    offsets[k] = uint8_t(j);
+                }
             }
         }
     }
@@ -207,17 +233,19 @@ __global__ __launch_bounds__(kEncodeThreads) void encode_kernel(
     Bits *vo = values + out0;
     uint8_t *oo = offsets + out0;
     // one wave-uniform branch on the block size, straight-line code inside
+    constexpr int LV = VEC == 4 ? 2 : 3;   // log2 VEC: blocks up to VEC stay inside a lane
     switch (lb) {
         case 0: small_blocks_all<Bits, VEC, UNROLL, 0>(v, cbase, lane, nblk, vo, oo); break;
         case 1: small_blocks_all<Bits, VEC, UNROLL, 1>(v, cbase, lane, nblk, vo, oo); break;
         case 2: small_blocks_all<Bits, VEC, UNROLL, 2>(v, cbase, lane, nblk, vo, oo); break;
         case 3:
-            if (VEC >= 8) {
-                small_blocks_all<Bits, VEC, UNROLL, 3>(v, cbase, lane, nblk, vo, oo);
-                break;
-            }
-            [[fallthrough]];
-        default: wide_blocks<Bits, VEC, UNROLL>(v, cbase, lb, lane, nblk, vo, oo);
+            if constexpr (LV >= 3) small_blocks_all<Bits, VEC, UNROLL, 3>(v, cbase, lane, nblk, vo, oo);
+            else wide_blocks<Bits, VEC, UNROLL, 3>(v, cbase, lane, nblk, vo, oo);
+            break;
+        case 4: wide_blocks<Bits, VEC, UNROLL, 4>(v, cbase, lane, nblk, vo, oo); break;
+        case 5: wide_blocks<Bits, VEC, UNROLL, 5>(v, cbase, lane, nblk, vo, oo); break;
+        case 6: wide_blocks<Bits, VEC, UNROLL, 6>(v, cbase, lane, nblk, vo, oo); break;
+        default: wide_blocks<Bits, VEC, UNROLL, 7>(v, cbase, lane, nblk, vo, oo); break;
     }
 }
 
