@@ -47,22 +47,31 @@ __global__ __launch_bounds__(kThreads) void lstm_cell_kernel(
 }
 
 constexpr int kStreamBlocks = 8192;
+constexpr int kReadUnroll = 4;     // 16-byte loads in flight per thread
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
+// Each workgroup reads one contiguous chunk of kReadUnroll * kThreads 16-byte
+// vectors with non-temporal loads, all issued before they are summed; one float per
+// workgroup goes to sink[blockIdx.x % kStreamBlocks] so the loads are kept.
 __global__ __launch_bounds__(kThreads) void stream_read_kernel(const f32x4 *__restrict__ buf,
                                                                int64_t n16, float *sink) {
-    float s = 0.0f;
-    for (int64_t i = int64_t(blockIdx.x) * kThreads + threadIdx.x; i < n16;
-         i += int64_t(gridDim.x) * kThreads) {
-        const f32x4 v = __builtin_nontemporal_load(buf + i);
-        s += (v[0] + v[1]) + (v[2] + v[3]);
+    const int64_t base = int64_t(blockIdx.x) * (kReadUnroll * kThreads) + threadIdx.x;
+    f32x4 v[kReadUnroll];
+#pragma unroll
+    for (int u = 0; u < kReadUnroll; ++u) {
+        const int64_t i = base + int64_t(u) * kThreads;
+        v[u] = __builtin_nontemporal_load(buf + (i < n16 ? i : n16 - 1));
     }
+    float s = 0.0f;
+#pragma unroll
+    for (int u = 0; u < kReadUnroll; ++u) s += (v[u][0] + v[u][1]) + (v[u][2] + v[u][3]);
     __shared__ float part[kThreads / 64];
     for (int m = 32; m >= 1; m >>= 1) s += __shfl_xor(s, m, 64);
     if ((threadIdx.x & 63) == 0) part[threadIdx.x / 64] = s;
     __syncthreads();
-    if (threadIdx.x == 0) sink[blockIdx.x] = (part[0] + part[1]) + (part[2] + part[3]);
+    if (threadIdx.x == 0)
+        sink[blockIdx.x % kStreamBlocks] = (part[0] + part[1]) + (part[2] + part[3]);
 }
 
 __global__ __launch_bounds__(kThreads) void stream_copy_kernel(float4 *__restrict__ dst,
@@ -106,8 +115,8 @@ hipError_t launch_lstm_cell(int64_t H, int64_t batch, const float *G, const floa
 
 hipError_t launch_stream_read(const void *buf, int64_t bytes, float *sink, hipStream_t s) {
     const int64_t n16 = bytes / 16;
-    int64_t blocks = (n16 + kThreads - 1) / kThreads;
-    if (blocks > kStreamBlocks) blocks = kStreamBlocks;
+    const int64_t blocks = (n16 + kReadUnroll * kThreads - 1) / (kReadUnroll * kThreads);
+    if (blocks > 0x7FFFFFFF) return hipErrorInvalidConfiguration;
     hipLaunchKernelGGL(stream_read_kernel, dim3(unsigned(blocks)), dim3(kThreads), 0, s,
                        static_cast<const f32x4 *>(buf), n16, sink);
     return hipGetLastError();
