@@ -39,7 +39,8 @@ def parse_args(argv=None):
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="fc_9216")
-    ap.add_argument("--batch", type=int, default=64, help="SpMM batch")
+    ap.add_argument("--batch", type=int, default=None,
+                    help="SpMM batch (default: the workload's own; 64 for fc_9216)")
     ap.add_argument("--rotate-w", type=int, default=4)
     ap.add_argument("--rotate-fmt", type=int, default=8)
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
@@ -108,6 +109,121 @@ def cpu_baseline(cfg, mi, x, X, seconds, bytes_per_step):
                       f"{platform.processor() or platform.machine()}"}
 
 
+def bench_lstm(args):
+    """The recurrent workload: 2-layer LSTM, hidden 1024, T = 200, batch 32, fp16 DARB
+    weights, fp32 state.  A step is one forward pass over the whole sequence (both
+    layers, darb_lstm_layer each).  The DARB weights are encoded once before timing
+    (model load); they stay cache-resident, as they would in a serving loop."""
+    import ctypes
+
+    import numpy as np
+    import torch
+
+    import paper_1911_08020_amd as darb
+    import workloads
+
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda", 0)
+    cfg, mats, xs, shp = workloads.make_lstm_inputs(seed=args.seed)
+    H, T, Bt = shp["hidden"], shp["seq_len"], shp["batch"]
+    layers, nnz = [], []
+    for (wih, whh) in mats:
+        pair = []
+        for mi in (wih, whh):
+            plan = darb.Plan(4 * H, H, mi.row_density, mi.matrix_density, darb.ROUND_FLOOR,
+                             cfg.b_min, cfg.b_max).upload()
+            v, o = plan.encode(torch.from_numpy(mi.W).to(dev))
+            pair.append((plan, v, o))
+            nnz.append(plan.nnz)
+        layers.append(tuple(pair))
+    x_seq = torch.from_numpy(xs).to(dev)
+    hs = [torch.empty((H, T * Bt), dtype=torch.float32, device=dev) for _ in layers]
+    hh = [torch.zeros((H, Bt), dtype=torch.float32, device=dev) for _ in layers]
+    cc = [torch.zeros((H, Bt), dtype=torch.float32, device=dev) for _ in layers]
+    ws = torch.empty(4 * H * T * Bt + 4 * H * Bt, dtype=torch.float32, device=dev)
+
+    def sequence():
+        inp = x_seq
+        for l, (wih, whh) in enumerate(layers):
+            hh[l].zero_()
+            cc[l].zero_()
+            darb.lstm_layer(wih, whh, inp, H, T, Bt, h=hh[l], c=cc[l], h_seq=hs[l], workspace=ws)
+            inp = hs[l]
+
+    for _ in range(max(1, args.warmup // 10)):
+        sequence()
+    torch.cuda.synchronize()
+    ref = hs[-1].clone()
+    K = max(1, args.steps // 20)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(K):
+        sequence()
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / K
+    assert torch.equal(hs[-1], ref), "sequence output changed across runs"
+
+    # per-kernel averages of the two product shapes, back-to-back between events
+    stream = torch.cuda.current_stream()
+    lib = darb.lib()
+    P = ctypes.c_void_p
+    plan, v, o = layers[0][0]
+    Uo = torch.empty((4 * H, T * Bt), dtype=torch.float32, device=dev)
+    Go = torch.empty((4 * H, Bt), dtype=torch.float32, device=dev)
+    reps = 50
+    res = {}
+    for name, (pl, vv, oo), X, Y, B in (("input_product", layers[0][0], x_seq, Uo, T * Bt),
+                                        ("recurrent_product", layers[0][1], hh[0], Go, Bt)):
+        a = (pl.handle, darb.F16, P(vv.data_ptr()), P(oo.data_ptr()), darb.F32, B,
+             P(X.data_ptr()), B, P(Y.data_ptr()), B, P(stream.cuda_stream))
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(reps):
+            lib.darb_spmm(*a)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) * 1e3 / reps
+        res[name] = {"avg_us": round(us, 3), "batch": B,
+                     "gflops": round(2 * pl.nnz * B / (us * 1e-6) / 1e9, 1)}
+    flops = sum(2 * n * T * Bt for n in nnz)
+    out = {
+        "metric": "DARB 2-layer LSTM forward tokens/s (hidden 1024, T=200, batch 32)",
+        "value": round(T * Bt / (ms * 1e-3), 1), "unit": "tokens/s", "n_gpus": 1,
+        "steps": K, "warmup": max(1, args.warmup // 10), "ms_per_step": round(ms, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f16",
+        "data": "synthetic: seeded fp16 weights, exact-k irregular densities, N(0,1) inputs",
+        "config": {"workload": "lstm2_seq: 2-layer LSTM, hidden 1024, T=200, batch 32, "
+                               "W_ih and W_hh [4096 x 1024] fp16 DARB (keep 5 %, b 4..64); "
+                               "step = one forward pass over the sequence",
+                   "nnz_per_matrix": nnz},
+        "gflops_step": round(flops / (ms * 1e-3) / 1e9, 1),
+        "kernels": res,
+        "roofline": None,
+        "cpu_baseline": None,
+    }
+    if args.cpu_seconds > 0:
+        import oracle
+        masked = []
+        for (wih, whh) in layers:
+            pair = []
+            for (pl, vv, oo) in (wih, whh):
+                log2b, row_start, perm = pl.export()
+                lay = oracle.layout(pl.N, log2b)
+                pair.append(oracle.decode(vv.cpu().numpy(), oo.cpu().numpy(), lay))
+            masked.append(tuple(pair))
+        from threadpoolctl import threadpool_limits
+        with threadpool_limits(limits=1):
+            t0 = time.perf_counter()
+            oracle.lstm_forward(masked, xs, H, T, Bt)
+            el = time.perf_counter() - t0
+        out["cpu_baseline"] = {"value": round(T * Bt / el, 1), "unit": "tokens/s", "cores": 1,
+                               "kind": "oracle",
+                               "sample": f"one full sequence in {el:.1f} s (numpy fp64 dense "
+                                         "masked products, one BLAS thread)"}
+    print(json.dumps(out), flush=True)
+
+
 def main(argv=None):
     args = parse_args(argv)
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -116,6 +232,9 @@ def main(argv=None):
               "no multi-GPU mode (rows would shard with no communication; see DESIGN.md). "
               "Run with --gpus 1.", file=sys.stderr)
         sys.exit(2)
+
+    if args.workload == "lstm2_seq":
+        return bench_lstm(args)
 
     import numpy as np
     import torch
@@ -166,18 +285,13 @@ def main(argv=None):
     spmm_args = [(h, wcode, P(fmt[j][0].data_ptr()), P(fmt[j][1].data_ptr()), xcode, B,
                   P(Xd[j].data_ptr()), B, P(Y.data_ptr()), B, sp) for j in range(RE)]
 
-    def step(i, ev=None):
-        if ev is not None:
-            ev[0].record(stream)
+    with_spmm = B > 1
+
+    def step(i):
         rc = lib.darb_encode(*enc_args[i % (RW * RE)])
-        if ev is not None:
-            ev[1].record(stream)
         rc |= lib.darb_spmv(*spmv_args[(i + 1) % RE])
-        if ev is not None:
-            ev[2].record(stream)
-        rc |= lib.darb_spmm(*spmm_args[(i + 2) % RE])
-        if ev is not None:
-            ev[3].record(stream)
+        if with_spmm:
+            rc |= lib.darb_spmm(*spmm_args[(i + 2) % RE])
         if rc:
             raise RuntimeError(f"DARB call failed: {lib.darb_last_error().decode()}")
 
@@ -216,10 +330,13 @@ def main(argv=None):
     spmv_rot = [spmv_args[(i + 1) % RE] for i in range(RE)]
     spmm_rot = [spmm_args[(i + 2) % RE] for i in range(RE)]
     avg_us = {"encode": timed_launches(lib.darb_encode, enc_args, K),
-              "spmv": timed_launches(lib.darb_spmv, spmv_rot, K),
-              "spmm": timed_launches(lib.darb_spmm, spmm_rot, K)}
-    names = ["encode", "spmv", "spmm"]
+              "spmv": timed_launches(lib.darb_spmv, spmv_rot, K)}
+    if with_spmm:
+        avg_us["spmm"] = timed_launches(lib.darb_spmm, spmm_rot, K)
+    names = ["encode", "spmv", "spmm"] if with_spmm else ["encode", "spmv"]
     nbytes = step_bytes(cfg.M, cfg.N, plan.nnz, s_w, s_x, B)
+    if not with_spmm:
+        nbytes.pop("spmm")
     flops = {"encode": 0, "spmv": 2 * plan.nnz, "spmm": 2 * plan.nnz * B}
     kernels = {}
     for n in names:
@@ -256,15 +373,8 @@ def main(argv=None):
     del big
     small_n = (nbytes["spmv"] // 16) * 4
     smalls = [torch.empty(small_n, dtype=torch.float32, device=dev) for _ in range(40)]
-    pairs = []
-    for r in range(200):
-        a, b_ = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        a.record(stream)
-        darb.stream_read(smalls[r % 40], sink)
-        b_.record(stream)
-        pairs.append((a, b_))
-    torch.cuda.synchronize()
-    small_us = float(np.mean([a.elapsed_time(b_) * 1e3 for a, b_ in pairs]))
+    small_args = [(P(t.data_ptr()), small_n * 4, P(sink.data_ptr()), sp) for t in smalls]
+    small_us = timed_launches(lib.darb_stream_read, small_args, K)
     small_gbps = small_n * 4 / (small_us * 1e-6) / 1e9
     del smalls
 
@@ -291,7 +401,7 @@ def main(argv=None):
         "config": {
             "workload": f"{cfg.name}: W {cfg.wdtype} [{cfg.M} x {cfg.N}] {cfg.dist}, "
                         f"keep {cfg.keep}, block sizes {cfg.b_min}..{cfg.b_max} (floor rule); "
-                        f"step = encode + SpMV (B=1) + SpMM (B={B})",
+                        f"step = encode + SpMV (B=1)" + (f" + SpMM (B={B})" if with_spmm else ""),
             "M": cfg.M, "N": cfg.N, "nnz": plan.nnz, "spmm_batch": B,
             "bins": {str(1 << b["log2b"]): b["rows"] for b in plan.bins},
             "rotation": {"W_copies": RW, "format_copies": RE},
@@ -302,7 +412,7 @@ def main(argv=None):
             "traffic": traffic.get(dominant),
         },
         "kernels": kernels,
-        "gflops_step": round((flops["spmv"] + flops["spmm"]) / (ms_per_step * 1e-3) / 1e9, 1),
+        "gflops_step": round(sum(flops[n] for n in names) / (ms_per_step * 1e-3) / 1e9, 1),
         "hbm_measured": {"stream_read_4GiB_gbps": round(read_peak, 1),
                          "stream_read_spmv_size_gbps": round(small_gbps, 1),
                          "stream_read_spmv_size_us": round(small_us, 3)},

@@ -320,9 +320,12 @@ __global__ __launch_bounds__(kSpmmThreads) void spmm_kernel(
     const int64_t first_row = pick(bins.first_row, g);
     const int64_t first_elem = pick(bins.first_elem, g);
 
+    // column slab outermost: the workgroups in flight together share one slab of X,
+    // which stays in L2 even when all of X does not
     const int local = int(blockIdx.x) - block_begin_of(sch, g);
-    const int row_blk = local / sch.col_slabs;
-    const int slab = local - row_blk * sch.col_slabs;
+    const int row_blks = int((rows + rows_pb - 1) / rows_pb);
+    const int slab = local / row_blks;
+    const int row_blk = local - slab * row_blks;
     const int64_t row0 = int64_t(row_blk) * rows_pb;
     const int rows_here = int(rows - row0 < rows_pb ? rows - row0 : rows_pb);
 
