@@ -290,6 +290,34 @@ template <int LGL, int T> __device__ __forceinline__ int group_bcast(int v) {
     }
 }
 
+// GM consecutive retained weights of a row (values and offset bytes) for one lane:
+// one vector load each when the bin is aligned for it, element loads otherwise.
+template <typename Tw, int GM> struct PairLoad {
+    struct alignas(GM * sizeof(Tw)) VV { Tw e[GM]; };
+    struct alignas(GM) OV { uint8_t e[GM]; };
+    // vec: the caller guarantees k % GM == 0 and k + GM <= nblk; otherwise every
+    // element index is clamped into the row [0, nblk)
+    __device__ static void load(const Tw *vr, const uint8_t *orr, int k, int nblk, bool vec,
+                                float (&v)[GM], int (&o)[GM]) {
+        if (vec) {
+            const VV a = *reinterpret_cast<const VV *>(vr + k);
+            const OV b = *reinterpret_cast<const OV *>(orr + k);
+#pragma unroll
+            for (int i = 0; i < GM; ++i) {
+                v[i] = to_f32<Tw>(a.e[i]);
+                o[i] = int(b.e[i]);
+            }
+        } else {
+#pragma unroll
+            for (int i = 0; i < GM; ++i) {
+                const int kk = k + i < nblk ? k + i : nblk - 1;
+                v[i] = to_f32<Tw>(vr[kk]);
+                o[i] = int(orr[kk]);
+            }
+        }
+    }
+};
+
 // Lanes map to batch columns (CPL per lane, 2^LGL lanes per matrix row, 64 >> LGL
 // rows per wave).  A wave owns a contiguous share [kbeg, kend) of its rows' weights
 // (KS waves split a row group).  The lanes of a row load S = max(2^LGL, 16) of the
@@ -336,7 +364,9 @@ __global__ __launch_bounds__(kSpmmThreads) void spmm_kernel(
     const int64_t col0 = (int64_t(slab) * L + sub) * CPL;
     const bool col_ok = col0 < B;                         // CPL > 1 only when CPL divides B
     const int64_t col_c = col_ok ? col0 : 0;
-    const int share = (nblk + KS - 1) / KS;
+    // each wave's share is a whole number of steps, so a lane's GM-vector of weights is
+    // either entirely inside [kbeg, kend) or entirely outside
+    const int share = (((nblk + KS - 1) / KS) + S - 1) / S * S;
     const int kbeg = ks * share;
     const int kend = kbeg + share < nblk ? kbeg + share : nblk;
     const int64_t re = first_elem + (row0 + (row_ok ? rl : 0)) * nblk;
@@ -347,18 +377,24 @@ __global__ __launch_bounds__(kSpmmThreads) void spmm_kernel(
 #pragma unroll
     for (int q = 0; q < CPL; ++q) acc[q] = 0.0f;
 
+    const bool vec_pairs = pick(sch.vec, g) != 0;
     for (int k0 = kbeg; k0 < kend; k0 += S) {
-        // this step's pairs: lane `sub` of the row holds weights k0 + gi*L + sub
+        // this step's pairs: lane `sub` of the row holds weights k0 + sub*GM + gi
         float vl[GM];
         int cl[GM];
-#pragma unroll
-        for (int gi = 0; gi < GM; ++gi) {
-            const int k = k0 + gi * L + sub;
+        {
+            const int k = k0 + sub * GM;
             const bool ok = row_ok && k < kend;
-            const int kc = ok ? k : kbeg;
-            vl[gi] = ok ? to_f32<Tw>(vr[kc]) : 0.0f;
-            const int c = (kc << lb) + int(orr[kc]);
-            cl[gi] = ok ? (c < N ? c : N - 1) : -1;   // the encode gives c < N; clamp anyway
+            float v[GM];
+            int o[GM];
+            PairLoad<Tw, GM>::load(vr, orr, ok ? k : kbeg, nblk, vec_pairs, v, o);
+#pragma unroll
+            for (int gi = 0; gi < GM; ++gi) {
+                const bool okg = ok && k + gi < kend;     // element test for the scalar path
+                vl[gi] = okg ? v[gi] : 0.0f;
+                const int c = ((k + gi) << lb) + o[gi];
+                cl[gi] = okg ? (c < N ? c : N - 1) : -1;   // the encode gives c < N
+            }
         }
         static_for<0, S / kSpmmBatch>([&](auto bc) {
             constexpr int b0 = decltype(bc)::value * kSpmmBatch;
@@ -368,8 +404,8 @@ __global__ __launch_bounds__(kSpmmThreads) void spmm_kernel(
             static_for<0, kSpmmBatch>([&](auto uc) {
                 constexpr int f = b0 + decltype(uc)::value;   // weight k0 + f of every row
                 vv[f - b0] = __builtin_bit_cast(
-                    float, group_bcast<LGL, f % L>(__builtin_bit_cast(int, vl[f / L])));
-                cc[f - b0] = group_bcast<LGL, f % L>(cl[f / L]);
+                    float, group_bcast<LGL, f / GM>(__builtin_bit_cast(int, vl[f % GM])));
+                cc[f - b0] = group_bcast<LGL, f / GM>(cl[f % GM]);
                 const int64_t c = cc[f - b0] >= 0 ? cc[f - b0] : 0;
                 xv[f - b0] = XL::load(X + c * ldx + col_c);
             });
@@ -476,7 +512,8 @@ hipError_t launch_spmv_t(const darb_plan &p, const void *values, const uint8_t *
     return hipGetLastError();
 }
 
-bool spmm_schedule(const darb_plan &p, int64_t B, int cpl, ProductSchedule &s) {
+bool spmm_schedule(const darb_plan &p, int64_t B, int cpl, size_t wbytes, const void *values,
+                   const uint8_t *offsets, ProductSchedule &s) {
     s = ProductSchedule{};
     s.nbins = p.bins.nbins;
     const int64_t lanes = (B + cpl - 1) / cpl;        // lanes needed for all columns
@@ -496,7 +533,11 @@ bool spmm_schedule(const darb_plan &p, int64_t B, int cpl, ProductSchedule &s) {
         const int rows_pb = R * (kSpmmWaves / KS);
         s.log2_lanes[g] = lgL;
         s.ksplit[g] = KS;
-        s.vec[g] = cpl;
+        // pairs load as GM-element vectors when every lane's run is aligned for it
+        const int64_t GM = lgL >= 4 ? 1 : (16 >> lgL);
+        s.vec[g] = (GM > 1 && nblk % GM == 0 && p.bins.first_elem[g] % GM == 0 &&
+                    reinterpret_cast<uintptr_t>(values) % (GM * wbytes) == 0 &&
+                    reinterpret_cast<uintptr_t>(offsets) % GM == 0) ? 1 : 0;
         s.block_begin[g] = int32_t(blocks);
         blocks += (p.bins.rows[g] + rows_pb - 1) / rows_pb * slabs;
         if (blocks > 0x7FFFFFFF) return false;
@@ -535,7 +576,8 @@ hipError_t launch_spmm_t(const darb_plan &p, const void *values, const uint8_t *
     const bool vec = (reinterpret_cast<uintptr_t>(X) % 16 == 0) &&
                      ((ldx * int64_t(sizeof(Tx))) % 16 == 0) && (B % CPL == 0);
     ProductSchedule s;
-    if (!spmm_schedule(p, B, vec ? CPL : 1, s)) return hipErrorInvalidConfiguration;
+    if (!spmm_schedule(p, B, vec ? CPL : 1, sizeof(Tw), values, offsets, s))
+        return hipErrorInvalidConfiguration;
     if (s.block_begin[s.nbins] == 0) return hipSuccess;
     const Tw *v = static_cast<const Tw *>(values);
     const Tx *x = static_cast<const Tx *>(X);
