@@ -378,6 +378,33 @@ def main(argv=None):
     small_gbps = small_n * 4 / (small_us * 1e-6) / 1e9
     del smalls
 
+    # context, not a target: the same masked matrix as a dense fp32/fp16 matrix through
+    # torch (hipBLASLt / rocBLAS), rotated like the DARB format
+    Wm = plan.decode(*fmt[0])
+    dense = [Wm.clone() for _ in range(RW)]
+    xs_t = [t.to(Wm.dtype) for t in xd]
+    Xs_t = [t.to(Wm.dtype) for t in Xd]
+    del Wm
+
+    def timed_torch(fn, count):
+        for i in range(3):
+            fn(i)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for i in range(count):
+            fn(i)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e3 / count
+
+    dense_ctx = {"gemv_us": round(timed_torch(
+        lambda i: torch.mv(dense[i % RW], xs_t[i % RE]), K), 3)}
+    if with_spmm:
+        dense_ctx["gemm_us"] = round(timed_torch(
+            lambda i: torch.mm(dense[i % RW], Xs_t[i % RE]), K), 3)
+    del dense, xs_t, Xs_t
+
     traffic = stored_traffic(args.workload, B)
     for n in names:
         kernels[n]["traffic_bytes"] = traffic.get(n)
@@ -417,6 +444,7 @@ def main(argv=None):
                          "stream_read_spmv_size_gbps": round(small_gbps, 1),
                          "stream_read_spmv_size_us": round(small_us, 3)},
         "spmv_frac_of_measured_read_peak": round(kernels["spmv"]["gbps"] / read_peak, 4),
+        "dense_masked_context": dense_ctx,
         "host": {"plan_ms": round(plan_ms, 3), "enqueue_us_per_step": round(host_us, 2)},
     }
     if args.cpu_seconds > 0:
