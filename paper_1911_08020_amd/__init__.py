@@ -10,7 +10,7 @@ arrays are accepted for host-side inputs (row densities).
     y = plan.spmv(values, offsets, x)       # fp32 [M]
     Y = plan.spmm(values, offsets, X)       # X: [N, B], fp32 [M, B]
 
-The library must have been built (``python -m paper_1911_08020_amd.build`` or
+The library must have been built (``python paper_1911_08020_amd/build.py`` or
 ``__graft_entry__.build()``); importing this package fails loudly otherwise.
 """
 from __future__ import annotations
@@ -64,7 +64,7 @@ def _load_library():
     if not os.path.exists(LIB_PATH):
         raise ImportError(
             f"DARB HIP library not built: {LIB_PATH} is missing. "
-            "Run `python -m paper_1911_08020_amd.build` (hipcc, gfx950) first.")
+            "Run `python paper_1911_08020_amd/build.py` (hipcc, gfx950) first.")
     lib = ctypes.CDLL(LIB_PATH)
     P, I64, I = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int
     sig = {

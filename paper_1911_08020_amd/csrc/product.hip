@@ -443,11 +443,6 @@ __global__ __launch_bounds__(kSpmmThreads) void spmm_kernel(
 // host-side schedules and launches
 // ---------------------------------------------------------------------------------
 
-int ilog2_floor(int64_t v) {
-    int l = 0;
-    while ((int64_t(2) << l) <= v) ++l;
-    return l;
-}
 int ilog2_ceil(int64_t v) {
     int l = 0;
     while ((int64_t(1) << l) < v) ++l;

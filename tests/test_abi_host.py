@@ -162,3 +162,12 @@ def test_single_hip_runtime_in_process():
     maps = open("/proc/self/maps").read()
     paths = {ln.split()[-1] for ln in maps.splitlines() if "libamdhip64" in ln}
     assert len(paths) == 1, paths
+
+
+def test_bench_refuses_more_than_one_gpu():
+    import subprocess
+    import sys
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr

@@ -292,3 +292,37 @@ def test_lstm_small(darb):
 def test_lstm_full_workload(darb):
     say("lstm 2 layers, hidden 1024, T=200, batch 32")
     _lstm_case(darb, hidden=None, seq_len=None, batch=None, layers=None, seed=0)
+
+
+# --------------------------------------------------------------------------------
+# paper-mode plans and the benchmark's output contract
+# --------------------------------------------------------------------------------
+
+def test_paper_rounding_mode_end_to_end(darb):
+    say("paper rounding mode: plan, encode, products")
+    cfg, mi, x, X = _config("lstm_1024")
+    plan, lay, vals, offs = encode_both(darb, mi.W, mi.row_density, mi.matrix_density,
+                                        darb.ROUND_PAPER, cfg.b_min, cfg.b_max)
+    y = host(plan.spmv(dev(vals), dev(offs), dev(x)))
+    check_product(y, vals, offs, lay, x, np.float32, "paper-mode spmv")
+    X16 = X[:, :1].repeat(16, axis=1) if X.shape[1] < 16 else X[:, :16]
+    Y = host(plan.spmm(dev(vals), dev(offs), dev(np.ascontiguousarray(X16))))
+    check_product(Y, vals, offs, lay, np.ascontiguousarray(X16), np.float32, "paper-mode spmm")
+
+
+def test_bench_prints_contract_json(darb, capsys):
+    say("bench.py main(): one short run, JSON contract")
+    import json
+
+    import bench
+    bench.main(["--steps", "3", "--warmup", "1", "--cpu-seconds", "0.2"])
+    line = capsys.readouterr().out.strip().splitlines()[-1]
+    d = json.loads(line)
+    for key in ("metric", "value", "unit", "n_gpus", "steps", "warmup", "ms_per_step",
+                "higher_is_better", "scaling", "vs_baseline", "dtype", "data", "config",
+                "roofline", "cpu_baseline"):
+        assert key in d, key
+    assert d["n_gpus"] == 1 and d["steps"] == 3 and d["value"] > 0
+    assert d["roofline"]["bound"] == "hbm" and 0 < d["roofline"]["frac"] < 1.5
+    assert d["cpu_baseline"]["kind"] == "oracle" and d["cpu_baseline"]["cores"] >= 1
+    assert "workload" in d["config"]
