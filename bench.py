@@ -403,6 +403,22 @@ def main(argv=None):
     if with_spmm:
         dense_ctx["gemm_us"] = round(timed_torch(
             lambda i: torch.mm(dense[i % RW], Xs_t[i % RE]), K), 3)
+    # the same masked matrix in CSR (hipSPARSE through torch); CSR keeps every retained
+    # weight's column index (4-8 bytes) instead of DARB's one offset byte
+    if cfg.wdtype == "f32":
+        try:
+            import warnings
+            with warnings.catch_warnings():
+                warnings.simplefilter("ignore")      # torch flags sparse CSR as beta
+                csr = [dense[0].to_sparse_csr() for _ in range(RE)]
+            dense_ctx["csr_spmv_us"] = round(timed_torch(
+                lambda i: torch.mv(csr[i % RE], xs_t[i % RE]), K), 3)
+            if with_spmm:
+                dense_ctx["csr_spmm_us"] = round(timed_torch(
+                    lambda i: torch.mm(csr[i % RE], Xs_t[i % RE]), K), 3)
+            del csr
+        except RuntimeError as e:          # sparse kernels unavailable in this torch build
+            dense_ctx["csr_error"] = str(e)[:120]
     del dense, xs_t, Xs_t
 
     traffic = stored_traffic(args.workload, B)
