@@ -15,6 +15,7 @@ in fp64 (``lstm_forward``).  Functions and the paper passages they follow:
 * ``encode``       -- section 3.1, block-max weight masking, per row with its own b
 * ``decode``       -- the masked dense matrix the format stands for
 * ``spmm``         -- section 2 / 3.2, product over retained weights, offsets select activations
+* ``pack_offsets``  -- section 4.2, log2(b)-bit indices (and ``unpack_offsets``)
 * ``dense_masked_product`` -- the plain definition of the product: a dense fp64 matmul
 * ``lstm_forward`` -- the LSTM recurrence of the recurrent workload on the decoded
                       masked matrices (dense fp64 products)
@@ -76,6 +77,12 @@ def _load():
     lib.oracle_spmm_f64.restype = I
     lib.oracle_spmm_absdot_f64.argtypes = [I64, I64, I, P, P, P, P, I, P, I64, I64, P, I64]
     lib.oracle_spmm_absdot_f64.restype = I
+    lib.oracle_packed_layout.argtypes = [I64, I64, P, P]
+    lib.oracle_packed_layout.restype = I64
+    lib.oracle_pack_offsets.argtypes = [I64, I64, P, P, P, P]
+    lib.oracle_pack_offsets.restype = None
+    lib.oracle_unpack_offsets.argtypes = [I64, I64, P, P, P, P]
+    lib.oracle_unpack_offsets.restype = None
     _lib = lib
     return lib
 
@@ -198,6 +205,33 @@ def spmm_absdot(values: np.ndarray, offsets: np.ndarray, lay: Layout, X: np.ndar
     if rc != 0:
         raise ValueError("malformed DARB format")
     return A[:, 0] if vec else A
+
+
+def packed_layout(lay: Layout):
+    """(total 32-bit words, first word of each block-size group l = 0..7)."""
+    first = np.zeros(8, dtype=np.int64)
+    words = _load().oracle_packed_layout(lay.M, lay.N, _ptr(lay.log2b), _ptr(first))
+    return int(words), first
+
+
+def pack_offsets(offsets: np.ndarray, lay: Layout) -> np.ndarray:
+    """Offsets as log2(b)-bit fields in 32-slot runs of l words per group (section 4.2)."""
+    offsets = np.ascontiguousarray(offsets, dtype=np.uint8)
+    words, _ = packed_layout(lay)
+    out = np.zeros(max(words, 1), dtype=np.uint32)
+    _load().oracle_pack_offsets(lay.M, lay.N, _ptr(lay.log2b), _ptr(lay.row_start),
+                                _ptr(offsets), _ptr(out))
+    return out[:words]
+
+
+def unpack_offsets(packed: np.ndarray, lay: Layout) -> np.ndarray:
+    packed = np.ascontiguousarray(packed, dtype=np.uint32)
+    if packed.size == 0:
+        packed = np.zeros(1, dtype=np.uint32)
+    out = np.zeros(lay.nnz, dtype=np.uint8)
+    _load().oracle_unpack_offsets(lay.M, lay.N, _ptr(lay.log2b), _ptr(lay.row_start),
+                                  _ptr(packed), _ptr(out))
+    return out
 
 
 def dense_masked_product(Wm: np.ndarray, X: np.ndarray) -> np.ndarray:

@@ -255,3 +255,87 @@ int oracle_spmm_absdot_f64(int64_t M, int64_t N, int wdtype, const void *values,
     }
     return ORACLE_OK;
 }
+
+/*
+ * Bit-packed offsets (section 4.2: an index inside a block of size b needs only
+ * log2 b bits).  Within each block-size group (log2 b = l) the group's slots are
+ * numbered j = 0, 1, ... in storage order and cut into runs of 32; run q takes
+ * exactly l 32-bit words, and slot j's offset occupies bits (j mod 32) * l ..
+ * (j mod 32) * l + l - 1 of the run's l words read as one little-endian bit string.
+ * Groups follow each other in storage order; a group of block size 1 takes no
+ * words.  first_word[g] receives each group's first word; returns the total words.
+ */
+int64_t oracle_packed_layout(int64_t M, int64_t N, const uint8_t *log2b, int64_t *first_word) {
+    int64_t words = 0;
+    for (int l = 0; l <= 7; ++l) {
+        int64_t rows = 0;
+        for (int64_t r = 0; r < M; ++r) rows += (log2b[r] == l);
+        int64_t b = (int64_t)1 << l;
+        int64_t slots = rows * ((N + b - 1) / b);
+        first_word[l] = words;
+        words += (slots + 31) / 32 * l;
+    }
+    return words;
+}
+
+void oracle_pack_offsets(int64_t M, int64_t N, const uint8_t *log2b, const int64_t *row_start,
+                         const uint8_t *offsets, uint32_t *packed) {
+    int64_t first_word[8];
+    int64_t words = oracle_packed_layout(M, N, log2b, first_word);
+    for (int64_t w = 0; w < words; ++w) packed[w] = 0u;
+    /* the first slot of each group in the grouped storage order */
+    int64_t group_first_slot[8];
+    for (int l = 0; l <= 7; ++l) group_first_slot[l] = -1;
+    for (int64_t r = 0; r < M; ++r) {
+        int l = log2b[r];
+        if (group_first_slot[l] < 0 || row_start[r] < group_first_slot[l])
+            group_first_slot[l] = row_start[r];
+    }
+    for (int64_t r = 0; r < M; ++r) {
+        int l = log2b[r];
+        if (l == 0) continue;
+        int64_t b = (int64_t)1 << l;
+        int64_t nblk = (N + b - 1) / b;
+        for (int64_t k = 0; k < nblk; ++k) {
+            int64_t j = row_start[r] + k - group_first_slot[l];     /* slot inside its group */
+            int64_t bit = (j % 32) * l;
+            uint32_t *run = packed + first_word[l] + (j / 32) * l;
+            for (int t = 0; t < l; ++t) {                         /* bit by bit, LSB first */
+                uint32_t v = (offsets[row_start[r] + k] >> t) & 1u;
+                int64_t pos = bit + t;
+                run[pos / 32] |= v << (pos % 32);
+            }
+        }
+    }
+}
+
+void oracle_unpack_offsets(int64_t M, int64_t N, const uint8_t *log2b, const int64_t *row_start,
+                           const uint32_t *packed, uint8_t *offsets) {
+    int64_t first_word[8];
+    oracle_packed_layout(M, N, log2b, first_word);
+    int64_t group_first_slot[8];
+    for (int l = 0; l <= 7; ++l) group_first_slot[l] = -1;
+    for (int64_t r = 0; r < M; ++r) {
+        int l = log2b[r];
+        if (group_first_slot[l] < 0 || row_start[r] < group_first_slot[l])
+            group_first_slot[l] = row_start[r];
+    }
+    for (int64_t r = 0; r < M; ++r) {
+        int l = log2b[r];
+        int64_t b = (int64_t)1 << l;
+        int64_t nblk = (N + b - 1) / b;
+        for (int64_t k = 0; k < nblk; ++k) {
+            uint32_t v = 0;
+            if (l > 0) {
+                int64_t j = row_start[r] + k - group_first_slot[l];
+                int64_t bit = (j % 32) * l;
+                const uint32_t *run = packed + first_word[l] + (j / 32) * l;
+                for (int t = 0; t < l; ++t) {
+                    int64_t pos = bit + t;
+                    v |= ((run[pos / 32] >> (pos % 32)) & 1u) << t;
+                }
+            }
+            offsets[row_start[r] + k] = (uint8_t)v;
+        }
+    }
+}

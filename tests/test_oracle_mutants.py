@@ -30,6 +30,10 @@ MUTANTS = {
     "product_sign_flipped": [("y[j] += v *", "y[j] -= v *")],
     "bins_in_wrong_order": [("for (int l = 0; l <= 7; ++l)", "for (int l = 7; l >= 0; --l)")],
     "half_exponent_bias": [("e - 25", "e - 24")],
+    "pack_bit_order": [("uint32_t v = (offsets[row_start[r] + k] >> t) & 1u;",
+                        "uint32_t v = (offsets[row_start[r] + k] >> (l - 1 - t)) & 1u;")],
+    "pack_run_length": [("int64_t bit = (j % 32) * l;\n            uint32_t *run = packed + first_word[l] + (j / 32) * l;",
+                         "int64_t bit = (j % 16) * l;\n            uint32_t *run = packed + first_word[l] + (j / 16) * l;")],
 }
 
 
@@ -85,6 +89,12 @@ def pin_suite(orc):
             Y = orc.spmm(v, o, lay, X)
             ref = np.where(kept, W, 0).astype(np.float64) @ X.astype(np.float64)
             assert np.allclose(Y, ref, rtol=0, atol=1e-12)
+    # packed offsets: the hand example and a round trip through the unmutated reader
+    lay = orc.layout(24, np.array([3], dtype=np.uint8))
+    assert orc.pack_offsets(np.array([5, 1, 7], dtype=np.uint8), lay).tolist() == [461, 0, 0]
+    lay = orc.layout(97, np.array([3, 5, 7, 2], dtype=np.uint8))
+    o = np.random.default_rng(1).integers(0, 4, size=lay.nnz).astype(np.uint8)
+    assert np.array_equal(oracle.unpack_offsets(orc.pack_offsets(o, lay), lay), o)
     # fp16 decoding of a few bit patterns against numpy
     for bits in [0x3C00, 0x0001, 0x7BFF, 0xC000, 0x0400]:
         assert orc.half_to_double(bits) == float(np.array([bits], np.uint16).view(np.float16)[0])

@@ -356,3 +356,44 @@ def test_lstm_forward_matches_torch_lstm():
     assert np.allclose(out, ref, rtol=0, atol=1e-12)
     for l in range(L):
         assert np.allclose(finals[l][1], cn[l].numpy().T, rtol=0, atol=1e-12)
+
+
+# ----------------------------------------------------------------------------------
+# bit-packed offsets (section 4.2: log2(b) bits per index)
+# ----------------------------------------------------------------------------------
+
+def test_packed_offsets_hand_example():
+    # one row of 24 columns, b = 8 (3 bits per index): offsets 5, 1, 7 become the bit
+    # string 101 100 111 (LSB first per field) = 5 + (1 << 3) + (7 << 6) in word 0 of
+    # the group's first run, which is 3 words long
+    lay = oracle.layout(24, np.array([3], dtype=np.uint8))
+    packed = oracle.pack_offsets(np.array([5, 1, 7], dtype=np.uint8), lay)
+    assert packed.tolist() == [5 + (1 << 3) + (7 << 6), 0, 0]
+
+
+def test_packed_offsets_word_counts_and_bits_per_index():
+    N = 300
+    log2b = np.array([0, 1, 2, 3, 4, 5, 6, 7, 3, 3], dtype=np.uint8)
+    lay = oracle.layout(N, log2b)
+    words, first = oracle.packed_layout(lay)
+    want = 0
+    for l in range(8):
+        slots = int((log2b == l).sum()) * -(-N // (1 << l))
+        assert first[l] == want
+        want += -(-slots // 32) * l          # runs of 32 slots, l words each
+    assert words == want
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_packed_offsets_round_trip(seed):
+    rng = np.random.default_rng(seed)
+    M, N = int(rng.integers(1, 60)), int(rng.integers(1, 700))
+    log2b = rng.integers(0, 8, size=M).astype(np.uint8)
+    lay = oracle.layout(N, log2b)
+    W = rng.standard_normal((M, N)).astype(np.float32)
+    v, o = oracle.encode(W, lay)
+    packed = oracle.pack_offsets(o, lay)
+    assert np.array_equal(oracle.unpack_offsets(packed, lay), o)
+    # each index occupies exactly log2 b bits: count the set bits both ways
+    ones = sum(bin(int(w)).count("1") for w in packed)
+    assert ones == sum(bin(int(x)).count("1") for x in o)
