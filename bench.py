@@ -349,6 +349,37 @@ def main(argv=None):
         }
     dominant = max(names, key=lambda n: kernels[n]["avg_us"])
 
+    # the paper's storage form: offsets bit-packed to log2 b bits (section 4.2).  The
+    # conversion from the encode's bytes and both products on the packed form, same
+    # rotation; outputs must equal the byte-offset products bit for bit.
+    packed = [plan.empty_packed(dev) for _ in range(RE)]
+    for j in range(RE):
+        plan.pack_offsets(fmt[j][1], packed[j])
+    torch.cuda.synchronize()
+    pack_args = [(h, P(fmt[j][1].data_ptr()), P(packed[j].data_ptr()), sp) for j in range(RE)]
+    pk_spmv = [(h, wcode, P(fmt[j][0].data_ptr()), P(packed[j].data_ptr()), xcode,
+                P(xd[j].data_ptr()), P(y.data_ptr()), sp) for j in range(RE)]
+    pk_spmm = [(h, wcode, P(fmt[j][0].data_ptr()), P(packed[j].data_ptr()), xcode, B,
+                P(Xd[j].data_ptr()), B, P(Y.data_ptr()), B, sp) for j in range(RE)]
+    pw = plan.packed_words
+    pk_bytes = {"pack": plan.nnz + 4 * pw,
+                "spmv": plan.nnz * s_w + 4 * pw + cfg.N * s_x + 8 * cfg.M,
+                "spmm": plan.nnz * s_w + 4 * pw + cfg.N * B * s_x + 4 * cfg.M * B + 4 * cfg.M}
+    pk_us = {"pack": timed_launches(lib.darb_pack_offsets, pack_args, K),
+             "spmv": timed_launches(lib.darb_spmv_packed, pk_spmv, K)}
+    pk_same = bool(torch.equal(y.view(torch.int32), y_ref.view(torch.int32)))
+    if with_spmm:
+        pk_us["spmm"] = timed_launches(lib.darb_spmm_packed, pk_spmm, K)
+        pk_same = pk_same and bool(torch.equal(Y.view(torch.int32), Y_ref.view(torch.int32)))
+    packed_ctx = {"words": pw, "bits_per_index": round(32.0 * pw / plan.nnz, 3),
+                  "format_bytes": plan.nnz * s_w + 4 * pw,
+                  "equals_byte_offset_products": pk_same}
+    for n, us in pk_us.items():
+        gbps = pk_bytes[n] / (us * 1e-6) / 1e9
+        packed_ctx[n] = {"avg_us": round(us, 3), "bytes": int(pk_bytes[n]), "gbps": round(gbps, 1),
+                         "frac_hbm_peak": round(gbps / HBM_PEAK_GBPS, 4)}
+    del packed
+
     # HBM reference rates measured in the same process: a plain stream read over
     # 4 GiB, and over buffers the size of the SpMV's bytes rotated past the cache
     # a plain copy of known size: its FETCH_SIZE / WRITE_SIZE counters calibrate the
@@ -460,6 +491,7 @@ def main(argv=None):
                          "stream_read_spmv_size_gbps": round(small_gbps, 1),
                          "stream_read_spmv_size_us": round(small_us, 3)},
         "spmv_frac_of_measured_read_peak": round(kernels["spmv"]["gbps"] / read_peak, 4),
+        "packed_offsets": packed_ctx,
         "dense_masked_context": dense_ctx,
         "host": {"plan_ms": round(plan_ms, 3), "enqueue_us_per_step": round(host_us, 2)},
     }

@@ -9,7 +9,8 @@
  *     may be shorter);
  *   - each block keeps exactly one weight, its largest-magnitude element
  *     (block-max weight masking, section 3.1), together with that element's
- *     position inside the block (a log2(b_r)-bit index, held here in one byte).
+ *     position inside the block (a log2(b_r)-bit index, held either in one
+ *     byte or bit-packed, see darb_pack_offsets).
  *
  * Storage order ("grouped layout"): rows are grouped by block size, smallest
  * block size first, rows of one group in ascending original index, and the
@@ -73,12 +74,14 @@ typedef struct {
     int64_t rows;       /* rows in the group                               */
     int64_t first_elem; /* slot of the group's first retained weight       */
     int64_t nblk;       /* retained weights per row = ceil(N / b)          */
+    int64_t first_word; /* packed offsets: the group's first 32-bit word   */
 } darb_bin;
 
 typedef struct {
     int64_t M, N;
     int64_t nnz;             /* retained weights = sum_r ceil(N / b_r)    */
     int64_t workspace_bytes; /* device workspace darb_plan_upload needs   */
+    int64_t packed_words;    /* uint32 words of the bit-packed offsets    */
     int32_t nbins;           /* non-empty block-size groups, <= 8         */
     int32_t reserved;
     darb_bin bins[8];        /* ascending block size                      */
@@ -171,6 +174,39 @@ int darb_spmv(const darb_plan *plan, int wdtype, const void *values, const uint8
 int darb_spmm(const darb_plan *plan, int wdtype, const void *values, const uint8_t *offsets,
               int xdtype, int64_t B, const void *X, int64_t ldx, float *Y, int64_t ldy,
               void *stream);
+
+/*
+ * Bit-packed offsets (section 4.2: the kept weight's position inside a block of
+ * size b needs log2 b bits, not a byte).  Layout: inside each block-size group
+ * (log2 b = l) the retained weights are numbered j = 0, 1, ... in storage order
+ * and cut into runs of 32; run j / 32 occupies l consecutive uint32 words, and
+ * weight j's index is bits (j % 32) * l ... (j % 32) * l + l - 1 of its run read
+ * as one little-endian bit string (bit i of the run is bit i % 32 of word i / 32).
+ * Groups follow each other in ascending block size starting at word
+ * bins[g].first_word; a group with b = 1 has no words (every index is 0).  The
+ * whole form is info.packed_words words, which may be 0 (then `packed` may be
+ * NULL).  `packed` is device memory, 4-byte aligned.
+ *
+ * darb_pack_offsets converts the byte offsets darb_encode writes (every one must
+ * be < b; only its low log2 b bits are stored) to the packed form, overwriting
+ * every packed word; darb_unpack_offsets converts back, writing all nnz bytes.
+ * Errors: DARB_E_INVALID, DARB_E_NOT_UPLOADED, DARB_E_HIP.
+ */
+int darb_pack_offsets(const darb_plan *plan, const uint8_t *offsets, uint32_t *packed,
+                      void *stream);
+int darb_unpack_offsets(const darb_plan *plan, const uint32_t *packed, uint8_t *offsets,
+                        void *stream);
+
+/*
+ * darb_spmv and darb_spmm reading the offsets in the packed form above.  Every
+ * other argument, and the result bit for bit, is as for the byte-offset calls.
+ * Errors: DARB_E_INVALID, DARB_E_DTYPE, DARB_E_NOT_UPLOADED, DARB_E_HIP.
+ */
+int darb_spmv_packed(const darb_plan *plan, int wdtype, const void *values,
+                     const uint32_t *packed, int xdtype, const void *x, float *y, void *stream);
+int darb_spmm_packed(const darb_plan *plan, int wdtype, const void *values,
+                     const uint32_t *packed, int xdtype, int64_t B, const void *X, int64_t ldx,
+                     float *Y, int64_t ldy, void *stream);
 
 /*
  * One LSTM layer over a sequence with DARB-stored weights (the recurrent

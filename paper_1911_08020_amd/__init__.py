@@ -9,6 +9,8 @@ arrays are accepted for host-side inputs (row densities).
     values, offsets = plan.encode(W)        # W: cuda tensor [M, N] fp32/fp16
     y = plan.spmv(values, offsets, x)       # fp32 [M]
     Y = plan.spmm(values, offsets, X)       # X: [N, B], fp32 [M, B]
+    packed = plan.pack_offsets(offsets)     # log2 b bits per weight (section 4.2)
+    y = plan.spmv_packed(values, packed, x) # same result, bit for bit
 
 The library must have been built (``python paper_1911_08020_amd/build.py`` or
 ``__graft_entry__.build()``); importing this package fails loudly otherwise.
@@ -47,12 +49,14 @@ class DarbError(RuntimeError):
 class _Bin(ctypes.Structure):
     _fields_ = [("log2b", ctypes.c_int32), ("reserved", ctypes.c_int32),
                 ("first_row", ctypes.c_int64), ("rows", ctypes.c_int64),
-                ("first_elem", ctypes.c_int64), ("nblk", ctypes.c_int64)]
+                ("first_elem", ctypes.c_int64), ("nblk", ctypes.c_int64),
+                ("first_word", ctypes.c_int64)]
 
 
 class _Info(ctypes.Structure):
     _fields_ = [("M", ctypes.c_int64), ("N", ctypes.c_int64), ("nnz", ctypes.c_int64),
-                ("workspace_bytes", ctypes.c_int64), ("nbins", ctypes.c_int32),
+                ("workspace_bytes", ctypes.c_int64), ("packed_words", ctypes.c_int64),
+                ("nbins", ctypes.c_int32),
                 ("reserved", ctypes.c_int32), ("bins", _Bin * 8)]
 
 
@@ -80,6 +84,10 @@ def _load_library():
         "darb_decode": ([P, I, P, P, P, I64, P], I),
         "darb_spmv": ([P, I, P, P, I, P, P, P], I),
         "darb_spmm": ([P, I, P, P, I, I64, P, I64, P, I64, P], I),
+        "darb_pack_offsets": ([P, P, P, P], I),
+        "darb_unpack_offsets": ([P, P, P, P], I),
+        "darb_spmv_packed": ([P, I, P, P, I, P, P, P], I),
+        "darb_spmm_packed": ([P, I, P, P, I, I64, P, I64, P, I64, P], I),
         "darb_lstm_layer": ([P, P, P, P, P, P, I, I64, I64, I64, P, P, P, P, P, I64, P], I),
         "darb_stream_read": ([P, I64, P, P], I),
         "darb_stream_copy": ([P, P, I64, P], I),
@@ -96,6 +104,7 @@ _lib = _load_library()
 #: every symbol include/darb.h declares
 EXPORTED = ("darb_plan_create", "darb_plan_info", "darb_plan_export", "darb_plan_upload",
             "darb_plan_destroy", "darb_encode", "darb_decode", "darb_spmv", "darb_spmm",
+            "darb_pack_offsets", "darb_unpack_offsets", "darb_spmv_packed", "darb_spmm_packed",
             "darb_lstm_layer", "darb_stream_read", "darb_stream_copy", "darb_strerror",
             "darb_last_error", "darb_version")
 
@@ -143,6 +152,14 @@ def _require_cuda(*ts):
             raise ValueError("device tensors required (torch cuda tensors)")
 
 
+def _check_format(t, n: int, name: str, dtypes=None):
+    """A flat device buffer of at least n elements (of one of `dtypes`)."""
+    if dtypes is not None and t.dtype not in dtypes:
+        raise TypeError(f"{name} must be one of {dtypes}, got {t.dtype}")
+    if not t.is_contiguous() or t.numel() < n:
+        raise ValueError(f"{name} must be contiguous with >= {n} elements, got {t.numel()}")
+
+
 def _row_major_ld(t, rows: int, cols: int, name: str) -> int:
     if t.dim() != 2 or t.shape[0] != rows or t.shape[1] != cols:
         raise ValueError(f"{name} must be [{rows}, {cols}], got {tuple(t.shape)}")
@@ -168,8 +185,9 @@ class Plan:
         _check(_lib.darb_plan_info(h, ctypes.byref(info)), "darb_plan_info")
         self.M, self.N, self.nnz = info.M, info.N, info.nnz
         self.workspace_bytes = info.workspace_bytes
+        self.packed_words = info.packed_words
         self.bins = [dict(log2b=b.log2b, first_row=b.first_row, rows=b.rows,
-                          first_elem=b.first_elem, nblk=b.nblk)
+                          first_elem=b.first_elem, nblk=b.nblk, first_word=b.first_word)
                      for b in info.bins[:info.nbins]]
         self.workspace = None
 
@@ -215,6 +233,10 @@ class Plan:
         ldw = _row_major_ld(W, self.M, self.N, "W")
         if values is None or offsets is None:
             values, offsets = self.empty_format(W.dtype, W.device)
+        _require_cuda(values, offsets)
+        self._check_values_offsets(values, offsets)
+        if values.dtype != W.dtype:
+            raise TypeError("values must have W's dtype")
         _check(_lib.darb_encode(self._h, _dtype_code(W), _ptr(W), ldw, _ptr(values),
                                 _ptr(offsets), _stream_ptr(stream)), "darb_encode")
         return values, offsets
@@ -222,8 +244,11 @@ class Plan:
     def decode(self, values, offsets, out=None, stream=None):
         torch = _torch()
         _require_cuda(values, offsets)
+        self._check_values_offsets(values, offsets)
         if out is None:
             out = torch.empty((self.M, self.N), dtype=values.dtype, device=values.device)
+        if out.dtype != values.dtype:
+            raise TypeError("out must have the values' dtype")
         ldw = _row_major_ld(out, self.M, self.N, "out")
         _check(_lib.darb_decode(self._h, _dtype_code(values), _ptr(values), _ptr(offsets),
                                 _ptr(out), ldw, _stream_ptr(stream)), "darb_decode")
@@ -232,10 +257,8 @@ class Plan:
     def spmv(self, values, offsets, x, y=None, stream=None):
         torch = _torch()
         _require_cuda(values, offsets, x)
-        if x.dim() != 1 or x.shape[0] != self.N or not x.is_contiguous():
-            raise ValueError(f"x must be a contiguous [{self.N}] tensor")
-        if y is None:
-            y = torch.empty(self.M, dtype=torch.float32, device=x.device)
+        self._check_values_offsets(values, offsets)
+        y = self._vector_out(x, y)
         _check(_lib.darb_spmv(self._h, _dtype_code(values), _ptr(values), _ptr(offsets),
                               _dtype_code(x), _ptr(x), _ptr(y), _stream_ptr(stream)),
                "darb_spmv")
@@ -244,17 +267,97 @@ class Plan:
     def spmm(self, values, offsets, X, Y=None, stream=None):
         torch = _torch()
         _require_cuda(values, offsets, X)
+        self._check_values_offsets(values, offsets)
+        B, ldx, Y, ldy = self._matrix_out(X, Y)
+        _check(_lib.darb_spmm(self._h, _dtype_code(values), _ptr(values), _ptr(offsets),
+                              _dtype_code(X), B, _ptr(X), ldx, _ptr(Y), ldy,
+                              _stream_ptr(stream)), "darb_spmm")
+        return Y
+
+    # -- bit-packed offsets (section 4.2) ---------------------------------------------
+    def empty_packed(self, device=None):
+        torch = _torch()
+        dev = self.workspace.device if device is None else device
+        return torch.empty(max(self.packed_words, 1), dtype=torch.int32, device=dev)
+
+    def pack_offsets(self, offsets, packed=None, stream=None):
+        """Byte offsets [nnz] -> packed words (int32 tensor holding the uint32 words)."""
+        torch = _torch()
+        _require_cuda(offsets)
+        _check_format(offsets, self.nnz, "offsets", (torch.uint8,))
+        if packed is None:
+            packed = self.empty_packed(offsets.device)
+        self._check_packed(packed)
+        _check(_lib.darb_pack_offsets(self._h, _ptr(offsets), _ptr(packed), _stream_ptr(stream)),
+               "darb_pack_offsets")
+        return packed
+
+    def unpack_offsets(self, packed, offsets=None, stream=None):
+        torch = _torch()
+        _require_cuda(packed)
+        self._check_packed(packed)
+        if offsets is None:
+            offsets = torch.empty(self.nnz, dtype=torch.uint8, device=packed.device)
+        _check_format(offsets, self.nnz, "offsets", (torch.uint8,))
+        _check(_lib.darb_unpack_offsets(self._h, _ptr(packed), _ptr(offsets),
+                                        _stream_ptr(stream)), "darb_unpack_offsets")
+        return offsets
+
+    def spmv_packed(self, values, packed, x, y=None, stream=None):
+        _require_cuda(values, packed, x)
+        self._check_values(values)
+        self._check_packed(packed)
+        y = self._vector_out(x, y)
+        _check(_lib.darb_spmv_packed(self._h, _dtype_code(values), _ptr(values), _ptr(packed),
+                                     _dtype_code(x), _ptr(x), _ptr(y), _stream_ptr(stream)),
+               "darb_spmv_packed")
+        return y
+
+    def spmm_packed(self, values, packed, X, Y=None, stream=None):
+        _require_cuda(values, packed, X)
+        self._check_values(values)
+        self._check_packed(packed)
+        B, ldx, Y, ldy = self._matrix_out(X, Y)
+        _check(_lib.darb_spmm_packed(self._h, _dtype_code(values), _ptr(values), _ptr(packed),
+                                     _dtype_code(X), B, _ptr(X), ldx, _ptr(Y), ldy,
+                                     _stream_ptr(stream)), "darb_spmm_packed")
+        return Y
+
+    # -- argument checks --------------------------------------------------------------
+    def _check_values(self, values):
+        torch = _torch()
+        _check_format(values, self.nnz, "values", (torch.float32, torch.float16))
+
+    def _check_values_offsets(self, values, offsets):
+        torch = _torch()
+        self._check_values(values)
+        _check_format(offsets, self.nnz, "offsets", (torch.uint8,))
+
+    def _check_packed(self, packed):
+        torch = _torch()
+        _check_format(packed, self.packed_words, "packed", (torch.int32,))
+
+    def _vector_out(self, x, y):
+        torch = _torch()
+        if x.dim() != 1 or x.shape[0] != self.N or not x.is_contiguous():
+            raise ValueError(f"x must be a contiguous [{self.N}] tensor")
+        if y is None:
+            y = torch.empty(self.M, dtype=torch.float32, device=x.device)
+        _check_format(y, self.M, "y", (torch.float32,))
+        return y
+
+    def _matrix_out(self, X, Y):
+        torch = _torch()
         if X.dim() != 2 or X.shape[0] != self.N:
             raise ValueError(f"X must be [{self.N}, B]")
         B = X.shape[1]
         ldx = _row_major_ld(X, self.N, B, "X")
         if Y is None:
             Y = torch.empty((self.M, B), dtype=torch.float32, device=X.device)
+        if Y.dtype != torch.float32:
+            raise TypeError("Y must be fp32")
         ldy = _row_major_ld(Y, self.M, B, "Y")
-        _check(_lib.darb_spmm(self._h, _dtype_code(values), _ptr(values), _ptr(offsets),
-                              _dtype_code(X), B, _ptr(X), ldx, _ptr(Y), ldy,
-                              _stream_ptr(stream)), "darb_spmm")
-        return Y
+        return B, ldx, Y, ldy
 
 
 def lstm_layer(wih: Tuple[Plan, object, object], whh: Tuple[Plan, object, object], x_seq,

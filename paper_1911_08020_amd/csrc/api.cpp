@@ -54,7 +54,7 @@ using namespace darb;
 
 extern "C" {
 
-int darb_version(void) { return 100; }
+int darb_version(void) { return 200; }
 
 const char *darb_strerror(int code) {
     switch (code) {
@@ -114,7 +114,7 @@ int darb_plan_create(int64_t M, int64_t N, const double *row_density, double mat
     }
     // grouped layout: groups by ascending block size, rows ascending inside
     int64_t group_row[kMaxBins], group_elem[kMaxBins];
-    int64_t row = 0, elem = 0;
+    int64_t row = 0, elem = 0, words = 0;
     BinTable &bt = p->bins;
     bt.nbins = 0;
     for (int l = 0; l <= kMaxLog2B; ++l) {
@@ -128,11 +128,15 @@ int darb_plan_create(int64_t M, int64_t N, const double *row_density, double mat
             bt.rows[g] = count[l];
             bt.first_elem[g] = elem;
             bt.nblk[g] = nblk;
+            bt.first_word[g] = words;
         }
         row += count[l];
         elem += count[l] * nblk;
+        // packed offsets (section 4.2): runs of 32 weights, log2 b words per run
+        words += (count[l] * nblk + 31) / 32 * l;
     }
     p->nnz = elem;
+    p->packed_words = words;
     for (int64_t r = 0; r < M; ++r) {
         const int l = p->log2b[r];
         const int64_t nblk = (N + (int64_t(1) << l) - 1) >> l;
@@ -154,6 +158,7 @@ int darb_plan_info(const darb_plan *p, darb_plan_info_t *info) {
     info->N = p->N;
     info->nnz = p->nnz;
     info->workspace_bytes = p->workspace_bytes;
+    info->packed_words = p->packed_words;
     info->nbins = p->bins.nbins;
     for (int g = 0; g < p->bins.nbins; ++g) {
         info->bins[g].log2b = p->bins.log2b[g];
@@ -161,6 +166,7 @@ int darb_plan_info(const darb_plan *p, darb_plan_info_t *info) {
         info->bins[g].rows = p->bins.rows[g];
         info->bins[g].first_elem = p->bins.first_elem[g];
         info->bins[g].nblk = p->bins.nblk[g];
+        info->bins[g].first_word = p->bins.first_word[g];
     }
     return DARB_OK;
 }
@@ -279,8 +285,15 @@ int darb_spmv(const darb_plan *p, int wdtype, const void *values, const uint8_t 
     rc = check_product_dtypes(wdtype, xdtype);
     if (rc) return rc;
     if (!values || !offsets || !x || !y) return fail(DARB_E_INVALID, "NULL buffer");
-    return launched(launch_spmv(*p, wdtype, values, offsets, xdtype, x, y,
+    return launched(launch_spmv(*p, wdtype, values, offsets, nullptr, xdtype, x, y,
                                 static_cast<hipStream_t>(stream)), "spmv launch");
+}
+
+static int check_batch(int64_t B, int64_t ldx, int64_t ldy) {
+    if (B < 1 || B >= (int64_t(1) << 31)) return fail(DARB_E_INVALID, "B must be in [1, 2^31)");
+    if (ldx < B) return fail(DARB_E_INVALID, "ldx < B");
+    if (ldy < B) return fail(DARB_E_INVALID, "ldy < B");
+    return DARB_OK;
 }
 
 int darb_spmm(const darb_plan *p, int wdtype, const void *values, const uint8_t *offsets,
@@ -292,11 +305,73 @@ int darb_spmm(const darb_plan *p, int wdtype, const void *values, const uint8_t 
     rc = check_product_dtypes(wdtype, xdtype);
     if (rc) return rc;
     if (!values || !offsets || !X || !Y) return fail(DARB_E_INVALID, "NULL buffer");
-    if (B < 1 || B >= (int64_t(1) << 31)) return fail(DARB_E_INVALID, "B must be in [1, 2^31)");
-    if (ldx < B) return fail(DARB_E_INVALID, "ldx < B");
-    if (ldy < B) return fail(DARB_E_INVALID, "ldy < B");
-    return launched(launch_spmm(*p, wdtype, values, offsets, xdtype, B, X, ldx, Y, ldy,
+    rc = check_batch(B, ldx, ldy);
+    if (rc) return rc;
+    return launched(launch_spmm(*p, wdtype, values, offsets, nullptr, xdtype, B, X, ldx, Y, ldy,
                                 static_cast<hipStream_t>(stream)), "spmm launch");
+}
+
+// The packed words: required (and 4-byte aligned) unless the plan has none.
+static int check_packed(const darb_plan *p, const uint32_t *packed) {
+    if (!packed && p->packed_words > 0) return fail(DARB_E_INVALID, "packed is NULL");
+    if (reinterpret_cast<uintptr_t>(packed) & 3)
+        return fail(DARB_E_INVALID, "packed must be 4-byte aligned");
+    return DARB_OK;
+}
+
+int darb_pack_offsets(const darb_plan *p, const uint8_t *offsets, uint32_t *packed,
+                      void *stream) {
+    clear_error();
+    int rc = check_uploaded(p);
+    if (rc) return rc;
+    if (!offsets) return fail(DARB_E_INVALID, "NULL buffer");
+    rc = check_packed(p, packed);
+    if (rc) return rc;
+    return launched(launch_pack_offsets(*p, offsets, packed, static_cast<hipStream_t>(stream)),
+                    "pack launch");
+}
+
+int darb_unpack_offsets(const darb_plan *p, const uint32_t *packed, uint8_t *offsets,
+                        void *stream) {
+    clear_error();
+    int rc = check_uploaded(p);
+    if (rc) return rc;
+    if (!offsets) return fail(DARB_E_INVALID, "NULL buffer");
+    rc = check_packed(p, packed);
+    if (rc) return rc;
+    return launched(launch_unpack_offsets(*p, packed, offsets, static_cast<hipStream_t>(stream)),
+                    "unpack launch");
+}
+
+int darb_spmv_packed(const darb_plan *p, int wdtype, const void *values, const uint32_t *packed,
+                     int xdtype, const void *x, float *y, void *stream) {
+    clear_error();
+    int rc = check_uploaded(p);
+    if (rc) return rc;
+    rc = check_product_dtypes(wdtype, xdtype);
+    if (rc) return rc;
+    if (!values || !x || !y) return fail(DARB_E_INVALID, "NULL buffer");
+    rc = check_packed(p, packed);
+    if (rc) return rc;
+    return launched(launch_spmv(*p, wdtype, values, nullptr, packed, xdtype, x, y,
+                                static_cast<hipStream_t>(stream)), "spmv (packed) launch");
+}
+
+int darb_spmm_packed(const darb_plan *p, int wdtype, const void *values, const uint32_t *packed,
+                     int xdtype, int64_t B, const void *X, int64_t ldx, float *Y, int64_t ldy,
+                     void *stream) {
+    clear_error();
+    int rc = check_uploaded(p);
+    if (rc) return rc;
+    rc = check_product_dtypes(wdtype, xdtype);
+    if (rc) return rc;
+    if (!values || !X || !Y) return fail(DARB_E_INVALID, "NULL buffer");
+    rc = check_packed(p, packed);
+    if (rc) return rc;
+    rc = check_batch(B, ldx, ldy);
+    if (rc) return rc;
+    return launched(launch_spmm(*p, wdtype, values, nullptr, packed, xdtype, B, X, ldx, Y, ldy,
+                                static_cast<hipStream_t>(stream)), "spmm (packed) launch");
 }
 
 int darb_lstm_layer(const darb_plan *wih, const void *wih_values, const uint8_t *wih_offsets,
@@ -324,12 +399,12 @@ int darb_lstm_layer(const darb_plan *wih, const void *wih_values, const uint8_t 
     hipStream_t s = static_cast<hipStream_t>(stream);
     float *U = workspace;              // [4H x T*batch]: input products of every step
     float *G = workspace + 4 * H * TB; // [4H x batch]: recurrent product of one step
-    rc = launched(launch_spmm(*wih, wdtype, wih_values, wih_offsets, DARB_F32, TB, x_seq, TB, U,
-                              TB, s), "lstm input product");
+    rc = launched(launch_spmm(*wih, wdtype, wih_values, wih_offsets, nullptr, DARB_F32, TB, x_seq,
+                              TB, U, TB, s), "lstm input product");
     if (rc) return rc;
     for (int64_t t = 0; t < T; ++t) {
-        rc = launched(launch_spmm(*whh, wdtype, whh_values, whh_offsets, DARB_F32, batch, h,
-                                  batch, G, batch, s), "lstm recurrent product");
+        rc = launched(launch_spmm(*whh, wdtype, whh_values, whh_offsets, nullptr, DARB_F32, batch,
+                                  h, batch, G, batch, s), "lstm recurrent product");
         if (rc) return rc;
         rc = launched(launch_lstm_cell(H, batch, G, U + t * batch, TB, h, c, h_seq + t * batch, TB,
                                        s), "lstm cell");

@@ -24,6 +24,7 @@ struct BinTable {
     int64_t rows[kMaxBins];
     int64_t first_elem[kMaxBins];  // slot of the group's first retained weight
     int64_t nblk[kMaxBins];        // retained weights per row
+    int64_t first_word[kMaxBins];  // packed offsets: the group's first 32-bit word
 };
 
 // Per-launch work split of the product kernels.  Every workgroup belongs to one
@@ -48,6 +49,7 @@ struct darb_plan {
     std::vector<int32_t> perm;
     darb::BinTable bins{};
     int64_t workspace_bytes = 0;
+    int64_t packed_words = 0;       // 32-bit words of the bit-packed offsets
     // device side (inside the caller's workspace)
     int32_t *d_perm = nullptr;      // [M] original row stored i-th
     int64_t *d_rowinfo = nullptr;   // [M] (row_start[r] << 8) | log2b[r], original order
@@ -65,12 +67,18 @@ hipError_t launch_encode(const darb_plan &p, int wdtype, const void *W, int64_t 
                          void *values, uint8_t *offsets, hipStream_t s);
 hipError_t launch_decode(const darb_plan &p, int wdtype, const void *values,
                          const uint8_t *offsets, void *W_out, int64_t ldw, hipStream_t s);
+// The products read the offsets from exactly one of `offsets` (one byte per
+// retained weight) and `packed` (log2 b bits per retained weight); the other is NULL.
 hipError_t launch_spmv(const darb_plan &p, int wdtype, const void *values,
-                       const uint8_t *offsets, int xdtype, const void *x, float *y,
-                       hipStream_t s);
+                       const uint8_t *offsets, const uint32_t *packed, int xdtype,
+                       const void *x, float *y, hipStream_t s);
 hipError_t launch_spmm(const darb_plan &p, int wdtype, const void *values,
-                       const uint8_t *offsets, int xdtype, int64_t B, const void *X,
-                       int64_t ldx, float *Y, int64_t ldy, hipStream_t s);
+                       const uint8_t *offsets, const uint32_t *packed, int xdtype, int64_t B,
+                       const void *X, int64_t ldx, float *Y, int64_t ldy, hipStream_t s);
+hipError_t launch_pack_offsets(const darb_plan &p, const uint8_t *offsets, uint32_t *packed,
+                               hipStream_t s);
+hipError_t launch_unpack_offsets(const darb_plan &p, const uint32_t *packed, uint8_t *offsets,
+                                 hipStream_t s);
 hipError_t launch_lstm_cell(int64_t H, int64_t batch, const float *G, const float *U,
                             int64_t ldu, float *h, float *c, float *h_seq, int64_t ld_seq,
                             hipStream_t s);

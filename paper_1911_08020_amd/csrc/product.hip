@@ -22,11 +22,16 @@
 // broadcasts them across a row's lanes register to register (DPP, swizzle or
 // readlane), gathering X rows kSpmmBatch at a time; up to 8 waves split a row
 // group's weights and their partial sums meet in LDS in a fixed order.
+//
+// Both products read the offsets either as one byte per retained weight or in the
+// bit-packed form of section 4.2 (log2 b bits each, packed_bits.h); the two forms
+// share every other step, so their results are bitwise identical.
 #include <hip/hip_fp16.h>
 
 #include <utility>
 
 #include "darb_internal.h"
+#include "packed_bits.h"
 
 namespace darb {
 namespace {
@@ -71,6 +76,89 @@ __device__ __forceinline__ int block_begin_of(const ProductSchedule &s, int g) {
 }
 
 // ---------------------------------------------------------------------------------
+// Offset sources.  A lane loads the indices of NV consecutive retained weights of a
+// group (group slots j .. j + NV - 1, j a multiple of NV) as `Raw`, keeps them in
+// registers while other loads are in flight, turns them into `Bits` when it needs
+// them and reads index q with field().
+// ---------------------------------------------------------------------------------
+
+struct GroupOffsets {
+    const uint8_t *u8;     // byte form: the group's first slot
+    PackedGroup pk;        // packed form
+};
+
+__device__ __forceinline__ GroupOffsets group_offsets(const void *offs, const BinTable &bins,
+                                                      int g) {
+    GroupOffsets go;
+    go.u8 = static_cast<const uint8_t *>(offs) + pick(bins.first_elem, g);
+    go.pk = packed_group(static_cast<const uint32_t *>(offs), pick(bins.first_word, g),
+                         pick(bins.log2b, g));
+    return go;
+}
+
+template <int NV> struct U8Vec;
+template <> struct U8Vec<1> { using T = uint8_t; };
+template <> struct U8Vec<2> { using T = uint16_t; };
+template <> struct U8Vec<4> { using T = uint32_t; };
+template <> struct U8Vec<8> { using T = u32x2; };
+template <> struct U8Vec<16> { using T = u32x4; };
+
+template <bool PK, int NV> struct Off;
+
+// one byte per weight: one NV-byte load (the caller guarantees its alignment)
+template <int NV> struct Off<false, NV> {
+    using Raw = typename U8Vec<NV>::T;
+    using Bits = Raw;
+    __device__ static Raw load(const GroupOffsets &go, int64_t j) {
+        return *reinterpret_cast<const Raw *>(go.u8 + j);
+    }
+    __device__ static Bits bits(const Raw &r, const GroupOffsets &) { return r; }
+    __device__ static int field(const Bits &b, int q, const GroupOffsets &) {
+        if constexpr (NV <= 4) return int((uint32_t(b) >> (8 * q)) & 0xFFu);
+        else return int((b[q >> 2] >> (8 * (q & 3))) & 0xFFu);
+    }
+};
+
+// packed, up to 4 indices (<= 28 bits): two words
+template <int NV> struct Off<true, NV> {
+    static_assert(NV <= 4, "wider vectors have their own specialisations");
+    using Raw = PackedWords2;
+    using Bits = uint32_t;
+    __device__ static Raw load(const GroupOffsets &go, int64_t j) { return packed_load2(go.pk, j); }
+    __device__ static Bits bits(const Raw &r, const GroupOffsets &) { return packed_bits32(r); }
+    __device__ static int field(Bits b, int q, const GroupOffsets &go) {
+        return packed_field(b, q, go.pk);
+    }
+};
+
+// packed, 8 indices (<= 56 bits): three words
+template <> struct Off<true, 8> {
+    using Raw = PackedWords3;
+    using Bits = uint64_t;
+    __device__ static Raw load(const GroupOffsets &go, int64_t j) { return packed_load3(go.pk, j); }
+    __device__ static Bits bits(const Raw &r, const GroupOffsets &) { return packed_bits64(r); }
+    __device__ static int field(Bits b, int q, const GroupOffsets &go) {
+        return packed_field(b, q, go.pk);
+    }
+};
+
+// packed, 16 indices: two 8-index windows (j is a multiple of 16, so both lie in
+// one run)
+template <> struct Off<true, 16> {
+    struct Raw { PackedWords3 lo, hi; };
+    struct Bits { uint64_t lo, hi; };
+    __device__ static Raw load(const GroupOffsets &go, int64_t j) {
+        return Raw{packed_load3(go.pk, j), packed_load3(go.pk, j + 8)};
+    }
+    __device__ static Bits bits(const Raw &r, const GroupOffsets &) {
+        return Bits{packed_bits64(r.lo), packed_bits64(r.hi)};
+    }
+    __device__ static int field(const Bits &b, int q, const GroupOffsets &go) {
+        return q < 8 ? packed_field(b.lo, q, go.pk) : packed_field(b.hi, q - 8, go.pk);
+    }
+};
+
+// ---------------------------------------------------------------------------------
 // SpMV
 // ---------------------------------------------------------------------------------
 
@@ -83,23 +171,16 @@ template <typename Tw> struct WVec;
 template <> struct WVec<float> {
     static constexpr int VEC = 4;
     using V = f32x4;        // 4 values, 16 bytes
-    using O = uint32_t;     // their 4 offset bytes
     __device__ static float get(const V &v, int i) { return v[i]; }
 };
 template <> struct WVec<__half> {
     static constexpr int VEC = 8;
     using V = u32x4;        // 8 fp16 values, 16 bytes
-    using O = u32x2;        // their 8 offset bytes
     __device__ static float get(const V &v, int i) {
         const uint32_t w = v[i >> 1];
         return half_bits_to_f32((i & 1) ? (w >> 16) : w);
     }
 };
-
-__device__ __forceinline__ uint32_t off_byte(uint32_t o, int i) { return (o >> (8 * i)) & 0xFFu; }
-__device__ __forceinline__ uint32_t off_byte(u32x2 o, int i) {
-    return (o[i >> 2] >> (8 * (i & 3))) & 0xFFu;
-}
 
 // Copy x (N elements) into LDS as fp32: SB 16-byte loads per thread in flight
 // (addresses clamped, stores masked), then the scalar tail.
@@ -137,13 +218,15 @@ __device__ __forceinline__ void stage_x(float *xs, const Tx *__restrict__ x, int
     for (int c = nv * E + int(threadIdx.x); c < N; c += kSpmvThreads) xs[c] = to_f32<Tx>(x[c]);
 }
 
-template <typename Tw, typename Tx, bool LDS, int SB>
+template <typename Tw, typename Tx, bool LDS, int SB, bool PK>
 __global__ __launch_bounds__(kSpmvThreads) void spmv_kernel(
-    const Tw *__restrict__ values, const uint8_t *__restrict__ offsets,
+    const Tw *__restrict__ values, const void *__restrict__ offs,
     const Tx *__restrict__ x, float *__restrict__ y, const int32_t *__restrict__ perm,
     int N, BinTable bins, ProductSchedule sch) {
     using WV = WVec<Tw>;
     constexpr int VEC = WV::VEC;
+    using OV = Off<PK, VEC>;
+    using OS = Off<PK, 1>;
     extern __shared__ float xs[];
 
     const int g = block_group(sch);
@@ -163,16 +246,17 @@ __global__ __launch_bounds__(kSpmvThreads) void spmv_kernel(
     const bool row_ok = row < rows;
     const int64_t row_c = row_ok ? row : rows - 1;
     const int sub = lane & (L - 1);
-    const int64_t e0 = first_elem + row_c * nblk;
+    const int64_t j0 = row_c * nblk;                     // the row's first slot in its group
+    const int64_t e0 = first_elem + j0;
     const int nvec = vec_path ? nblk / VEC : nblk;
+    const GroupOffsets go = group_offsets(offs, bins, g);
 
     // the destination row and the first round of this lane's vectors, issued
     // before x is staged
     const int32_t dest = perm[first_row + row_c];
     typename WV::V wv[kVmax];
-    typename WV::O ov[kVmax];
+    typename OV::Raw ov[kVmax];
     const typename WV::V *vrow = reinterpret_cast<const typename WV::V *>(values + e0);
-    const typename WV::O *orow = reinterpret_cast<const typename WV::O *>(offsets + e0);
     if (vec_path) {
 #pragma unroll
         for (int t = 0; t < kVmax; ++t) {
@@ -180,7 +264,7 @@ __global__ __launch_bounds__(kSpmvThreads) void spmv_kernel(
                 const int vi = sub + t * L;
                 const int vc = vi < nvec ? vi : nvec - 1;
                 wv[t] = __builtin_nontemporal_load(vrow + vc);
-                ov[t] = orow[vc];
+                ov[t] = OV::load(go, j0 + int64_t(vc) * VEC);
             }
         }
     }
@@ -203,9 +287,10 @@ __global__ __launch_bounds__(kSpmvThreads) void spmv_kernel(
             for (int t = 0; t < kVmax; ++t) {
                 const int vi = base + sub + t * L;
                 if (vi < nvec) {
+                    const typename OV::Bits ob = OV::bits(ov[t], go);
 #pragma unroll
                     for (int q = 0; q < VEC; ++q) {
-                        const int c = ((vi * VEC + q) << lb) + int(off_byte(ov[t], q));
+                        const int c = ((vi * VEC + q) << lb) + OV::field(ob, q, go);
                         acc = fmaf(WV::get(wv[t], q), xat(c), acc);
                     }
                 }
@@ -217,15 +302,16 @@ __global__ __launch_bounds__(kSpmvThreads) void spmv_kernel(
                     const int vi = base + L * kVmax + sub + t * L;
                     const int vc = vi < nvec ? vi : nvec - 1;
                     wv[t] = __builtin_nontemporal_load(vrow + vc);
-                    ov[t] = orow[vc];
+                    ov[t] = OV::load(go, j0 + int64_t(vc) * VEC);
                 }
             }
         }
     } else {
         const Tw *vr = values + e0;
-        const uint8_t *orr = offsets + e0;
-        for (int k = sub; k < nblk; k += L)
-            acc = fmaf(to_f32<Tw>(vr[k]), xat((k << lb) + int(orr[k])), acc);
+        for (int k = sub; k < nblk; k += L) {
+            const int o = OS::field(OS::bits(OS::load(go, j0 + k), go), 0, go);
+            acc = fmaf(to_f32<Tw>(vr[k]), xat((k << lb) + o), acc);
+        }
     }
 
     for (int m = L >> 1; m >= 1; m >>= 1) acc += __shfl_xor(acc, m, kWave);
@@ -290,29 +376,31 @@ template <int LGL, int T> __device__ __forceinline__ int group_bcast(int v) {
     }
 }
 
-// GM consecutive retained weights of a row (values and offset bytes) for one lane:
-// one vector load each when the bin is aligned for it, element loads otherwise.
-template <typename Tw, int GM> struct PairLoad {
+// GM consecutive retained weights of a row (values and offsets) for one lane: one
+// vector load each when the bin is aligned for it, element loads otherwise.
+template <typename Tw, int GM, bool PK> struct PairLoad {
     struct alignas(GM * sizeof(Tw)) VV { Tw e[GM]; };
-    struct alignas(GM) OV { uint8_t e[GM]; };
-    // vec: the caller guarantees k % GM == 0 and k + GM <= nblk; otherwise every
-    // element index is clamped into the row [0, nblk)
-    __device__ static void load(const Tw *vr, const uint8_t *orr, int k, int nblk, bool vec,
-                                float (&v)[GM], int (&o)[GM]) {
+    // vec: the caller guarantees k % GM == 0, k + GM <= nblk and nblk % GM == 0 (so
+    // the group slot j0 + k is a multiple of GM); otherwise every element index is
+    // clamped into the row [0, nblk).  j0 is the row's first slot in its group.
+    __device__ static void load(const Tw *vr, const GroupOffsets &go, int64_t j0, int k,
+                                int nblk, bool vec, float (&v)[GM], int (&o)[GM]) {
         if (vec) {
+            using OV = Off<PK, GM>;
             const VV a = *reinterpret_cast<const VV *>(vr + k);
-            const OV b = *reinterpret_cast<const OV *>(orr + k);
+            const typename OV::Bits b = OV::bits(OV::load(go, j0 + k), go);
 #pragma unroll
             for (int i = 0; i < GM; ++i) {
                 v[i] = to_f32<Tw>(a.e[i]);
-                o[i] = int(b.e[i]);
+                o[i] = OV::field(b, i, go);
             }
         } else {
+            using OS = Off<PK, 1>;
 #pragma unroll
             for (int i = 0; i < GM; ++i) {
                 const int kk = k + i < nblk ? k + i : nblk - 1;
                 v[i] = to_f32<Tw>(vr[kk]);
-                o[i] = int(orr[kk]);
+                o[i] = OS::field(OS::bits(OS::load(go, j0 + kk), go), 0, go);
             }
         }
     }
@@ -325,9 +413,9 @@ template <typename Tw, int GM> struct PairLoad {
 // HBM with coalesced loads, then broadcast each pair to the row's lanes with a
 // register-to-register exchange and gather its X row; kSpmmBatch gathers are in
 // flight per lane.  Partial sums of the KS waves meet in LDS in a fixed order.
-template <typename Tw, typename Tx, int CPL, int LGL>
+template <typename Tw, typename Tx, int CPL, int LGL, bool PK>
 __global__ __launch_bounds__(kSpmmThreads) void spmm_kernel(
-    const Tw *__restrict__ values, const uint8_t *__restrict__ offsets,
+    const Tw *__restrict__ values, const void *__restrict__ offs,
     const Tx *__restrict__ X, int64_t ldx, int64_t B, float *__restrict__ Y, int64_t ldy,
     const int32_t *__restrict__ perm, int N, BinTable bins, ProductSchedule sch) {
     using XL = XLoad<Tx, CPL>;
@@ -369,9 +457,9 @@ __global__ __launch_bounds__(kSpmmThreads) void spmm_kernel(
     const int share = (((nblk + KS - 1) / KS) + S - 1) / S * S;
     const int kbeg = ks * share;
     const int kend = kbeg + share < nblk ? kbeg + share : nblk;
-    const int64_t re = first_elem + (row0 + (row_ok ? rl : 0)) * nblk;
-    const Tw *vr = values + re;
-    const uint8_t *orr = offsets + re;
+    const int64_t j0 = (row0 + (row_ok ? rl : 0)) * nblk;   // the row's first slot in its group
+    const Tw *vr = values + first_elem + j0;
+    const GroupOffsets go = group_offsets(offs, bins, g);
 
     float acc[CPL];
 #pragma unroll
@@ -387,7 +475,7 @@ __global__ __launch_bounds__(kSpmmThreads) void spmm_kernel(
             const bool ok = row_ok && k < kend;
             float v[GM];
             int o[GM];
-            PairLoad<Tw, GM>::load(vr, orr, ok ? k : kbeg, nblk, vec_pairs, v, o);
+            PairLoad<Tw, GM, PK>::load(vr, go, j0, ok ? k : kbeg, nblk, vec_pairs, v, o);
 #pragma unroll
             for (int gi = 0; gi < GM; ++gi) {
                 const bool okg = ok && k + gi < kend;     // element test for the scalar path
@@ -449,6 +537,21 @@ int ilog2_ceil(int64_t v) {
     return l;
 }
 
+// The offsets argument of the kernels: the byte form, or the packed words.  A plan
+// without packed words has b = 1 everywhere; the kernels then still load one word
+// (and mask it to nothing), so they get the plan's row order, >= 4 readable bytes.
+const void *offset_source(const darb_plan &p, const uint8_t *offsets, const uint32_t *packed) {
+    if (offsets) return offsets;
+    return p.packed_words > 0 ? static_cast<const void *>(packed)
+                              : static_cast<const void *>(p.d_perm);
+}
+
+// Byte offsets are loaded VEC at a time, so their address must be aligned for it;
+// packed offsets are loaded as whole words at any weight index.
+bool offsets_aligned(const uint8_t *offsets, int vec) {
+    return !offsets || reinterpret_cast<uintptr_t>(offsets) % vec == 0;
+}
+
 template <typename Tw>
 bool spmv_schedule(const darb_plan &p, const void *values, const uint8_t *offsets,
                    ProductSchedule &s) {
@@ -457,7 +560,7 @@ bool spmv_schedule(const darb_plan &p, const void *values, const uint8_t *offset
     s.nbins = p.bins.nbins;
     s.col_slabs = 1;
     const bool ptr_ok = (reinterpret_cast<uintptr_t>(values) % 16 == 0) &&
-                        (reinterpret_cast<uintptr_t>(offsets) % VEC == 0);
+                        offsets_aligned(offsets, VEC);
     int64_t blocks = 0;
     for (int g = 0; g < s.nbins; ++g) {
         const int64_t nblk = p.bins.nblk[g];
@@ -477,23 +580,24 @@ bool spmv_schedule(const darb_plan &p, const void *values, const uint8_t *offset
     return true;
 }
 
-template <typename Tw, typename Tx>
+template <typename Tw, typename Tx, bool PK>
 hipError_t launch_spmv_t(const darb_plan &p, const void *values, const uint8_t *offsets,
-                         const void *x, float *y, hipStream_t st) {
+                         const uint32_t *packed, const void *x, float *y, hipStream_t st) {
     ProductSchedule s;
     if (!spmv_schedule<Tw>(p, values, offsets, s)) return hipErrorInvalidConfiguration;
     const int blocks = s.block_begin[s.nbins];
     if (blocks == 0) return hipSuccess;
     const Tw *v = static_cast<const Tw *>(values);
+    const void *offs = offset_source(p, offsets, packed);
     const Tx *xx = static_cast<const Tx *>(x);
     const int N = int(p.N);
     if (p.N <= kLdsMaxFloats) {
         const size_t lds = size_t(p.N) * sizeof(float);
         const int64_t nv = p.N / (16 / int64_t(sizeof(Tx)));
         const int64_t per_thread = (nv + kSpmvThreads - 1) / kSpmvThreads;
-#define DARB_SPMV_LDS(SB)                                                                       \
-    hipLaunchKernelGGL((spmv_kernel<Tw, Tx, true, SB>), dim3(blocks), dim3(kSpmvThreads), lds, \
-                       st, v, offsets, xx, y, p.d_perm, N, p.bins, s)
+#define DARB_SPMV_LDS(SB)                                                                    \
+    hipLaunchKernelGGL((spmv_kernel<Tw, Tx, true, SB, PK>), dim3(blocks), dim3(kSpmvThreads), \
+                       lds, st, v, offs, xx, y, p.d_perm, N, p.bins, s)
         if (per_thread <= 1) DARB_SPMV_LDS(1);
         else if (per_thread <= 2) DARB_SPMV_LDS(2);
         else if (per_thread <= 4) DARB_SPMV_LDS(4);
@@ -501,10 +605,17 @@ hipError_t launch_spmv_t(const darb_plan &p, const void *values, const uint8_t *
         else DARB_SPMV_LDS(16);
 #undef DARB_SPMV_LDS
     } else {
-        hipLaunchKernelGGL((spmv_kernel<Tw, Tx, false, 1>), dim3(blocks), dim3(kSpmvThreads), 0,
-                           st, v, offsets, xx, y, p.d_perm, N, p.bins, s);
+        hipLaunchKernelGGL((spmv_kernel<Tw, Tx, false, 1, PK>), dim3(blocks), dim3(kSpmvThreads),
+                           0, st, v, offs, xx, y, p.d_perm, N, p.bins, s);
     }
     return hipGetLastError();
+}
+
+template <typename Tw, typename Tx>
+hipError_t launch_spmv_form(const darb_plan &p, const void *values, const uint8_t *offsets,
+                            const uint32_t *packed, const void *x, float *y, hipStream_t st) {
+    if (offsets) return launch_spmv_t<Tw, Tx, false>(p, values, offsets, nullptr, x, y, st);
+    return launch_spmv_t<Tw, Tx, true>(p, values, nullptr, packed, x, y, st);
 }
 
 bool spmm_schedule(const darb_plan &p, int64_t B, int cpl, size_t wbytes, const void *values,
@@ -532,7 +643,7 @@ bool spmm_schedule(const darb_plan &p, int64_t B, int cpl, size_t wbytes, const 
         const int64_t GM = lgL >= 4 ? 1 : (16 >> lgL);
         s.vec[g] = (GM > 1 && nblk % GM == 0 && p.bins.first_elem[g] % GM == 0 &&
                     reinterpret_cast<uintptr_t>(values) % (GM * wbytes) == 0 &&
-                    reinterpret_cast<uintptr_t>(offsets) % GM == 0) ? 1 : 0;
+                    offsets_aligned(offsets, int(GM))) ? 1 : 0;
         s.block_begin[g] = int32_t(blocks);
         blocks += (p.bins.rows[g] + rows_pb - 1) / rows_pb * slabs;
         if (blocks > 0x7FFFFFFF) return false;
@@ -541,15 +652,15 @@ bool spmm_schedule(const darb_plan &p, int64_t B, int cpl, size_t wbytes, const 
     return true;
 }
 
-template <typename Tw, typename Tx, int CPL>
+template <typename Tw, typename Tx, int CPL, bool PK>
 hipError_t launch_spmm_cpl(const darb_plan &p, const ProductSchedule &s, const Tw *v,
-                           const uint8_t *offsets, int64_t B, const Tx *x, int64_t ldx, float *Y,
+                           const void *offs, int64_t B, const Tx *x, int64_t ldx, float *Y,
                            int64_t ldy, hipStream_t st) {
     const int blocks = s.block_begin[s.nbins];
     const int N = int(p.N);
-#define DARB_SPMM(LGL)                                                                          \
-    hipLaunchKernelGGL((spmm_kernel<Tw, Tx, CPL, LGL>), dim3(blocks), dim3(kSpmmThreads), 0, st, \
-                       v, offsets, x, ldx, B, Y, ldy, p.d_perm, N, p.bins, s)
+#define DARB_SPMM(LGL)                                                                    \
+    hipLaunchKernelGGL((spmm_kernel<Tw, Tx, CPL, LGL, PK>), dim3(blocks), dim3(kSpmmThreads), \
+                       0, st, v, offs, x, ldx, B, Y, ldy, p.d_perm, N, p.bins, s)
     switch (s.log2_lanes[0]) {
         case 0: DARB_SPMM(0); break;
         case 1: DARB_SPMM(1); break;
@@ -563,10 +674,10 @@ hipError_t launch_spmm_cpl(const darb_plan &p, const ProductSchedule &s, const T
     return hipGetLastError();
 }
 
-template <typename Tw, typename Tx>
+template <typename Tw, typename Tx, bool PK>
 hipError_t launch_spmm_t(const darb_plan &p, const void *values, const uint8_t *offsets,
-                         int64_t B, const void *X, int64_t ldx, float *Y, int64_t ldy,
-                         hipStream_t st) {
+                         const uint32_t *packed, int64_t B, const void *X, int64_t ldx, float *Y,
+                         int64_t ldy, hipStream_t st) {
     constexpr int CPL = 16 / int(sizeof(Tx));
     const bool vec = (reinterpret_cast<uintptr_t>(X) % 16 == 0) &&
                      ((ldx * int64_t(sizeof(Tx))) % 16 == 0) && (B % CPL == 0);
@@ -575,29 +686,41 @@ hipError_t launch_spmm_t(const darb_plan &p, const void *values, const uint8_t *
         return hipErrorInvalidConfiguration;
     if (s.block_begin[s.nbins] == 0) return hipSuccess;
     const Tw *v = static_cast<const Tw *>(values);
+    const void *offs = offset_source(p, offsets, packed);
     const Tx *x = static_cast<const Tx *>(X);
-    if (vec) return launch_spmm_cpl<Tw, Tx, CPL>(p, s, v, offsets, B, x, ldx, Y, ldy, st);
-    return launch_spmm_cpl<Tw, Tx, 1>(p, s, v, offsets, B, x, ldx, Y, ldy, st);
+    if (vec) return launch_spmm_cpl<Tw, Tx, CPL, PK>(p, s, v, offs, B, x, ldx, Y, ldy, st);
+    return launch_spmm_cpl<Tw, Tx, 1, PK>(p, s, v, offs, B, x, ldx, Y, ldy, st);
+}
+
+template <typename Tw, typename Tx>
+hipError_t launch_spmm_form(const darb_plan &p, const void *values, const uint8_t *offsets,
+                            const uint32_t *packed, int64_t B, const void *X, int64_t ldx,
+                            float *Y, int64_t ldy, hipStream_t st) {
+    if (offsets)
+        return launch_spmm_t<Tw, Tx, false>(p, values, offsets, nullptr, B, X, ldx, Y, ldy, st);
+    return launch_spmm_t<Tw, Tx, true>(p, values, nullptr, packed, B, X, ldx, Y, ldy, st);
 }
 
 }  // namespace
 
 hipError_t launch_spmv(const darb_plan &p, int wdtype, const void *values,
-                       const uint8_t *offsets, int xdtype, const void *x, float *y,
-                       hipStream_t s) {
-    if (wdtype == DARB_F32) return launch_spmv_t<float, float>(p, values, offsets, x, y, s);
-    if (xdtype == DARB_F16) return launch_spmv_t<__half, __half>(p, values, offsets, x, y, s);
-    return launch_spmv_t<__half, float>(p, values, offsets, x, y, s);
+                       const uint8_t *offsets, const uint32_t *packed, int xdtype,
+                       const void *x, float *y, hipStream_t s) {
+    if (wdtype == DARB_F32)
+        return launch_spmv_form<float, float>(p, values, offsets, packed, x, y, s);
+    if (xdtype == DARB_F16)
+        return launch_spmv_form<__half, __half>(p, values, offsets, packed, x, y, s);
+    return launch_spmv_form<__half, float>(p, values, offsets, packed, x, y, s);
 }
 
 hipError_t launch_spmm(const darb_plan &p, int wdtype, const void *values,
-                       const uint8_t *offsets, int xdtype, int64_t B, const void *X,
-                       int64_t ldx, float *Y, int64_t ldy, hipStream_t s) {
+                       const uint8_t *offsets, const uint32_t *packed, int xdtype, int64_t B,
+                       const void *X, int64_t ldx, float *Y, int64_t ldy, hipStream_t s) {
     if (wdtype == DARB_F32)
-        return launch_spmm_t<float, float>(p, values, offsets, B, X, ldx, Y, ldy, s);
+        return launch_spmm_form<float, float>(p, values, offsets, packed, B, X, ldx, Y, ldy, s);
     if (xdtype == DARB_F16)
-        return launch_spmm_t<__half, __half>(p, values, offsets, B, X, ldx, Y, ldy, s);
-    return launch_spmm_t<__half, float>(p, values, offsets, B, X, ldx, Y, ldy, s);
+        return launch_spmm_form<__half, __half>(p, values, offsets, packed, B, X, ldx, Y, ldy, s);
+    return launch_spmm_form<__half, float>(p, values, offsets, packed, B, X, ldx, Y, ldy, s);
 }
 
 }  // namespace darb

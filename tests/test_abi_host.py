@@ -56,6 +56,11 @@ def _plan_matches_oracle(M, N, d, D, mode, bmin, bmax):
         assert (log2b[rows] == b["log2b"]).all()
         assert row_start[rows[0]] == b["first_elem"]
         assert b["nblk"] == -(-N // (1 << b["log2b"]))
+    # the bit-packed offsets take the oracle's word count and group starts
+    words, first = oracle.packed_layout(lay)
+    assert p.packed_words == words
+    for b in p.bins:
+        assert b["first_word"] == first[b["log2b"]]
     return p
 
 
@@ -88,6 +93,15 @@ def test_plan_random_densities_and_bounds():
         bmax = 1 << int(rng.integers(int(np.log2(bmin)), 8))
         for mode in (darb.ROUND_FLOOR, darb.ROUND_PAPER):
             _plan_matches_oracle(M, N, d, D, mode, bmin, bmax)
+
+
+def test_plan_packed_words_table7():
+    # one row per block size 2 ... 64 over 1500 columns (Table 7's decoders): the
+    # offsets take sum_b ceil(ceil(1500 / b) / 32) * log2 b words
+    p = darb.Plan(6, 1500, np.array([0.5, 0.25, 0.125, 1 / 16, 1 / 32, 1 / 64]), 0.1,
+                  darb.ROUND_FLOOR, 1, 128)
+    want = sum(-(-(-(-1500 // b)) // 32) * l for l, b in enumerate([2, 4, 8, 16, 32, 64], 1))
+    assert p.packed_words == want == 24 + 24 + 18 + 12 + 10 + 6
 
 
 def test_plan_table7_and_worked_example():
@@ -133,6 +147,12 @@ def test_null_arguments_and_not_uploaded():
     assert L.darb_decode(p.handle, 0, buf, buf, buf, 8, None) == darb.E_NOT_UPLOADED
     assert L.darb_spmv(p.handle, 0, buf, buf, 0, buf, buf, None) == darb.E_NOT_UPLOADED
     assert L.darb_spmm(p.handle, 0, buf, buf, 0, 4, buf, 4, buf, 4, None) == darb.E_NOT_UPLOADED
+    assert L.darb_pack_offsets(p.handle, buf, buf, None) == darb.E_NOT_UPLOADED
+    assert L.darb_unpack_offsets(p.handle, buf, buf, None) == darb.E_NOT_UPLOADED
+    assert L.darb_spmv_packed(p.handle, 0, buf, buf, 0, buf, buf, None) == darb.E_NOT_UPLOADED
+    assert L.darb_spmm_packed(p.handle, 0, buf, buf, 0, 4, buf, 4, buf, 4, None) \
+        == darb.E_NOT_UPLOADED
+    assert L.darb_spmv_packed(None, 0, buf, buf, 0, buf, buf, None) == darb.E_INVALID
     assert L.darb_encode(None, 0, buf, 8, buf, buf, None) == darb.E_INVALID
     assert L.darb_plan_info(None, None) == darb.E_INVALID
     assert L.darb_plan_upload(p.handle, None, 1024, None) == darb.E_INVALID
