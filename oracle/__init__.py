@@ -16,6 +16,8 @@ in fp64 (``lstm_forward``).  Functions and the paper passages they follow:
 * ``decode``       -- the masked dense matrix the format stands for
 * ``spmm``         -- section 2 / 3.2, product over retained weights, offsets select activations
 * ``pack_offsets``  -- section 4.2, log2(b)-bit indices (and ``unpack_offsets``)
+* ``prune_counts`` -- section 3.2's first step (irregular top-K magnitude pruning,
+                      section 2), per-row kept counts that give the row densities
 * ``dense_masked_product`` -- the plain definition of the product: a dense fp64 matmul
 * ``lstm_forward`` -- the LSTM recurrence of the recurrent workload on the decoded
                       masked matrices (dense fp64 products)
@@ -83,6 +85,8 @@ def _load():
     lib.oracle_pack_offsets.restype = None
     lib.oracle_unpack_offsets.argtypes = [I64, I64, P, P, P, P]
     lib.oracle_unpack_offsets.restype = None
+    lib.oracle_prune_counts.argtypes = [I64, I64, I, P, I64, I64, P]
+    lib.oracle_prune_counts.restype = I
     _lib = lib
     return lib
 
@@ -232,6 +236,24 @@ def unpack_offsets(packed: np.ndarray, lay: Layout) -> np.ndarray:
     _load().oracle_unpack_offsets(lay.M, lay.N, _ptr(lay.log2b), _ptr(lay.row_start),
                                   _ptr(packed), _ptr(out))
     return out
+
+
+def prune_counts(W: np.ndarray, k: int) -> np.ndarray:
+    """Per-row counts of the k largest-magnitude elements of W (sections 2 and 3.2).
+
+    Magnitude is the stored bits with the sign cleared; equal magnitudes go to the
+    lower flat index.  Returns int64 [M].
+    """
+    W = np.asarray(W)
+    if W.ndim != 2 or W.dtype not in _DT:
+        raise TypeError("W must be a 2-D fp32 or fp16 array")
+    M, N = W.shape
+    Wc = np.ascontiguousarray(W)
+    counts = np.zeros(M, dtype=np.int64)
+    rc = _load().oracle_prune_counts(M, N, _DT[W.dtype], _ptr(Wc), N, int(k), _ptr(counts))
+    if rc != 0:
+        raise ValueError("invalid pruning arguments")
+    return counts
 
 
 def dense_masked_product(Wm: np.ndarray, X: np.ndarray) -> np.ndarray:

@@ -30,6 +30,7 @@
  */
 #include <math.h>
 #include <stdint.h>
+#include <stdlib.h>
 #include <string.h>
 
 #define ORACLE_OK 0
@@ -338,4 +339,47 @@ void oracle_unpack_offsets(int64_t M, int64_t N, const uint8_t *log2b, const int
             offsets[row_start[r] + k] = (uint8_t)v;
         }
     }
+}
+
+/*
+ * Irregular magnitude pruning, the starting point of DARB (section 3.2: the
+ * irregular mask is computed only to measure each row's density; section 2
+ * describes irregular pruning as keeping the top-K weights by magnitude).
+ * Keep the k elements of W with the largest magnitude key (stored bits with the
+ * sign cleared, the same key the block-max selection uses); among equal keys the
+ * lower flat index r*N + c comes first.  Written as the definition: sort every
+ * element by (key descending, flat index ascending), keep the first k, count the
+ * kept elements of each row.
+ */
+typedef struct {
+    uint32_t key;
+    int64_t idx;
+} oracle_ranked;
+
+static int ranked_before(const void *a, const void *b) {
+    const oracle_ranked *x = (const oracle_ranked *)a, *y = (const oracle_ranked *)b;
+    if (x->key != y->key) return x->key > y->key ? -1 : 1;
+    return x->idx < y->idx ? -1 : (x->idx > y->idx ? 1 : 0);
+}
+
+int oracle_prune_counts(int64_t M, int64_t N, int dtype, const void *W, int64_t ldw, int64_t k,
+                        int64_t *counts) {
+    if (M < 1 || N < 1 || ldw < N || k < 0 || k > M * N) return ORACLE_EINVAL;
+    if (dtype != DT_F32 && dtype != DT_F16) return ORACLE_EINVAL;
+    oracle_ranked *all = (oracle_ranked *)malloc((size_t)(M * N) * sizeof(oracle_ranked));
+    if (!all) return ORACLE_EINVAL;
+    for (int64_t r = 0; r < M; ++r) {
+        for (int64_t c = 0; c < N; ++c) {
+            uint32_t key;
+            if (dtype == DT_F32) key = ((const uint32_t *)W)[r * ldw + c] & 0x7FFFFFFFu;
+            else key = ((const uint16_t *)W)[r * ldw + c] & 0x7FFFu;
+            all[r * N + c].key = key;
+            all[r * N + c].idx = r * N + c;
+        }
+    }
+    qsort(all, (size_t)(M * N), sizeof(oracle_ranked), ranked_before);
+    for (int64_t r = 0; r < M; ++r) counts[r] = 0;
+    for (int64_t i = 0; i < k; ++i) counts[all[i].idx / N] += 1;
+    free(all);
+    return ORACLE_OK;
 }

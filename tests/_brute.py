@@ -7,7 +7,9 @@ the oracle can be pinned to something other than itself:
   rational arithmetic (``fractions.Fraction``);
 * the kept weight of a block is found with a per-element predicate on Python
   float magnitudes ("no element of the block is larger, and no earlier element
-  is as large"), not with a running argmax over integer keys.
+  is as large"), not with a running argmax over integer keys;
+* the irregular top-K mask ranks every element with Python's sort on
+  (magnitude key descending, flat index ascending) and counts the first K.
 """
 from fractions import Fraction
 
@@ -55,3 +57,15 @@ def encode_brute(W: np.ndarray, block_sizes):
         cols = kept_positions(W[r], int(block_sizes[r]))
         out.append(cols)
     return out
+
+
+def prune_brute(W, k):
+    """Brute force: rank every element by (magnitude bits desc, flat index asc)."""
+    ut = np.uint32 if W.dtype == np.float32 else np.uint16
+    mag = 0x7FFFFFFF if W.dtype == np.float32 else 0x7FFF
+    keys = [int(b) & mag for b in W.reshape(-1).view(ut)]
+    order = sorted(range(len(keys)), key=lambda i: (-keys[i], i))
+    counts = [0] * W.shape[0]
+    for i in order[:k]:
+        counts[i // W.shape[1]] += 1
+    return counts

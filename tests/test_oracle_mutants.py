@@ -14,7 +14,7 @@ import numpy as np
 import pytest
 
 import oracle
-from tests._brute import block_size_brute, kept_positions
+from tests._brute import block_size_brute, kept_positions, prune_brute
 
 ORACLE_DIR = os.path.dirname(oracle.__file__)
 
@@ -34,6 +34,12 @@ MUTANTS = {
                         "uint32_t v = (offsets[row_start[r] + k] >> (l - 1 - t)) & 1u;")],
     "pack_run_length": [("int64_t bit = (j % 32) * l;\n            uint32_t *run = packed + first_word[l] + (j / 32) * l;",
                          "int64_t bit = (j % 16) * l;\n            uint32_t *run = packed + first_word[l] + (j / 16) * l;")],
+    "prune_ties_to_high_index": [("return x->idx < y->idx ? -1 : (x->idx > y->idx ? 1 : 0);",
+                                  "return x->idx > y->idx ? -1 : (x->idx < y->idx ? 1 : 0);")],
+    "prune_sign_kept": [("key = ((const uint32_t *)W)[r * ldw + c] & 0x7FFFFFFFu;",
+                         "key = ((const uint32_t *)W)[r * ldw + c];")],
+    "prune_keeps_one_less": [("for (int64_t i = 0; i < k; ++i) counts",
+                              "for (int64_t i = 1; i < k; ++i) counts")],
 }
 
 
@@ -95,6 +101,11 @@ def pin_suite(orc):
     lay = orc.layout(97, np.array([3, 5, 7, 2], dtype=np.uint8))
     o = np.random.default_rng(1).integers(0, 4, size=lay.nnz).astype(np.uint8)
     assert np.array_equal(oracle.unpack_offsets(orc.pack_offsets(o, lay), lay), o)
+    # irregular pruning counts against brute force, ties and negative values included
+    for dtype in (np.float32, np.float16):
+        W = (rng.integers(-3, 4, size=(4, 9)) * 0.5).astype(dtype)
+        for k in (0, 1, 5, 17, 36):
+            assert orc.prune_counts(W, k).tolist() == prune_brute(W, k), (dtype, k)
     # fp16 decoding of a few bit patterns against numpy
     for bits in [0x3C00, 0x0001, 0x7BFF, 0xC000, 0x0400]:
         assert orc.half_to_double(bits) == float(np.array([bits], np.uint16).view(np.float16)[0])

@@ -11,7 +11,8 @@ import numpy as np
 import pytest
 
 import oracle
-from tests._brute import block_size_brute, encode_brute, kept_positions
+import workloads
+from tests._brute import block_size_brute, encode_brute, kept_positions, prune_brute
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
 
@@ -397,3 +398,52 @@ def test_packed_offsets_round_trip(seed):
     # each index occupies exactly log2 b bits: count the set bits both ways
     ones = sum(bin(int(w)).count("1") for w in packed)
     assert ones == sum(bin(int(x)).count("1") for x in o)
+
+
+# ----------------------------------------------------------------------------------
+# irregular top-K magnitude pruning: per-row kept counts (sections 2 and 3.2)
+# ----------------------------------------------------------------------------------
+
+@pytest.mark.parametrize("dtype", [np.float32, np.float16])
+@pytest.mark.parametrize("seed", [0, 1, 2, 3])
+def test_prune_counts_brute_force(dtype, seed):
+    rng = np.random.default_rng(seed)
+    M, N = int(rng.integers(1, 9)), int(rng.integers(1, 13))
+    # few distinct magnitudes with both signs: many ties, +0 / -0 among them
+    W = (rng.integers(-3, 4, size=(M, N)) * 0.5).astype(dtype)
+    W[rng.random((M, N)) < 0.1] = -0.0
+    for k in range(0, M * N + 1):
+        assert oracle.prune_counts(W, k).tolist() == prune_brute(W, k), k
+
+
+def test_prune_counts_special_values():
+    W = np.array([[np.inf, 1.0, np.nan], [-np.inf, -0.0, 0.0]], dtype=np.float32)
+    # key order: NaN (0x7FC00000) > +inf == -inf > 1.0 > +0 == -0
+    assert oracle.prune_counts(W, 1).tolist() == [1, 0]          # the NaN
+    assert oracle.prune_counts(W, 2).tolist() == [2, 0]          # + inf at column 0
+    assert oracle.prune_counts(W, 3).tolist() == [2, 1]          # - inf
+    assert oracle.prune_counts(W, 4).tolist() == [3, 1]          # 1.0
+    assert oracle.prune_counts(W, 5).tolist() == [3, 2]          # -0 before +0 (lower index)
+
+
+def test_prune_counts_all_ties_take_flat_order():
+    M, N = 5, 7
+    W = np.full((M, N), -2.5, dtype=np.float16)
+    for k in (0, 1, 6, 7, 8, 20, 35):
+        want = [min(N, max(0, k - r * N)) for r in range(M)]
+        assert oracle.prune_counts(W, k).tolist() == want
+
+
+def test_prune_counts_invariants_and_generator_agreement():
+    # distinct magnitudes: the kept set is the k largest |w|, whatever the tie rule
+    rng = np.random.default_rng(9)
+    W = rng.standard_normal((64, 300)).astype(np.float32)
+    k = 1920
+    c = oracle.prune_counts(W, k)
+    assert c.sum() == k and (c >= 0).all() and (c <= 300).all()
+    thr = np.sort(np.abs(W).reshape(-1))[-k]
+    assert np.array_equal(c, (np.abs(W) >= thr).sum(axis=1))
+    # the input generator's own exact-k selection (np.partition) agrees on a workload
+    mi = workloads.make_matrix(256, 512, wdtype="f16", dist="normal", sigma=0.7, keep=0.05,
+                               seed=3)
+    assert np.array_equal(oracle.prune_counts(mi.W, mi.k), mi.mask.sum(axis=1))
