@@ -349,6 +349,24 @@ def main(argv=None):
         }
     dominant = max(names, key=lambda n: kernels[n]["avg_us"])
 
+    # the step DARB starts from, on the device: per-row counts of the k largest
+    # magnitudes (radix select over W, several kernels); each pass streams W once
+    nb_ws = ctypes.c_int64()
+    lib.darb_prune_workspace(cfg.M, cfg.N, wcode, ctypes.byref(nb_ws))
+    prune_ws = torch.empty(nb_ws.value, dtype=torch.uint8, device=dev)
+    counts = torch.empty(cfg.M, dtype=torch.int64, device=dev)
+    prune_args = [(cfg.M, cfg.N, wcode, P(Wd[i].data_ptr()), cfg.N, mi.k, P(counts.data_ptr()),
+                   P(prune_ws.data_ptr()), nb_ws.value, sp) for i in range(RW)]
+    prune_us = timed_launches(lib.darb_prune_counts, prune_args, max(K // 4, 8))
+    prune_ok = bool(np.array_equal(counts.cpu().numpy(), mi.mask.sum(axis=1)))
+    w_passes = 4 if cfg.wdtype == "f32" else 3
+    w_stream = cfg.M * cfg.N * s_w
+    prune_ctx = {"avg_us": round(prune_us, 3), "k": mi.k, "passes_over_W": w_passes,
+                 "bytes": w_passes * w_stream,
+                 "gbps": round(w_passes * w_stream / (prune_us * 1e-6) / 1e9, 1),
+                 "counts_equal_generator": prune_ok}
+    del prune_ws
+
     # the paper's storage form: offsets bit-packed to log2 b bits (section 4.2).  The
     # conversion from the encode's bytes and both products on the packed form, same
     # rotation; outputs must equal the byte-offset products bit for bit.
@@ -408,6 +426,10 @@ def main(argv=None):
     small_us = timed_launches(lib.darb_stream_read, small_args, K)
     small_gbps = small_n * 4 / (small_us * 1e-6) / 1e9
     del smalls
+    # the same kernel reading the encode's input: the rotated W copies themselves
+    w_bytes = (Wd[0].numel() * Wd[0].element_size()) // 16 * 16
+    w_args = [(P(t.data_ptr()), w_bytes, P(sink.data_ptr()), sp) for t in Wd]
+    w_read_us = timed_launches(lib.darb_stream_read, w_args, K)
 
     # context, not a target: the same masked matrix as a dense fp32/fp16 matrix through
     # torch (hipBLASLt / rocBLAS), rotated like the DARB format
@@ -489,9 +511,13 @@ def main(argv=None):
         "gflops_step": round(sum(flops[n] for n in names) / (ms_per_step * 1e-3) / 1e9, 1),
         "hbm_measured": {"stream_read_4GiB_gbps": round(read_peak, 1),
                          "stream_read_spmv_size_gbps": round(small_gbps, 1),
-                         "stream_read_spmv_size_us": round(small_us, 3)},
+                         "stream_read_spmv_size_us": round(small_us, 3),
+                         "stream_read_W_us": round(w_read_us, 3),
+                         "stream_read_W_gbps": round(w_bytes / (w_read_us * 1e-6) / 1e9, 1)},
+        "encode_frac_of_W_read": round(w_read_us / kernels["encode"]["avg_us"], 4),
         "spmv_frac_of_measured_read_peak": round(kernels["spmv"]["gbps"] / read_peak, 4),
         "packed_offsets": packed_ctx,
+        "prune_counts": prune_ctx,
         "dense_masked_context": dense_ctx,
         "host": {"plan_ms": round(plan_ms, 3), "enqueue_us_per_step": round(host_us, 2)},
     }

@@ -103,6 +103,15 @@ typedef struct {
 int darb_plan_create(int64_t M, int64_t N, const double *row_density, double matrix_density,
                      int round_mode, int b_min, int b_max, darb_plan **out);
 
+/*
+ * darb_plan_create from kept counts: row_density[r] = row_count[r] / N and
+ * matrix_density = kept / (M * N), as produced by darb_prune_counts.
+ *   row_count  host int64 [M], each in [0, N];  kept in [0, M * N]
+ * Errors: DARB_E_INVALID, DARB_E_NOMEM.
+ */
+int darb_plan_create_counts(int64_t M, int64_t N, const int64_t *row_count, int64_t kept,
+                            int round_mode, int b_min, int b_max, darb_plan **out);
+
 /* Sizes and groups of a plan.  Errors: DARB_E_INVALID (null pointer). */
 int darb_plan_info(const darb_plan *plan, darb_plan_info_t *info);
 
@@ -207,6 +216,28 @@ int darb_spmv_packed(const darb_plan *plan, int wdtype, const void *values,
 int darb_spmm_packed(const darb_plan *plan, int wdtype, const void *values,
                      const uint32_t *packed, int xdtype, int64_t B, const void *X, int64_t ldx,
                      float *Y, int64_t ldy, void *stream);
+
+/*
+ * Irregular magnitude pruning, the step DARB starts from (section 3.2: the
+ * irregular mask is computed only to measure each row's density; irregular
+ * pruning keeps the K largest-magnitude weights, section 2).  Keeps the k
+ * elements of W with the largest magnitude -- the stored bits with the sign
+ * cleared, compared as unsigned integers, as in darb_encode; among equal
+ * magnitudes the lower flat index r * N + c first -- and writes how many each
+ * row keeps.  No mask is materialised.
+ *   wdtype     DARB_F32 or DARB_F16
+ *   W          device [M x ldw] row-major, ldw >= N (elements)
+ *   k          0 <= k <= M * N
+ *   counts     device int64 [M], 8-byte aligned, overwritten
+ *   workspace  device, 256-byte aligned, >= the size darb_prune_workspace
+ *              returns; its contents on entry do not matter
+ * Work is enqueued on `stream` only (several kernels, no host synchronisation);
+ * calls sharing a workspace must not overlap.
+ * Errors: DARB_E_INVALID, DARB_E_DTYPE, DARB_E_WORKSPACE, DARB_E_HIP.
+ */
+int darb_prune_workspace(int64_t M, int64_t N, int wdtype, int64_t *bytes);
+int darb_prune_counts(int64_t M, int64_t N, int wdtype, const void *W, int64_t ldw, int64_t k,
+                      int64_t *counts, void *workspace, int64_t workspace_bytes, void *stream);
 
 /*
  * One LSTM layer over a sequence with DARB-stored weights (the recurrent

@@ -5,6 +5,8 @@ kernels.  torch supplies device memory and the current HIP stream; numpy
 arrays are accepted for host-side inputs (row densities).
 
     plan = Plan(M, N, row_density, matrix_density, mode=ROUND_FLOOR, b_min=4, b_max=64)
+    # or, from the device-side irregular pruning of W (k largest magnitudes):
+    #   plan = Plan.from_counts(N, prune_counts(W, k), k, ROUND_FLOOR, 4, 64)
     plan.upload()                           # device metadata into a torch workspace
     values, offsets = plan.encode(W)        # W: cuda tensor [M, N] fp32/fp16
     y = plan.spmv(values, offsets, x)       # fp32 [M]
@@ -84,6 +86,9 @@ def _load_library():
         "darb_decode": ([P, I, P, P, P, I64, P], I),
         "darb_spmv": ([P, I, P, P, I, P, P, P], I),
         "darb_spmm": ([P, I, P, P, I, I64, P, I64, P, I64, P], I),
+        "darb_plan_create_counts": ([I64, I64, P, I64, I, I, I, ctypes.POINTER(P)], I),
+        "darb_prune_workspace": ([I64, I64, I, ctypes.POINTER(I64)], I),
+        "darb_prune_counts": ([I64, I64, I, P, I64, I64, P, P, I64, P], I),
         "darb_pack_offsets": ([P, P, P, P], I),
         "darb_unpack_offsets": ([P, P, P, P], I),
         "darb_spmv_packed": ([P, I, P, P, I, P, P, P], I),
@@ -102,7 +107,8 @@ def _load_library():
 _lib = _load_library()
 
 #: every symbol include/darb.h declares
-EXPORTED = ("darb_plan_create", "darb_plan_info", "darb_plan_export", "darb_plan_upload",
+EXPORTED = ("darb_plan_create", "darb_plan_create_counts", "darb_prune_workspace",
+            "darb_prune_counts", "darb_plan_info", "darb_plan_export", "darb_plan_upload",
             "darb_plan_destroy", "darb_encode", "darb_decode", "darb_spmv", "darb_spmm",
             "darb_pack_offsets", "darb_unpack_offsets", "darb_spmv_packed", "darb_spmm_packed",
             "darb_lstm_layer", "darb_stream_read", "darb_stream_copy", "darb_strerror",
@@ -172,14 +178,20 @@ class Plan:
     """A DARB plan: block sizes and grouped layout from row densities (section 3.2)."""
 
     def __init__(self, M: int, N: int, row_density, matrix_density: float,
-                 mode: int = ROUND_FLOOR, b_min: int = 1, b_max: int = 128):
-        d = np.ascontiguousarray(row_density, dtype=np.float64)
-        if d.shape != (M,):
-            raise ValueError(f"row_density must have shape ({M},)")
+                 mode: int = ROUND_FLOOR, b_min: int = 1, b_max: int = 128, *, _counts=None):
         h = ctypes.c_void_p()
-        _check(_lib.darb_plan_create(int(M), int(N), d.ctypes.data_as(ctypes.c_void_p),
-                                     float(matrix_density), int(mode), int(b_min), int(b_max),
-                                     ctypes.byref(h)), "darb_plan_create")
+        if _counts is None:
+            d = np.ascontiguousarray(row_density, dtype=np.float64)
+            if d.shape != (M,):
+                raise ValueError(f"row_density must have shape ({M},)")
+            _check(_lib.darb_plan_create(int(M), int(N), d.ctypes.data_as(ctypes.c_void_p),
+                                         float(matrix_density), int(mode), int(b_min),
+                                         int(b_max), ctypes.byref(h)), "darb_plan_create")
+        else:
+            c, kept = _counts
+            _check(_lib.darb_plan_create_counts(int(M), int(N), c.ctypes.data_as(ctypes.c_void_p),
+                                                int(kept), int(mode), int(b_min), int(b_max),
+                                                ctypes.byref(h)), "darb_plan_create_counts")
         self._h = h
         info = _Info()
         _check(_lib.darb_plan_info(h, ctypes.byref(info)), "darb_plan_info")
@@ -190,6 +202,17 @@ class Plan:
                           first_elem=b.first_elem, nblk=b.nblk, first_word=b.first_word)
                      for b in info.bins[:info.nbins]]
         self.workspace = None
+
+    @classmethod
+    def from_counts(cls, N: int, row_count, kept: int, mode: int = ROUND_FLOOR, b_min: int = 1,
+                    b_max: int = 128):
+        """Plan from per-row kept counts (e.g. ``prune_counts``): d_r = count_r / N."""
+        if hasattr(row_count, "is_cuda"):
+            row_count = row_count.cpu().numpy()
+        c = np.ascontiguousarray(row_count, dtype=np.int64)
+        if c.ndim != 1:
+            raise ValueError("row_count must be 1-D")
+        return cls(c.shape[0], N, None, 0.0, mode, b_min, b_max, _counts=(c, kept))
 
     def __del__(self):
         h = getattr(self, "_h", None)
@@ -358,6 +381,32 @@ class Plan:
             raise TypeError("Y must be fp32")
         ldy = _row_major_ld(Y, self.M, B, "Y")
         return B, ldx, Y, ldy
+
+
+def prune_counts(W, k: int, counts=None, workspace=None, stream=None):
+    """Per-row counts of the k largest-magnitude elements of W (cuda, fp32/fp16).
+
+    The irregular-pruning step DARB starts from (section 3.2), on the device.
+    Returns an int64 cuda tensor [M].
+    """
+    torch = _torch()
+    _require_cuda(W)
+    if W.dim() != 2:
+        raise ValueError("W must be 2-D")
+    M, N = W.shape
+    ldw = _row_major_ld(W, M, N, "W")
+    code = _dtype_code(W)
+    need = ctypes.c_int64()
+    _check(_lib.darb_prune_workspace(M, N, code, ctypes.byref(need)), "darb_prune_workspace")
+    if workspace is None:
+        workspace = torch.empty(need.value, dtype=torch.uint8, device=W.device)
+    if counts is None:
+        counts = torch.empty(M, dtype=torch.int64, device=W.device)
+    _check_format(counts, M, "counts", (torch.int64,))
+    _check_format(workspace, need.value, "workspace", (torch.uint8,))
+    _check(_lib.darb_prune_counts(M, N, code, _ptr(W), ldw, int(k), _ptr(counts), _ptr(workspace),
+                                  workspace.numel(), _stream_ptr(stream)), "darb_prune_counts")
+    return counts
 
 
 def lstm_layer(wih: Tuple[Plan, object, object], whh: Tuple[Plan, object, object], x_seq,

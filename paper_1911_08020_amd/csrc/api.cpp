@@ -71,6 +71,30 @@ const char *darb_strerror(int code) {
 
 const char *darb_last_error(void) { return g_last_error.c_str(); }
 
+int darb_plan_create_counts(int64_t M, int64_t N, const int64_t *row_count, int64_t kept,
+                            int round_mode, int b_min, int b_max, darb_plan **out) {
+    clear_error();
+    if (!out) return fail(DARB_E_INVALID, "out is NULL");
+    *out = nullptr;
+    if (M < 1 || M >= (int64_t(1) << 31)) return fail(DARB_E_INVALID, "M must be in [1, 2^31)");
+    if (N < 1 || N >= (int64_t(1) << 31)) return fail(DARB_E_INVALID, "N must be in [1, 2^31)");
+    if (!row_count) return fail(DARB_E_INVALID, "row_count is NULL");
+    if (kept < 0 || kept > M * N) return fail(DARB_E_INVALID, "kept must be in [0, M*N]");
+    std::vector<double> d;
+    try {
+        d.resize(M);
+    } catch (const std::bad_alloc &) {
+        return fail(DARB_E_NOMEM, "densities");
+    }
+    for (int64_t r = 0; r < M; ++r) {
+        if (row_count[r] < 0 || row_count[r] > N)
+            return fail(DARB_E_INVALID, "row_count[" + std::to_string(r) + "] not in [0, N]");
+        d[r] = double(row_count[r]) / double(N);
+    }
+    return darb_plan_create(M, N, d.data(), double(kept) / (double(M) * double(N)), round_mode,
+                            b_min, b_max, out);
+}
+
 int darb_plan_create(int64_t M, int64_t N, const double *row_density, double matrix_density,
                      int round_mode, int b_min, int b_max, darb_plan **out) {
     clear_error();
@@ -372,6 +396,36 @@ int darb_spmm_packed(const darb_plan *p, int wdtype, const void *values, const u
     if (rc) return rc;
     return launched(launch_spmm(*p, wdtype, values, nullptr, packed, xdtype, B, X, ldx, Y, ldy,
                                 static_cast<hipStream_t>(stream)), "spmm (packed) launch");
+}
+
+int darb_prune_workspace(int64_t M, int64_t N, int wdtype, int64_t *bytes) {
+    clear_error();
+    if (!bytes) return fail(DARB_E_INVALID, "bytes is NULL");
+    if (M < 1 || M >= (int64_t(1) << 31) || N < 1 || N >= (int64_t(1) << 31))
+        return fail(DARB_E_INVALID, "M and N must be in [1, 2^31)");
+    if (!valid_dtype(wdtype)) return fail(DARB_E_DTYPE, "unknown weight dtype");
+    *bytes = prune_workspace_bytes(M, N, wdtype);
+    return DARB_OK;
+}
+
+int darb_prune_counts(int64_t M, int64_t N, int wdtype, const void *W, int64_t ldw, int64_t k,
+                      int64_t *counts, void *workspace, int64_t workspace_bytes, void *stream) {
+    clear_error();
+    if (M < 1 || M >= (int64_t(1) << 31) || N < 1 || N >= (int64_t(1) << 31))
+        return fail(DARB_E_INVALID, "M and N must be in [1, 2^31)");
+    if (!valid_dtype(wdtype)) return fail(DARB_E_DTYPE, "unknown weight dtype");
+    if (!W || !counts || !workspace) return fail(DARB_E_INVALID, "NULL buffer");
+    if (ldw < N) return fail(DARB_E_INVALID, "ldw < N");
+    if (k < 0 || k > M * N) return fail(DARB_E_INVALID, "k must be in [0, M*N]");
+    if ((reinterpret_cast<uintptr_t>(workspace) & 255) != 0)
+        return fail(DARB_E_INVALID, "workspace must be 256-byte aligned");
+    if ((reinterpret_cast<uintptr_t>(counts) & 7) != 0)
+        return fail(DARB_E_INVALID, "counts must be 8-byte aligned");
+    const int64_t need = prune_workspace_bytes(M, N, wdtype);
+    if (workspace_bytes < need)
+        return fail(DARB_E_WORKSPACE, "pruning workspace needs " + std::to_string(need) + " bytes");
+    return launched(launch_prune_counts(M, N, wdtype, W, ldw, k, counts, workspace,
+                                        static_cast<hipStream_t>(stream)), "prune launch");
 }
 
 int darb_lstm_layer(const darb_plan *wih, const void *wih_values, const uint8_t *wih_offsets,

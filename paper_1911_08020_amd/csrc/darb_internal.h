@@ -79,6 +79,9 @@ hipError_t launch_pack_offsets(const darb_plan &p, const uint8_t *offsets, uint3
                                hipStream_t s);
 hipError_t launch_unpack_offsets(const darb_plan &p, const uint32_t *packed, uint8_t *offsets,
                                  hipStream_t s);
+int64_t prune_workspace_bytes(int64_t M, int64_t N, int wdtype);
+hipError_t launch_prune_counts(int64_t M, int64_t N, int wdtype, const void *W, int64_t ldw,
+                               int64_t k, int64_t *counts, void *workspace, hipStream_t s);
 hipError_t launch_lstm_cell(int64_t H, int64_t batch, const float *G, const float *U,
                             int64_t ldu, float *h, float *c, float *h_seq, int64_t ld_seq,
                             hipStream_t s);

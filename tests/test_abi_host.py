@@ -104,6 +104,48 @@ def test_plan_packed_words_table7():
     assert p.packed_words == want == 24 + 24 + 18 + 12 + 10 + 6
 
 
+def test_plan_from_counts_equals_plan_from_densities():
+    rng = np.random.default_rng(4)
+    M, N = 200, 1000
+    counts = rng.integers(0, N + 1, size=M)
+    counts[:7] = 0
+    kept = int(counts.sum())
+    for mode in (darb.ROUND_FLOOR, darb.ROUND_PAPER):
+        a = darb.Plan.from_counts(N, counts, kept, mode, 2, 128)
+        b = darb.Plan(M, N, counts / N, kept / (M * N), mode, 2, 128)
+        for x, y in zip(a.export(), b.export()):
+            assert np.array_equal(x, y)
+    L = darb.lib()
+    h = ctypes.c_void_p()
+    c = np.array([1, 2, 3], dtype=np.int64)
+    P = c.ctypes.data_as(ctypes.c_void_p)
+    assert L.darb_plan_create_counts(3, 2, P, 3, 0, 1, 2, ctypes.byref(h)) == darb.E_INVALID
+    assert L.darb_plan_create_counts(3, 4, P, 13, 0, 1, 2, ctypes.byref(h)) == darb.E_INVALID
+    assert L.darb_plan_create_counts(3, 4, None, 3, 0, 1, 2, ctypes.byref(h)) == darb.E_INVALID
+
+
+def test_prune_argument_checks():
+    L = darb.lib()
+    nbytes = ctypes.c_int64()
+    assert L.darb_prune_workspace(64, 300, darb.F32, ctypes.byref(nbytes)) == 0
+    assert nbytes.value > 0 and nbytes.value % 256 == 0
+    assert L.darb_prune_workspace(64, 300, 7, ctypes.byref(nbytes)) == darb.E_DTYPE
+    assert L.darb_prune_workspace(0, 300, darb.F32, ctypes.byref(nbytes)) == darb.E_INVALID
+    buf = ctypes.c_void_p(0x1000)
+    # every check fails before any HIP work
+    assert L.darb_prune_counts(4, 8, darb.F32, buf, 8, 33, buf, buf, 1 << 20, None) \
+        == darb.E_INVALID                                     # k > M*N
+    assert L.darb_prune_counts(4, 8, darb.F32, buf, 7, 3, buf, buf, 1 << 20, None) \
+        == darb.E_INVALID                                     # ldw < N
+    assert L.darb_prune_counts(4, 8, darb.F32, None, 8, 3, buf, buf, 1 << 20, None) \
+        == darb.E_INVALID
+    assert L.darb_prune_counts(4, 8, darb.F32, buf, 8, 3, buf, ctypes.c_void_p(0x1010),
+                               1 << 20, None) == darb.E_INVALID  # workspace alignment
+    assert L.darb_prune_counts(4, 8, darb.F32, buf, 8, 3, buf, buf, 16, None) \
+        == darb.E_WORKSPACE
+    assert L.darb_prune_counts(4, 8, 9, buf, 8, 3, buf, buf, 1 << 20, None) == darb.E_DTYPE
+
+
 def test_plan_table7_and_worked_example():
     p = darb.Plan(6, 1500, np.array([0.5, 0.25, 0.125, 1 / 16, 1 / 32, 1 / 64]), 0.1,
                   darb.ROUND_FLOOR, 1, 128)

@@ -1,0 +1,131 @@
+"""GPU parity of the device-side irregular pruning (section 3.2's first step).
+
+The per-row kept counts of the k largest-magnitude elements are integers and
+unique (ties go to the lower flat index), so the HIP result must equal the
+oracle's exactly.
+"""
+import ctypes
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+import workloads
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+def say(*a):
+    print(*a, flush=True, file=sys.stderr)
+
+
+@pytest.fixture(scope="module")
+def darb():
+    assert torch.cuda.is_available(), "GPU tests need a visible MI355X"
+    import paper_1911_08020_amd as d
+    return d
+
+
+def dev(a: np.ndarray):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def gpu_counts(darb, Wd, k):
+    c = darb.prune_counts(Wd, k)
+    torch.cuda.synchronize()
+    return c.cpu().numpy()
+
+
+@pytest.mark.parametrize("name", ["lstm_tiny", "lstm_1024", "gru_1536", "fc_9216", "lstm2_seq"])
+def test_config_counts_equal_oracle(darb, name):
+    cfg, mi, _, _ = workloads.make_config(name, seed=0)
+    say(f"{name}: prune {cfg.M}x{cfg.N} {cfg.wdtype}, k = {mi.k}")
+    got = gpu_counts(darb, dev(mi.W), mi.k)
+    assert got.sum() == mi.k
+    assert np.array_equal(got, oracle.prune_counts(mi.W, mi.k))
+    # the plan built on the device counts is the plan of the generator's densities
+    a = darb.Plan.from_counts(cfg.N, got, mi.k, darb.ROUND_FLOOR, cfg.b_min, cfg.b_max)
+    b = darb.Plan(cfg.M, cfg.N, mi.row_density, mi.matrix_density, darb.ROUND_FLOOR,
+                  cfg.b_min, cfg.b_max)
+    for x, y in zip(a.export(), b.export()):
+        assert np.array_equal(x, y)
+
+
+@pytest.mark.parametrize("dtype", [np.float32, np.float16])
+@pytest.mark.parametrize("seed", range(4))
+def test_random_ties_and_every_k_class(darb, dtype, seed):
+    # few distinct magnitudes (heavy ties at the threshold), ragged shapes
+    rng = np.random.default_rng(seed)
+    M, N = int(rng.integers(1, 90)), int(rng.integers(1, 5000))
+    W = (rng.integers(-6, 7, size=(M, N)) * 0.25).astype(dtype)
+    W[rng.random((M, N)) < 0.05] = -0.0
+    Wd = dev(W)
+    size = M * N
+    for k in sorted({0, 1, 2, size // 7, size // 2, size - 1, size}):
+        if k < 0:
+            continue
+        say(f"  {dtype.__name__} {M}x{N} k={k}")
+        assert np.array_equal(gpu_counts(darb, Wd, k), oracle.prune_counts(W, k)), k
+
+
+@pytest.mark.parametrize("dtype", [np.float32, np.float16])
+def test_continuous_values_many_digits(darb, dtype):
+    # distinct magnitudes spread over many exponents: every radix digit matters
+    rng = np.random.default_rng(11)
+    M, N = 300, 2500
+    W = (rng.standard_normal((M, N)) * np.exp(rng.uniform(-8, 4, size=(M, N)))).astype(dtype)
+    Wd = dev(W)
+    for keep in (0.003, 0.05, 0.5, 0.97):
+        k = int(np.floor(keep * M * N + 0.5))
+        assert np.array_equal(gpu_counts(darb, Wd, k), oracle.prune_counts(W, k)), keep
+
+
+def test_special_values(darb):
+    W = np.zeros((6, 40), dtype=np.float32)
+    W[0, 3], W[1, 0], W[2, 39], W[3, 7] = np.nan, np.inf, -np.inf, 1e-45
+    W[4, :] = -0.0
+    W[5, 10:20] = 3.0
+    for k in range(0, 240, 7):
+        assert np.array_equal(gpu_counts(darb, dev(W), k), oracle.prune_counts(W, k)), k
+
+
+def test_all_equal_takes_flat_order(darb):
+    M, N = 37, 1111
+    W = np.full((M, N), 0.5, dtype=np.float16)
+    for k in (1, N - 1, N, 5 * N + 3, M * N - 2):
+        want = np.array([min(N, max(0, k - r * N)) for r in range(M)], dtype=np.int64)
+        assert np.array_equal(gpu_counts(darb, dev(W), k), want), k
+
+
+@pytest.mark.parametrize("dtype", [np.float32, np.float16])
+def test_strided_and_misaligned_rows(darb, dtype):
+    rng = np.random.default_rng(21)
+    M, N = 50, 1500
+    W = rng.standard_normal((M, N)).astype(dtype)
+    k = 4321
+    ref = oracle.prune_counts(W, k)
+    # a leading dimension larger than N, and rows starting off a 16-byte boundary
+    big = torch.zeros((M, N + 9), dtype=torch.float32 if dtype == np.float32 else torch.float16,
+                      device="cuda")
+    big[:, 1:N + 1] = dev(W)
+    view = big[:, 1:N + 1]
+    assert view.stride(0) == N + 9
+    assert np.array_equal(gpu_counts(darb, view, k), ref)
+
+
+def test_repeat_calls_reuse_workspace(darb):
+    # a workspace reused across calls holds the previous call's state: results
+    # must not depend on it
+    rng = np.random.default_rng(3)
+    W = rng.standard_normal((64, 777)).astype(np.float32)
+    Wd = dev(W)
+    nbytes = ctypes.c_int64()
+    assert darb.lib().darb_prune_workspace(64, 777, darb.F32, ctypes.byref(nbytes)) == 0
+    ws = torch.full((nbytes.value,), 0xAB, dtype=torch.uint8, device="cuda")
+    for k in (5000, 17, 5000, 0, 49000):
+        c = darb.prune_counts(Wd, k, workspace=ws)
+        torch.cuda.synchronize()
+        assert np.array_equal(c.cpu().numpy(), oracle.prune_counts(W, k)), k
