@@ -392,10 +392,12 @@ def main(argv=None):
     packed_ctx = {"words": pw, "bits_per_index": round(32.0 * pw / plan.nnz, 3),
                   "format_bytes": plan.nnz * s_w + 4 * pw,
                   "equals_byte_offset_products": pk_same}
+    traffic = stored_traffic(args.workload, B)
     for n, us in pk_us.items():
         gbps = pk_bytes[n] / (us * 1e-6) / 1e9
         packed_ctx[n] = {"avg_us": round(us, 3), "bytes": int(pk_bytes[n]), "gbps": round(gbps, 1),
-                         "frac_hbm_peak": round(gbps / HBM_PEAK_GBPS, 4)}
+                         "frac_hbm_peak": round(gbps / HBM_PEAK_GBPS, 4),
+                         "traffic_bytes": traffic.get(n if n == "pack" else n + "_packed")}
     del packed
 
     # HBM reference rates measured in the same process: a plain stream read over
@@ -474,7 +476,6 @@ def main(argv=None):
             dense_ctx["csr_error"] = str(e)[:120]
     del dense, xs_t, Xs_t
 
-    traffic = stored_traffic(args.workload, B)
     for n in names:
         kernels[n]["traffic_bytes"] = traffic.get(n)
     step_total = sum(nbytes.values())
