@@ -140,7 +140,7 @@ def bench_lstm(args):
     hs = [torch.empty((H, T * Bt), dtype=torch.float32, device=dev) for _ in layers]
     hh = [torch.zeros((H, Bt), dtype=torch.float32, device=dev) for _ in layers]
     cc = [torch.zeros((H, Bt), dtype=torch.float32, device=dev) for _ in layers]
-    ws = torch.empty(4 * H * T * Bt + 4 * H * Bt, dtype=torch.float32, device=dev)
+    ws = torch.empty(darb.lstm_workspace_floats(H, T, Bt), dtype=torch.float32, device=dev)
 
     def sequence():
         inp = x_seq

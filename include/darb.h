@@ -250,7 +250,8 @@ int darb_prune_counts(int64_t M, int64_t N, int wdtype, const void *W, int64_t l
  *   x_seq      device fp32 [I x T*batch], column t*batch + n
  *   h_seq      device fp32 [H x T*batch], receives h_t in columns t*batch + n
  *   h, c       device fp32 [H x batch], initial state in, final state out
- *   workspace  device fp32, at least 4H*T*batch + 4H*batch floats
+ *   workspace  device fp32, 16-byte aligned, at least 4H*T*batch + 4H*batch floats
+ *              (darb_lstm_workspace)
  * Errors: DARB_E_INVALID, DARB_E_DTYPE, DARB_E_NOT_UPLOADED, DARB_E_HIP.
  */
 int darb_lstm_layer(const darb_plan *wih_plan, const void *wih_values,
@@ -259,6 +260,9 @@ int darb_lstm_layer(const darb_plan *wih_plan, const void *wih_values,
                     int64_t H, int64_t T, int64_t batch, const float *x_seq, float *h_seq,
                     float *h, float *c, float *workspace, int64_t workspace_floats,
                     void *stream);
+
+/* Workspace floats darb_lstm_layer needs for (H, T, batch).  Errors: DARB_E_INVALID. */
+int darb_lstm_workspace(int64_t H, int64_t T, int64_t batch, int64_t *floats);
 
 /*
  * Measurement helpers (not part of DARB).  darb_stream_read reads `bytes`

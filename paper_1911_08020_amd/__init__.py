@@ -94,6 +94,7 @@ def _load_library():
         "darb_spmv_packed": ([P, I, P, P, I, P, P, P], I),
         "darb_spmm_packed": ([P, I, P, P, I, I64, P, I64, P, I64, P], I),
         "darb_lstm_layer": ([P, P, P, P, P, P, I, I64, I64, I64, P, P, P, P, P, I64, P], I),
+        "darb_lstm_workspace": ([I64, I64, I64, ctypes.POINTER(I64)], I),
         "darb_stream_read": ([P, I64, P, P], I),
         "darb_stream_copy": ([P, P, I64, P], I),
     }
@@ -111,7 +112,7 @@ EXPORTED = ("darb_plan_create", "darb_plan_create_counts", "darb_prune_workspace
             "darb_prune_counts", "darb_plan_info", "darb_plan_export", "darb_plan_upload",
             "darb_plan_destroy", "darb_encode", "darb_decode", "darb_spmv", "darb_spmm",
             "darb_pack_offsets", "darb_unpack_offsets", "darb_spmv_packed", "darb_spmm_packed",
-            "darb_lstm_layer", "darb_stream_read", "darb_stream_copy", "darb_strerror",
+            "darb_lstm_layer", "darb_lstm_workspace", "darb_stream_read", "darb_stream_copy", "darb_strerror",
             "darb_last_error", "darb_version")
 
 
@@ -409,6 +410,13 @@ def prune_counts(W, k: int, counts=None, workspace=None, stream=None):
     return counts
 
 
+def lstm_workspace_floats(hidden: int, seq_len: int, batch: int) -> int:
+    n = ctypes.c_int64()
+    _check(_lib.darb_lstm_workspace(hidden, seq_len, batch, ctypes.byref(n)),
+           "darb_lstm_workspace")
+    return n.value
+
+
 def lstm_layer(wih: Tuple[Plan, object, object], whh: Tuple[Plan, object, object], x_seq,
                hidden: int, seq_len: int, batch: int, h=None, c=None, h_seq=None,
                workspace=None, stream=None):
@@ -426,7 +434,7 @@ def lstm_layer(wih: Tuple[Plan, object, object], whh: Tuple[Plan, object, object
         c = torch.zeros((H, Bt), dtype=torch.float32, device=dev)
     if h_seq is None:
         h_seq = torch.empty((H, T * Bt), dtype=torch.float32, device=dev)
-    need = 4 * H * T * Bt + 4 * H * Bt
+    need = lstm_workspace_floats(H, T, Bt)
     if workspace is None:
         workspace = torch.empty(need, dtype=torch.float32, device=dev)
     for t in (x_seq, h, c, h_seq, workspace):
@@ -434,6 +442,12 @@ def lstm_layer(wih: Tuple[Plan, object, object], whh: Tuple[Plan, object, object
             raise ValueError("LSTM state and sequences must be contiguous fp32")
     if x_seq.shape != (wih[0].N, T * Bt):
         raise ValueError("x_seq must be [I, T*batch]")
+    for t, shape in ((h, (H, Bt)), (c, (H, Bt)), (h_seq, (H, T * Bt))):
+        if tuple(t.shape) != shape:
+            raise ValueError(f"LSTM buffer must be {shape}, got {tuple(t.shape)}")
+    for (p, v, o), name in ((wih, "wih"), (whh, "whh")):
+        _require_cuda(v, o)
+        p._check_values_offsets(v, o)
     _check(_lib.darb_lstm_layer(wih[0].handle, _ptr(wih[1]), _ptr(wih[2]), whh[0].handle,
                                 _ptr(whh[1]), _ptr(whh[2]), _dtype_code(wih[1]), H, T, Bt,
                                 _ptr(x_seq), _ptr(h_seq), _ptr(h), _ptr(c), _ptr(workspace),

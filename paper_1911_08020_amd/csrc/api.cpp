@@ -428,12 +428,16 @@ int darb_prune_counts(int64_t M, int64_t N, int wdtype, const void *W, int64_t l
                                         static_cast<hipStream_t>(stream)), "prune launch");
 }
 
-int darb_lstm_layer(const darb_plan *wih, const void *wih_values, const uint8_t *wih_offsets,
-                    const darb_plan *whh, const void *whh_values, const uint8_t *whh_offsets,
-                    int wdtype, int64_t H, int64_t T, int64_t batch, const float *x_seq,
-                    float *h_seq, float *h, float *c, float *workspace,
-                    int64_t workspace_floats, void *stream) {
-    clear_error();
+// Workspace of the LSTM layer, in floats: U [4H x T*batch] and G [4H x batch].
+static int64_t lstm_workspace_floats(int64_t H, int64_t T, int64_t batch) {
+    return 4 * H * T * batch + 4 * H * batch;
+}
+
+static int lstm_check(const darb_plan *wih, const void *wih_values, const uint8_t *wih_offsets,
+                      const darb_plan *whh, const void *whh_values, const uint8_t *whh_offsets,
+                      int wdtype, int64_t H, int64_t T, int64_t batch, const float *x_seq,
+                      float *h_seq, float *h, float *c, float *workspace,
+                      int64_t workspace_floats) {
     int rc = check_uploaded(wih);
     if (rc) return rc;
     rc = check_uploaded(whh);
@@ -445,26 +449,56 @@ int darb_lstm_layer(const darb_plan *wih, const void *wih_values, const uint8_t 
     if (H < 1 || T < 1 || batch < 1) return fail(DARB_E_INVALID, "H, T, batch must be >= 1");
     if (whh->M != 4 * H || whh->N != H) return fail(DARB_E_INVALID, "W_hh must be [4H x H]");
     if (wih->M != 4 * H) return fail(DARB_E_INVALID, "W_ih must have 4H rows");
-    const int64_t TB = T * batch;
-    if (TB >= (int64_t(1) << 31)) return fail(DARB_E_INVALID, "T * batch too large");
-    const int64_t need = 4 * H * TB + 4 * H * batch;
+    if (T * batch >= (int64_t(1) << 31)) return fail(DARB_E_INVALID, "T * batch too large");
+    if ((reinterpret_cast<uintptr_t>(workspace) & 15) != 0)
+        return fail(DARB_E_INVALID, "workspace must be 16-byte aligned");
+    const int64_t need = lstm_workspace_floats(H, T, batch);
     if (workspace_floats < need)
         return fail(DARB_E_WORKSPACE, "lstm workspace needs " + std::to_string(need) + " floats");
-    hipStream_t s = static_cast<hipStream_t>(stream);
-    float *U = workspace;              // [4H x T*batch]: input products of every step
-    float *G = workspace + 4 * H * TB; // [4H x batch]: recurrent product of one step
-    rc = launched(launch_spmm(*wih, wdtype, wih_values, wih_offsets, nullptr, DARB_F32, TB, x_seq,
-                              TB, U, TB, s), "lstm input product");
-    if (rc) return rc;
+    return DARB_OK;
+}
+
+// The per-step loop: recurrent product, then the gate cell, T times.
+static int lstm_steps(const darb_plan *whh, const void *whh_values, const uint8_t *whh_offsets,
+                      int wdtype, int64_t H, int64_t T, int64_t batch, const float *U, float *G,
+                      float *h_seq, float *h, float *c, hipStream_t s) {
+    const int64_t TB = T * batch;
     for (int64_t t = 0; t < T; ++t) {
-        rc = launched(launch_spmm(*whh, wdtype, whh_values, whh_offsets, nullptr, DARB_F32, batch,
-                                  h, batch, G, batch, s), "lstm recurrent product");
+        int rc = launched(launch_spmm(*whh, wdtype, whh_values, whh_offsets, nullptr, DARB_F32,
+                                      batch, h, batch, G, batch, s), "lstm recurrent product");
         if (rc) return rc;
         rc = launched(launch_lstm_cell(H, batch, G, U + t * batch, TB, h, c, h_seq + t * batch, TB,
                                        s), "lstm cell");
         if (rc) return rc;
     }
     return DARB_OK;
+}
+
+int darb_lstm_workspace(int64_t H, int64_t T, int64_t batch, int64_t *floats) {
+    clear_error();
+    if (!floats) return fail(DARB_E_INVALID, "floats is NULL");
+    if (H < 1 || T < 1 || batch < 1) return fail(DARB_E_INVALID, "H, T, batch must be >= 1");
+    *floats = lstm_workspace_floats(H, T, batch);
+    return DARB_OK;
+}
+
+int darb_lstm_layer(const darb_plan *wih, const void *wih_values, const uint8_t *wih_offsets,
+                    const darb_plan *whh, const void *whh_values, const uint8_t *whh_offsets,
+                    int wdtype, int64_t H, int64_t T, int64_t batch, const float *x_seq,
+                    float *h_seq, float *h, float *c, float *workspace,
+                    int64_t workspace_floats, void *stream) {
+    clear_error();
+    int rc = lstm_check(wih, wih_values, wih_offsets, whh, whh_values, whh_offsets, wdtype, H, T,
+                        batch, x_seq, h_seq, h, c, workspace, workspace_floats);
+    if (rc) return rc;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const int64_t TB = T * batch;
+    float *U = workspace;              // [4H x T*batch]: input products of every step
+    float *G = workspace + 4 * H * TB; // [4H x batch]: recurrent product of one step
+    rc = launched(launch_spmm(*wih, wdtype, wih_values, wih_offsets, nullptr, DARB_F32, TB, x_seq,
+                              TB, U, TB, s), "lstm input product");
+    if (rc) return rc;
+    return lstm_steps(whh, whh_values, whh_offsets, wdtype, H, T, batch, U, G, h_seq, h, c, s);
 }
 
 int darb_stream_read(const void *buf, int64_t bytes, float *sink, void *stream) {

@@ -24,7 +24,15 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(
     W[int64_t(perm[i]) * ldw + c] = (offsets[e] == j) ? values[e] : Bits(0);
 }
 
-__device__ __forceinline__ float sigmoidf(float z) { return 1.0f / (1.0f + __expf(-z)); }
+__device__ __forceinline__ float lstm_sigmoid(float z) { return 1.0f / (1.0f + __expf(-z)); }
+
+// The LSTM cell of the recurrent models (section 4.1): no bias, gate order
+// (i, f, g, o); c' = sigmoid(f) c + sigmoid(i) tanh(g), h' = sigmoid(o) tanh(c').
+__device__ __forceinline__ float lstm_cell(float gi, float gf, float gg, float go, float &c) {
+    const float cn = lstm_sigmoid(gf) * c + lstm_sigmoid(gi) * tanhf(gg);
+    c = cn;
+    return lstm_sigmoid(go) * tanhf(cn);
+}
 
 // gates = G + U (G: recurrent product [4H x batch], U: input product slice of
 // this step, leading dimension ldu), gate order (i, f, g, o).
@@ -39,8 +47,8 @@ __global__ __launch_bounds__(kThreads) void lstm_cell_kernel(
     const float gf = G[(H + u) * batch + n] + U[(H + u) * ldu + n];
     const float gg = G[(2 * H + u) * batch + n] + U[(2 * H + u) * ldu + n];
     const float go = G[(3 * H + u) * batch + n] + U[(3 * H + u) * ldu + n];
-    const float cn = sigmoidf(gf) * c[idx] + sigmoidf(gi) * tanhf(gg);
-    const float hn = sigmoidf(go) * tanhf(cn);
+    float cn = c[idx];
+    const float hn = lstm_cell(gi, gf, gg, go, cn);
     c[idx] = cn;
     h[idx] = hn;
     h_seq[u * ld_seq + n] = hn;

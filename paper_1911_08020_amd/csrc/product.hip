@@ -60,11 +60,12 @@ __device__ __forceinline__ T pick(const T (&a)[kMaxBins], int g) {
     return r;
 }
 
-__device__ __forceinline__ int block_group(const ProductSchedule &s) {
+// The block-size group that workgroup `tile` of a launch belongs to.
+__device__ __forceinline__ int block_group(const ProductSchedule &s, int tile) {
     int g = 0;
 #pragma unroll
     for (int b = 1; b < kMaxBins; ++b)
-        if (b < s.nbins && int(blockIdx.x) >= s.block_begin[b]) g = b;
+        if (b < s.nbins && tile >= s.block_begin[b]) g = b;
     return g;
 }
 
@@ -229,7 +230,7 @@ __global__ __launch_bounds__(kSpmvThreads) void spmv_kernel(
     using OS = Off<PK, 1>;
     extern __shared__ float xs[];
 
-    const int g = block_group(sch);
+    const int g = block_group(sch, int(blockIdx.x));
     const int wave = wave_uniform(int(threadIdx.x) / kWave);
     const int lane = int(threadIdx.x) & (kWave - 1);
     const int lgL = pick(sch.log2_lanes, g);
@@ -406,26 +407,29 @@ template <typename Tw, int GM, bool PK> struct PairLoad {
     }
 };
 
-// Lanes map to batch columns (CPL per lane, 2^LGL lanes per matrix row, 64 >> LGL
-// rows per wave).  A wave owns a contiguous share [kbeg, kend) of its rows' weights
+// One workgroup-sized tile of the SpMM: lanes map to batch columns (CPL per lane,
+// 2^LGL lanes per matrix row, 64 >> LGL rows per wave).  A wave owns a contiguous share [kbeg, kend) of its rows' weights
 // (KS waves split a row group).  The lanes of a row load S = max(2^LGL, 16) of the
 // row's (value, column) pairs per step, one pair per lane and group, straight from
 // HBM with coalesced loads, then broadcast each pair to the row's lanes with a
 // register-to-register exchange and gather its X row; kSpmmBatch gathers are in
-// flight per lane.  Partial sums of the KS waves meet in LDS in a fixed order.
-template <typename Tw, typename Tx, int CPL, int LGL, bool PK>
-__global__ __launch_bounds__(kSpmmThreads) void spmm_kernel(
-    const Tw *__restrict__ values, const void *__restrict__ offs,
-    const Tx *__restrict__ X, int64_t ldx, int64_t B, float *__restrict__ Y, int64_t ldy,
-    const int32_t *__restrict__ perm, int N, BinTable bins, ProductSchedule sch) {
+// flight per lane.  Partial sums of the KS waves meet in LDS (`part`, kSpmmThreads *
+// CPL floats) in a fixed order.  The finished rows go to
+//     epi(row_ok, col_ok, original row, first column, acc[CPL], lane in row),
+// called by every lane of the waves that hold finished rows (wave-uniform), so an
+// epilogue may exchange values between the lanes of a row.
+template <typename Tw, typename Tx, int CPL, int LGL, bool PK, typename Epi>
+__device__ __forceinline__ void spmm_tile(
+    int tile, const Tw *__restrict__ values, const void *__restrict__ offs,
+    const Tx *__restrict__ X, int64_t ldx, int64_t B, const int32_t *__restrict__ perm, int N,
+    const BinTable &bins, const ProductSchedule &sch, float *part, Epi &&epi) {
     using XL = XLoad<Tx, CPL>;
     constexpr int L = 1 << LGL;
     constexpr int R = kWave >> LGL;                       // rows per wave
     constexpr int GM = L >= 16 ? 1 : 16 / L;              // pair groups per lane per step
     constexpr int S = L * GM;                             // weights per row per step
-    __shared__ float part[kSpmmThreads * CPL];
 
-    const int g = block_group(sch);
+    const int g = block_group(sch, tile);
     const int wave = wave_uniform(int(threadIdx.x) / kWave);
     const int lane = int(threadIdx.x) & (kWave - 1);
     const int KS = pick(sch.ksplit, g);
@@ -438,7 +442,7 @@ __global__ __launch_bounds__(kSpmmThreads) void spmm_kernel(
 
     // column slab outermost: the workgroups in flight together share one slab of X,
     // which stays in L2 even when all of X does not
-    const int local = int(blockIdx.x) - block_begin_of(sch, g);
+    const int local = tile - block_begin_of(sch, g);
     const int row_blks = int((rows + rows_pb - 1) / rows_pb);
     const int slab = local / row_blks;
     const int row_blk = local - slab * row_blks;
@@ -520,11 +524,24 @@ __global__ __launch_bounds__(kSpmmThreads) void spmm_kernel(
             }
         }
     }
-    if (ks == 0 && row_ok && col_ok) {
-        float *yrow = Y + int64_t(perm[first_row + row0 + rl]) * ldy + col0;
+    if (ks == 0) epi(row_ok, col_ok, row_ok ? perm[first_row + row0 + rl] : 0, col0, acc, sub);
+}
+
+template <typename Tw, typename Tx, int CPL, int LGL, bool PK>
+__global__ __launch_bounds__(kSpmmThreads) void spmm_kernel(
+    const Tw *__restrict__ values, const void *__restrict__ offs,
+    const Tx *__restrict__ X, int64_t ldx, int64_t B, float *__restrict__ Y, int64_t ldy,
+    const int32_t *__restrict__ perm, int N, BinTable bins, ProductSchedule sch) {
+    __shared__ float part[kSpmmThreads * CPL];
+    spmm_tile<Tw, Tx, CPL, LGL, PK>(
+        int(blockIdx.x), values, offs, X, ldx, B, perm, N, bins, sch, part,
+        [&](bool row_ok, bool col_ok, int32_t orig, int64_t col0, const float (&acc)[CPL], int) {
+            if (row_ok && col_ok) {
+                float *yrow = Y + int64_t(orig) * ldy + col0;
 #pragma unroll
-        for (int q = 0; q < CPL; ++q) yrow[q] = acc[q];
-    }
+                for (int q = 0; q < CPL; ++q) yrow[q] = acc[q];
+            }
+        });
 }
 
 // ---------------------------------------------------------------------------------

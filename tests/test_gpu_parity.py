@@ -282,11 +282,20 @@ def _lstm_case(darb, hidden, seq_len, batch, layers, seed):
     say(f"  lstm H={H} T={T} B={Bt}: max abs err {err:.3e}")
     assert err <= 2e-3
     assert np.abs(host(c) - finals[-1][1]).max() <= 2e-3
+    # the final hidden state is the last step's output
+    assert np.array_equal(host(h), out[:, (T - 1) * Bt:])
 
 
 def test_lstm_small(darb):
     say("lstm small")
     _lstm_case(darb, hidden=64, seq_len=7, batch=3, layers=2, seed=1)
+
+
+@pytest.mark.parametrize("batch", [1, 8, 40, 200, 300])
+def test_lstm_batches(darb, batch):
+    # lanes per row from 1 to 64, and a batch past one column slab
+    say(f"lstm batch {batch}")
+    _lstm_case(darb, hidden=96, seq_len=5, batch=batch, layers=1, seed=batch)
 
 
 def test_lstm_full_workload(darb):
