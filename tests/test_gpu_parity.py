@@ -225,6 +225,30 @@ def test_product_edge_cases(darb, case):
     check_product(Y, vals, offs, lay, X, wdt, case + " spmm")
 
 
+@pytest.mark.parametrize("case", ["many_rows", "wide_rows", "wide_batch"])
+def test_large_shapes(darb, case):
+    # grids of 10^5+ workgroups, x past the LDS staging size with every block size,
+    # and a batch spanning several column slabs
+    say(f"large shape {case}")
+    rng = np.random.default_rng(len(case) + 40)
+    B = 5
+    if case == "many_rows":
+        M, N = 200_000, 48
+    elif case == "wide_rows":
+        M, N = 24, 100_003
+    else:
+        M, N, B = 300, 1500, 1000
+    W = rng.standard_normal((M, N)).astype(np.float32)
+    d = 1.0 / (1 << rng.integers(0, 8, size=M))
+    plan, lay, vals, offs = encode_both(darb, W, d, 0.1, 0, 1, 128)
+    x = rng.standard_normal(N).astype(np.float32)
+    check_product(host(plan.spmv(dev(vals), dev(offs), dev(x))), vals, offs, lay, x, np.float32,
+                  case + " spmv")
+    X = rng.standard_normal((N, B)).astype(np.float32)
+    check_product(host(plan.spmm(dev(vals), dev(offs), dev(X))), vals, offs, lay, X, np.float32,
+                  case + f" spmm B={B}")
+
+
 def test_spmv_misaligned_values_uses_scalar_path(darb):
     say("spmv with values/offsets starting at an odd element")
     rng = np.random.default_rng(12)
