@@ -34,7 +34,8 @@
  *   - A plan is host memory created by darb_plan_create and released by
  *     darb_plan_destroy.  One plan may be used from several threads for device
  *     calls once uploaded; create/upload/destroy are not thread-safe.
- *   - Sizes: 1 <= M, N < 2^31; block sizes are powers of two in [1, 128].
+ *   - Sizes: 1 <= M < 2^31, 1 <= N <= 2^31 - 256 (a plan's products form column
+ *     indices in 32 bits); block sizes are powers of two in [1, 128].
  */
 #ifndef DARB_H
 #define DARB_H

@@ -215,10 +215,12 @@ class Plan:
             raise ValueError("row_count must be 1-D")
         return cls(c.shape[0], N, None, 0.0, mode, b_min, b_max, _counts=(c, kept))
 
-    def __del__(self):
+    # bound at class creation: module globals may already be cleared when a plan is
+    # collected at interpreter exit
+    def __del__(self, _destroy=_lib.darb_plan_destroy):
         h = getattr(self, "_h", None)
         if h is not None and h.value:
-            _lib.darb_plan_destroy(h)
+            _destroy(h)
             self._h = None
 
     @property

@@ -20,6 +20,8 @@ void clear_error() { g_last_error.clear(); }
 
 static bool is_pow2(int64_t v) { return v > 0 && (v & (v - 1)) == 0; }
 
+static constexpr int64_t kMaxColumns = (int64_t(1) << 31) - 256;
+
 // workspace layout: perm (int32 [M]) padded to 256 bytes, then rowinfo (int64 [M])
 static int64_t perm_bytes(int64_t M) { return (M * int64_t(sizeof(int32_t)) + 255) / 256 * 256; }
 
@@ -77,7 +79,8 @@ int darb_plan_create_counts(int64_t M, int64_t N, const int64_t *row_count, int6
     if (!out) return fail(DARB_E_INVALID, "out is NULL");
     *out = nullptr;
     if (M < 1 || M >= (int64_t(1) << 31)) return fail(DARB_E_INVALID, "M must be in [1, 2^31)");
-    if (N < 1 || N >= (int64_t(1) << 31)) return fail(DARB_E_INVALID, "N must be in [1, 2^31)");
+    if (N < 1 || N > kMaxColumns)
+        return fail(DARB_E_INVALID, "N must be in [1, 2^31 - 256]");
     if (!row_count) return fail(DARB_E_INVALID, "row_count is NULL");
     if (kept < 0 || kept > M * N) return fail(DARB_E_INVALID, "kept must be in [0, M*N]");
     std::vector<double> d;
@@ -101,7 +104,9 @@ int darb_plan_create(int64_t M, int64_t N, const double *row_density, double mat
     if (!out) return fail(DARB_E_INVALID, "out is NULL");
     *out = nullptr;
     if (M < 1 || M >= (int64_t(1) << 31)) return fail(DARB_E_INVALID, "M must be in [1, 2^31)");
-    if (N < 1 || N >= (int64_t(1) << 31)) return fail(DARB_E_INVALID, "N must be in [1, 2^31)");
+    // the products form a column as (block << log2 b) + offset in 32 bits
+    if (N < 1 || N > kMaxColumns)
+        return fail(DARB_E_INVALID, "N must be in [1, 2^31 - 256]");
     if (!row_density) return fail(DARB_E_INVALID, "row_density is NULL");
     if (round_mode != DARB_ROUND_FLOOR && round_mode != DARB_ROUND_PAPER)
         return fail(DARB_E_INVALID, "unknown round_mode");

@@ -156,6 +156,7 @@ def test_plan_table7_and_worked_example():
 
 @pytest.mark.parametrize("kw,code", [
     (dict(M=0), darb.E_INVALID), (dict(N=0), darb.E_INVALID), (dict(M=-3), darb.E_INVALID),
+    (dict(N=(1 << 31) - 255), darb.E_INVALID), (dict(M=1 << 31), darb.E_INVALID),
     (dict(b_min=3), darb.E_INVALID), (dict(b_max=256), darb.E_INVALID),
     (dict(b_min=64, b_max=8), darb.E_INVALID), (dict(mode=5), darb.E_INVALID),
     (dict(D=float("nan")), darb.E_INVALID), (dict(D=1.5), darb.E_INVALID),
