@@ -129,3 +129,36 @@ def test_repeat_calls_reuse_workspace(darb):
         c = darb.prune_counts(Wd, k, workspace=ws)
         torch.cuda.synchronize()
         assert np.array_equal(c.cpu().numpy(), oracle.prune_counts(W, k)), k
+
+
+@pytest.mark.parametrize("name", ["lstm_tiny", "gru_1536"])
+def test_whole_pipeline_on_device(darb, name):
+    # W -> device pruning counts -> plan -> encode -> bit-packed offsets -> products,
+    # against the oracle's own chain (its pruning, plan, encode and packing)
+    cfg, mi, x, X = workloads.make_config(name, seed=0)
+    say(f"{name}: whole pipeline")
+    Wd = dev(mi.W)
+    counts = gpu_counts(darb, Wd, mi.k)
+    plan = darb.Plan.from_counts(cfg.N, counts, mi.k, darb.ROUND_FLOOR, cfg.b_min,
+                                 cfg.b_max).upload()
+    values, offsets = plan.encode(Wd)
+    packed = plan.pack_offsets(offsets)
+    y = plan.spmv_packed(values, packed, dev(x))
+    Y = plan.spmm_packed(values, packed, dev(X))
+    torch.cuda.synchronize()
+
+    ref_counts = oracle.prune_counts(mi.W, mi.k)
+    lay = oracle.plan(cfg.N, ref_counts / cfg.N, mi.k / (cfg.M * cfg.N), oracle.ROUND_FLOOR,
+                      cfg.b_min, cfg.b_max)
+    vr, orf = oracle.encode(mi.W, lay)
+    ut = np.uint32 if mi.W.dtype == np.float32 else np.uint16
+    assert np.array_equal(values.cpu().numpy().view(ut), vr.view(ut))
+    assert np.array_equal(offsets.cpu().numpy(), orf)
+    assert np.array_equal(packed.cpu().numpy()[:plan.packed_words].view(np.uint32),
+                          oracle.pack_offsets(orf, lay))
+    tol = 1e-5 if mi.W.dtype == np.float32 else 2e-3
+    for got, act in ((y.cpu().numpy(), x), (Y.cpu().numpy(), X)):
+        ref = oracle.spmm(vr, orf, lay, act)
+        scale = oracle.spmm_absdot(vr, orf, lay, act)
+        err = np.abs(np.asarray(got, dtype=np.float64).reshape(ref.shape) - ref)
+        assert (err <= tol * scale).all()
