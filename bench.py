@@ -187,6 +187,15 @@ def bench_lstm(args):
         res[name] = {"avg_us": round(us, 3), "batch": B,
                      "gflops": round(2 * pl.nnz * B / (us * 1e-6) / 1e9, 1)}
     flops = sum(2 * n * T * Bt for n in nnz)
+    # the dominant kernel by total time is the recurrent product (T launches per layer);
+    # its algorithmic bytes per launch: the format, h once, G once, the row order
+    rp = layers[0][1][0]
+    rec_bytes = rp.nnz * (2 + 1) + H * Bt * 4 + 4 * H * Bt * 4 + 4 * rp.M
+    rec_gbps = rec_bytes / (res["recurrent_product"]["avg_us"] * 1e-6) / 1e9
+    roofline = {"kernel": "recurrent_product", "bound": "hbm", "achieved": round(rec_gbps, 1),
+                "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(rec_gbps / HBM_PEAK_GBPS, 4),
+                "traffic": None,
+                "note": "latency-bound: 1.5 MB per launch, W_hh cache-resident"}
     out = {
         "metric": "DARB 2-layer LSTM forward tokens/s (hidden 1024, T=200, batch 32)",
         "value": round(T * Bt / (ms * 1e-3), 1), "unit": "tokens/s", "n_gpus": 1,
@@ -199,7 +208,7 @@ def bench_lstm(args):
                    "nnz_per_matrix": nnz},
         "gflops_step": round(flops / (ms * 1e-3) / 1e9, 1),
         "kernels": res,
-        "roofline": None,
+        "roofline": roofline,
         "cpu_baseline": None,
     }
     if args.cpu_seconds > 0:
