@@ -463,11 +463,31 @@ static int lstm_check(const darb_plan *wih, const void *wih_values, const uint8_
     return DARB_OK;
 }
 
-// The per-step loop: recurrent product, then the gate cell, T times.
+// The time steps.  When every gate row of the recurrent matrix fits the fused
+// step kernel, one launch per step computes the product and the cell of every
+// hidden unit, reading h from one buffer and writing the other (h and, as the
+// second buffer, the first H x batch floats of G); otherwise two launches per
+// step: the recurrent product into G, then the cell.
 static int lstm_steps(const darb_plan *whh, const void *whh_values, const uint8_t *whh_offsets,
                       int wdtype, int64_t H, int64_t T, int64_t batch, const float *U, float *G,
                       float *h_seq, float *h, float *c, hipStream_t s) {
     const int64_t TB = T * batch;
+    if (lstm_step_fusable(*whh, batch, h, G)) {
+        float *hb[2] = {h, G};
+        for (int64_t t = 0; t < T; ++t) {
+            int rc = launched(launch_lstm_step(*whh, wdtype, whh_values, whh_offsets, H, batch,
+                                               hb[t & 1], U + t * batch, TB, c, hb[(t + 1) & 1],
+                                               h_seq + t * batch, TB, s), "lstm step");
+            if (rc) return rc;
+        }
+        if (T & 1) {            // the final state ended in the second buffer
+            hipError_t e = hipMemcpyAsync(h, G, size_t(H * batch) * sizeof(float),
+                                          hipMemcpyDeviceToDevice, s);
+            if (e != hipSuccess)
+                return fail(DARB_E_HIP, std::string("lstm state copy: ") + hipGetErrorString(e));
+        }
+        return DARB_OK;
+    }
     for (int64_t t = 0; t < T; ++t) {
         int rc = launched(launch_spmm(*whh, wdtype, whh_values, whh_offsets, nullptr, DARB_F32,
                                       batch, h, batch, G, batch, s), "lstm recurrent product");

@@ -82,6 +82,13 @@ hipError_t launch_unpack_offsets(const darb_plan &p, const uint32_t *packed, uin
 int64_t prune_workspace_bytes(int64_t M, int64_t N, int wdtype);
 hipError_t launch_prune_counts(int64_t M, int64_t N, int wdtype, const void *W, int64_t ldw,
                                int64_t k, int64_t *counts, void *workspace, hipStream_t s);
+// One fused LSTM step (recurrent product and gate cell of every hidden unit), when
+// lstm_step_fusable: h_in is read, h_out written (distinct buffers).
+bool lstm_step_fusable(const darb_plan &whh, int64_t batch, const float *h, const float *h2);
+hipError_t launch_lstm_step(const darb_plan &whh, int wdtype, const void *values,
+                            const uint8_t *offsets, int64_t H, int64_t batch, const float *h_in,
+                            const float *U, int64_t ldu, float *c, float *h_out, float *h_seq,
+                            int64_t ld_seq, hipStream_t s);
 hipError_t launch_lstm_cell(int64_t H, int64_t batch, const float *G, const float *U,
                             int64_t ldu, float *h, float *c, float *h_seq, int64_t ld_seq,
                             hipStream_t s);

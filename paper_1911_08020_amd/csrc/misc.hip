@@ -1,6 +1,7 @@
 // Decode to the masked dense matrix, the LSTM cell of the recurrent workload,
 // and the HBM stream kernels the DARB kernels are measured against.
 #include "darb_internal.h"
+#include "lstm_cell.h"
 
 namespace darb {
 namespace {
@@ -22,16 +23,6 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(
     const int64_t e = bins.first_elem[g] + (i - bins.first_row[g]) * bins.nblk[g] + (c >> lb);
     const int64_t j = c & ((int64_t(1) << lb) - 1);
     W[int64_t(perm[i]) * ldw + c] = (offsets[e] == j) ? values[e] : Bits(0);
-}
-
-__device__ __forceinline__ float lstm_sigmoid(float z) { return 1.0f / (1.0f + __expf(-z)); }
-
-// The LSTM cell of the recurrent models (section 4.1): no bias, gate order
-// (i, f, g, o); c' = sigmoid(f) c + sigmoid(i) tanh(g), h' = sigmoid(o) tanh(c').
-__device__ __forceinline__ float lstm_cell(float gi, float gf, float gg, float go, float &c) {
-    const float cn = lstm_sigmoid(gf) * c + lstm_sigmoid(gi) * tanhf(gg);
-    c = cn;
-    return lstm_sigmoid(go) * tanhf(cn);
 }
 
 // gates = G + U (G: recurrent product [4H x batch], U: input product slice of
