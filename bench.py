@@ -187,15 +187,31 @@ def bench_lstm(args):
         res[name] = {"avg_us": round(us, 3), "batch": B,
                      "gflops": round(2 * pl.nnz * B / (us * 1e-6) / 1e9, 1)}
     flops = sum(2 * n * T * Bt for n in nnz)
-    # the dominant kernel by total time is the recurrent product (T launches per layer);
-    # its algorithmic bytes per launch: the format, h once, G once, the row order
-    rp = layers[0][1][0]
-    rec_bytes = rp.nnz * (2 + 1) + H * Bt * 4 + 4 * H * Bt * 4 + 4 * rp.M
-    rec_gbps = rec_bytes / (res["recurrent_product"]["avg_us"] * 1e-6) / 1e9
-    roofline = {"kernel": "recurrent_product", "bound": "hbm", "achieved": round(rec_gbps, 1),
-                "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(rec_gbps / HBM_PEAK_GBPS, 4),
+    # the dominant kernel by total time is the time step (T launches per layer): its
+    # average from the layer's time minus its input product, between events
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    wih, whh = layers[0]
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for _ in range(3):
+        hh[0].zero_()
+        cc[0].zero_()
+        darb.lstm_layer(wih, whh, x_seq, H, T, Bt, h=hh[0], c=cc[0], h_seq=hs[0], workspace=ws)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    layer_us = e0.elapsed_time(e1) * 1e3 / 3
+    step_us = (layer_us - res["input_product"]["avg_us"]) / T
+    rp = whh[0]
+    # per step: the recurrent format, h_{t-1} once, the step's input products, c read
+    # and written, h_t written twice (state and sequence), the per-row table of 4H rows
+    step_bytes = rp.nnz * (2 + 1) + H * Bt * 4 + 4 * H * Bt * 4 + 2 * H * Bt * 4 + \
+        2 * H * Bt * 4 + 8 * rp.M
+    res["step"] = {"avg_us": round(step_us, 3), "derived_from_layer_us": round(layer_us, 1)}
+    step_gbps = step_bytes / (step_us * 1e-6) / 1e9
+    roofline = {"kernel": "lstm_step", "bound": "hbm", "achieved": round(step_gbps, 1),
+                "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(step_gbps / HBM_PEAK_GBPS, 4),
                 "traffic": None,
-                "note": "latency-bound: 1.5 MB per launch, W_hh cache-resident"}
+                "note": "latency-bound: about 2 MB per launch, W_hh cache-resident"}
     out = {
         "metric": "DARB 2-layer LSTM forward tokens/s (hidden 1024, T=200, batch 32)",
         "value": round(T * Bt / (ms * 1e-3), 1), "unit": "tokens/s", "n_gpus": 1,
