@@ -430,8 +430,9 @@ __device__ __forceinline__ void spmm_tile(
     constexpr int GM = L >= 16 ? 1 : 16 / L;              // pair groups per lane per step
     constexpr int S = L * GM;                             // weights per row per step
     // steps whose pairs load together: four for rows of 16 or fewer lanes (measured
-    // 11 % faster at 16 lanes, batch 64); a 64-lane row's step already spans 64 weights
-    constexpr int DEPTH = (L >= kWave || GM >= 4) ? 1 : 4 / GM;
+    // 11 % faster at 16 lanes, batch 64), two when the offsets are packed (their word
+    // windows take more registers); a 64-lane row's step already spans 64 weights
+    constexpr int DEPTH = (L >= kWave || GM >= 4) ? 1 : (PK ? 2 : 4) / GM;
 
     const int g = block_group(sch, tile);
     const int wave = wave_uniform(int(threadIdx.x) / kWave);
