@@ -28,6 +28,7 @@
 // share every other step, so their results are bitwise identical.
 #include <hip/hip_fp16.h>
 
+#include <type_traits>
 #include <utility>
 
 #include "darb_internal.h"
@@ -220,6 +221,22 @@ __device__ __forceinline__ void stage_x(float *xs, const Tx *__restrict__ x, int
     for (int c = nv * E + int(threadIdx.x); c < N; c += kSpmvThreads) xs[c] = to_f32<Tx>(x[c]);
 }
 
+// fp32 x straight into LDS: each wave moves 1 KiB chunks with direct global-to-LDS
+// loads (lane i's 16 bytes land at chunk + 16 i), so no registers hold x on the way;
+// the rest (a partial chunk, a tail shorter than 16 bytes) goes through registers.
+// The caller waits for the loads and synchronises the workgroup.
+__device__ __forceinline__ void stage_x_direct(float *xs, const float *__restrict__ x, int N) {
+    typedef __attribute__((address_space(1))) const float *gptr;
+    typedef __attribute__((address_space(3))) void *lptr;
+    const int wave = wave_uniform(int(threadIdx.x) / kWave);
+    const int lane = int(threadIdx.x) & (kWave - 1);
+    const int chunks = N / (kWave * 4);
+    for (int j = wave; j < chunks; j += kSpmvWaves)
+        __builtin_amdgcn_global_load_lds((gptr)(x + (j * kWave + lane) * 4),
+                                         (lptr)(xs + j * kWave * 4), 16, 0, 0);
+    for (int c = chunks * kWave * 4 + int(threadIdx.x); c < N; c += kSpmvThreads) xs[c] = x[c];
+}
+
 template <typename Tw, typename Tx, bool LDS, int SB, bool PK>
 __global__ __launch_bounds__(kSpmvThreads) void spmv_kernel(
     const Tw *__restrict__ values, const void *__restrict__ offs,
@@ -272,7 +289,12 @@ __global__ __launch_bounds__(kSpmvThreads) void spmv_kernel(
     }
 
     if constexpr (LDS) {
-        stage_x<Tx, SB>(xs, x, N);
+        if constexpr (SB == 0 && std::is_same<Tx, float>::value) {   // fp32 x, 16 B aligned
+            stage_x_direct(xs, x, N);
+            __builtin_amdgcn_s_waitcnt(0);                // the direct loads have landed
+        } else {
+            stage_x<Tx, SB>(xs, x, N);
+        }
         __syncthreads();
     }
     auto xat = [&](int c) -> float {
@@ -761,7 +783,13 @@ hipError_t launch_spmv_t(const darb_plan &p, const void *values, const uint8_t *
 #define DARB_SPMV_LDS(SB)                                                                    \
     hipLaunchKernelGGL((spmv_kernel<Tw, Tx, true, SB, PK>), dim3(blocks), dim3(kSpmvThreads), \
                        lds, st, v, offs, xx, y, p.d_perm, N, p.bins, s)
-        if (per_thread <= 1) DARB_SPMV_LDS(1);
+        bool direct = false;
+        if constexpr (std::is_same<Tx, float>::value) {
+            direct = reinterpret_cast<uintptr_t>(x) % 16 == 0;
+            if (direct) DARB_SPMV_LDS(0);
+        }
+        if (direct) {
+        } else if (per_thread <= 1) DARB_SPMV_LDS(1);
         else if (per_thread <= 2) DARB_SPMV_LDS(2);
         else if (per_thread <= 4) DARB_SPMV_LDS(4);
         else if (per_thread <= 8) DARB_SPMV_LDS(8);
