@@ -579,6 +579,143 @@ __global__ __launch_bounds__(kSpmmThreads) void spmm_kernel(
 }
 
 // ---------------------------------------------------------------------------------
+// SpMM for short rows of X and many batch columns (the recurrent workload's input
+// products: N = 1024, B = 6400).  A workgroup takes one slab of SC = 4L batch
+// columns, copies X[:, slab] (N x SC fp32, <= 128 KiB) into LDS once, then runs
+// every row of every group against it -- the X-row gathers hit LDS instead of L2.
+// The format is read by every workgroup, from L2.  One lane group of L lanes per
+// row, S weights per step, DEPTH steps of pairs per load round.
+// ---------------------------------------------------------------------------------
+
+constexpr int kXldsThreads = 1024;
+constexpr int kXldsWaves = kXldsThreads / kWave;
+constexpr int kXldsFloats = 32768;                  // 128 KiB of LDS
+constexpr int kXldsStep = 16;                       // weights per row per step
+constexpr int kXldsBatch = 16;                      // LDS gathers in flight per lane
+
+// 16 consecutive retained values of one row, loaded as 16-byte vectors.
+template <typename Tw> struct Step16;
+template <> struct Step16<float> {
+    f32x4 v[4];
+    __device__ static Step16 load(const float *p) {
+        Step16 s;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) s.v[i] = reinterpret_cast<const f32x4 *>(p)[i];
+        return s;
+    }
+    __device__ float get(int i) const { return v[i >> 2][i & 3]; }
+};
+template <> struct Step16<__half> {
+    u32x4 v[2];
+    __device__ static Step16 load(const __half *p) {
+        Step16 s;
+#pragma unroll
+        for (int i = 0; i < 2; ++i) s.v[i] = reinterpret_cast<const u32x4 *>(p)[i];
+        return s;
+    }
+    __device__ float get(int i) const {
+        const uint32_t w = v[i >> 3][(i >> 1) & 3];
+        return half_bits_to_f32((i & 1) ? (w >> 16) : w);
+    }
+};
+
+template <typename Tw, int LGL>
+__global__ __launch_bounds__(kXldsThreads) void spmm_xlds_kernel(
+    const Tw *__restrict__ values, const uint8_t *__restrict__ offsets,
+    const float *__restrict__ X, int64_t ldx, int64_t B, float *__restrict__ Y, int64_t ldy,
+    const int32_t *__restrict__ perm, int N, BinTable bins, ProductSchedule sch) {
+    constexpr int L = 1 << LGL;
+    constexpr int R = kWave >> LGL;
+    constexpr int SC = 4 * L;                           // slab columns
+    constexpr int kStage = 8;                           // 16-byte staging loads in flight
+    __shared__ float xs[kXldsFloats];
+    using XL = XLoad<float, 4>;
+
+    const int64_t colbase = int64_t(blockIdx.x) * SC;
+    // X[:, slab] -> xs[c * SC + j]; columns past B read as zero (4 divides B)
+    {
+        constexpr int per_row = SC / 4;
+        const int items = N * per_row;
+        for (int base = 0; base < items; base += kStage * kXldsThreads) {
+            f32x4 v[kStage];
+            bool in[kStage];
+#pragma unroll
+            for (int u = 0; u < kStage; ++u) {
+                const int i = base + u * kXldsThreads + int(threadIdx.x);
+                const int ic = i < items ? i : items - 1;
+                const int c = ic / per_row, q = ic - c * per_row;
+                const int64_t col = colbase + int64_t(q) * 4;
+                in[u] = i < items && col < B;
+                v[u] = XL::load(X + int64_t(c) * ldx + (col < B ? col : 0));
+            }
+#pragma unroll
+            for (int u = 0; u < kStage; ++u) {
+                const int i = base + u * kXldsThreads + int(threadIdx.x);
+                if (i < items) {
+                    const f32x4 z = {0.0f, 0.0f, 0.0f, 0.0f};
+                    *reinterpret_cast<f32x4 *>(xs + i * 4) = in[u] ? v[u] : z;
+                }
+            }
+        }
+    }
+    __syncthreads();
+
+    const int wave = wave_uniform(int(threadIdx.x) / kWave);
+    const int lane = int(threadIdx.x) & (kWave - 1);
+    const int sub = lane & (L - 1);
+    const int64_t col0 = colbase + int64_t(sub) * 4;
+    const bool col_ok = col0 < B;
+    const int xoff = sub * 4;
+    for (int g = 0; g < sch.nbins; ++g) {                // uniform
+        const int lb = pick(bins.log2b, g);
+        const int nblk = int(pick(bins.nblk, g));        // a multiple of kXldsStep
+        const int64_t rows = pick(bins.rows, g);
+        const int64_t first_row = pick(bins.first_row, g);
+        const int64_t first_elem = pick(bins.first_elem, g);
+        for (int64_t p0 = 0; p0 < rows; p0 += int64_t(kXldsWaves) * R) {
+            const int64_t rl = p0 + wave * R + (lane >> LGL);
+            const bool row_ok = rl < rows;
+            const int64_t e0 = first_elem + (row_ok ? rl : 0) * nblk;   // 16-aligned
+            float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+            // every lane of the row loads the step's 16 (value, offset) pairs itself
+            // (equal addresses within one load merge), so no lane exchange is needed;
+            // the next step's pairs load while this step gathers
+            Step16<Tw> w = Step16<Tw>::load(values + e0);
+            u32x4 ob = *reinterpret_cast<const u32x4 *>(offsets + e0);
+            for (int k0 = 0; k0 < nblk; k0 += kXldsStep) {
+                const int kn = k0 + kXldsStep < nblk ? k0 + kXldsStep : k0;
+                const Step16<Tw> w_next = Step16<Tw>::load(values + e0 + kn);
+                const u32x4 ob_next = *reinterpret_cast<const u32x4 *>(offsets + e0 + kn);
+                static_for<0, kXldsStep / kXldsBatch>([&](auto bc) {
+                    constexpr int b0 = decltype(bc)::value * kXldsBatch;
+                    f32x4 xv[kXldsBatch];
+                    static_for<0, kXldsBatch>([&](auto uc) {
+                        constexpr int f = b0 + decltype(uc)::value;
+                        const int o = int((ob[f >> 2] >> (8 * (f & 3))) & 0xFFu);
+                        int c = ((k0 + f) << lb) + o;
+                        c = c < N ? c : N - 1;                // the encode gives c < N
+                        xv[f - b0] = *reinterpret_cast<const f32x4 *>(xs + c * SC + xoff);
+                    });
+#pragma unroll
+                    for (int u = 0; u < kXldsBatch; ++u) {
+                        const float vw = w.get(b0 + u);
+#pragma unroll
+                        for (int q = 0; q < 4; ++q) acc[q] = fmaf(vw, xv[u][q], acc[q]);
+                    }
+                });
+                w = w_next;
+                ob = ob_next;
+            }
+            if (row_ok && col_ok) {
+                float *yrow = Y + int64_t(perm[first_row + rl]) * ldy + col0;
+#pragma unroll
+                for (int q = 0; q < 4; ++q) yrow[q] = acc[q];
+            }
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------------
 // One LSTM time step in one kernel (the recurrent models of section 4.1).  A
 // workgroup owns one hidden unit u: its four gate rows u, H+u, 2H+u, 3H+u (in
 // different block-size groups, found through the per-row table) are cut into
@@ -865,6 +1002,17 @@ hipError_t launch_spmm_cpl(const darb_plan &p, const ProductSchedule &s, const T
     return hipGetLastError();
 }
 
+// Lanes per row of the LDS-slab SpMM (slab = 4 * lanes columns), or -1 when it does
+// not apply: fp32 X with 16-byte rows, a slab of >= 32 columns whose N rows fit in
+// LDS, and enough slabs (>= 128) to give every CU a workgroup.
+int xlds_lgl(const darb_plan &p, int64_t B) {
+    for (int lgl = 4; lgl >= 3; --lgl) {
+        const int64_t sc = int64_t(4) << lgl;
+        if (p.N * sc <= kXldsFloats && (B + sc - 1) / sc >= 128) return lgl;
+    }
+    return -1;
+}
+
 template <typename Tw, typename Tx, bool PK>
 hipError_t launch_spmm_t(const darb_plan &p, const void *values, const uint8_t *offsets,
                          const uint32_t *packed, int64_t B, const void *X, int64_t ldx, float *Y,
@@ -872,6 +1020,34 @@ hipError_t launch_spmm_t(const darb_plan &p, const void *values, const uint8_t *
     constexpr int CPL = 16 / int(sizeof(Tx));
     const bool vec = (reinterpret_cast<uintptr_t>(X) % 16 == 0) &&
                      ((ldx * int64_t(sizeof(Tx))) % 16 == 0) && (B % CPL == 0);
+    if constexpr (std::is_same<Tx, float>::value && !PK) {
+        int lgl = vec ? xlds_lgl(p, B) : -1;
+        // every row's steps of 16 pairs load as 16-byte vectors
+        bool aligned16 = reinterpret_cast<uintptr_t>(values) % (kXldsStep * sizeof(Tw)) == 0 &&
+                         offsets_aligned(offsets, kXldsStep);
+        for (int g = 0; g < p.bins.nbins; ++g)
+            aligned16 = aligned16 && p.bins.nblk[g] % kXldsStep == 0 &&
+                        p.bins.first_elem[g] % kXldsStep == 0;
+        if (!aligned16) lgl = -1;
+        if (lgl >= 0) {
+            ProductSchedule s;
+            if (!spmm_schedule(p, B, CPL, sizeof(Tw), values, offsets, s))
+                return hipErrorInvalidConfiguration;
+            const int64_t slabs = (B + (int64_t(4) << lgl) - 1) / (int64_t(4) << lgl);
+            if (slabs > 0x7FFFFFFF) return hipErrorInvalidConfiguration;
+            const Tw *v = static_cast<const Tw *>(values);
+            const float *x = static_cast<const float *>(X);
+            if (lgl == 4)
+                hipLaunchKernelGGL((spmm_xlds_kernel<Tw, 4>), dim3(unsigned(slabs)),
+                                   dim3(kXldsThreads), 0, st, v, offsets, x, ldx, B, Y, ldy,
+                                   p.d_perm, int(p.N), p.bins, s);
+            else
+                hipLaunchKernelGGL((spmm_xlds_kernel<Tw, 3>), dim3(unsigned(slabs)),
+                                   dim3(kXldsThreads), 0, st, v, offsets, x, ldx, B, Y, ldy,
+                                   p.d_perm, int(p.N), p.bins, s);
+            return hipGetLastError();
+        }
+    }
     ProductSchedule s;
     if (!spmm_schedule(p, B, vec ? CPL : 1, sizeof(Tw), values, offsets, s))
         return hipErrorInvalidConfiguration;

@@ -249,6 +249,25 @@ def test_large_shapes(darb, case):
                   case + f" spmm B={B}")
 
 
+@pytest.mark.parametrize("case", [(1024, 4100, "f32", 64), (512, 8200, "f32", 32),
+                                  (1024, 4096, "f16", 64), (700, 4100, "f32", 128)])
+def test_spmm_wide_batch_short_rows(darb, case):
+    # N small enough that a slab of X (32 or 64 columns) fits in LDS, B wide enough
+    # for >= 128 slabs and rows in whole steps of 16 weights: the product stages X
+    # slabs in LDS (the last case has rows of ragged length and takes the general path)
+    N, B, wdt, bmax = case
+    wdt = np.float32 if wdt == "f32" else np.float16
+    say(f"wide-batch spmm N={N} B={B} w={wdt.__name__} b<={bmax}")
+    rng = np.random.default_rng(N + B)
+    M = 300
+    W = rng.standard_normal((M, N)).astype(wdt)
+    d = rng.integers(0, N // 3, size=M) / N
+    plan, lay, vals, offs = encode_both(darb, W, d, 0.1, 0, 1, bmax)
+    X = rng.standard_normal((N, B)).astype(np.float32)
+    Y = host(plan.spmm(dev(vals), dev(offs), dev(X)))
+    check_product(Y, vals, offs, lay, X, wdt, f"wide B={B}")
+
+
 def test_spmv_misaligned_values_uses_scalar_path(darb):
     say("spmv with values/offsets starting at an odd element")
     rng = np.random.default_rng(12)
