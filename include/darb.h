@@ -247,7 +247,12 @@ int darb_prune_counts(int64_t M, int64_t N, int wdtype, const void *W, int64_t l
  *   c_t = sigmoid(f) * c_{t-1} + sigmoid(i) * tanh(g),  h_t = sigmoid(o) * tanh(c_t).
  * W_ih is [4H x I] and W_hh is [4H x H], both of wdtype, each with its own
  * uploaded plan.  The input products of all steps are computed first as one
- * darb_spmm with B = T * batch.
+ * darb_spmm with B = T * batch.  Each time step is then one launch: a workgroup per
+ * hidden unit computes the unit's four gate rows of W_hh h_{t-1} and the cell
+ * (batch <= 64 and W_hh rows of at most 512 retained weights); other shapes run
+ * the recurrent product and the cell as two launches.  Both give the same result
+ * within the product tolerance; the call is deterministic.  The workspace also
+ * holds the second buffer of h that the steps alternate with `h`.
  *   x_seq      device fp32 [I x T*batch], column t*batch + n
  *   h_seq      device fp32 [H x T*batch], receives h_t in columns t*batch + n
  *   h, c       device fp32 [H x batch], initial state in, final state out
