@@ -249,7 +249,8 @@ int darb_prune_counts(int64_t M, int64_t N, int wdtype, const void *W, int64_t l
  * uploaded plan.  The input products of all steps are computed first as one
  * darb_spmm with B = T * batch.  Each time step is then one launch: a workgroup per
  * hidden unit computes the unit's four gate rows of W_hh h_{t-1} and the cell
- * (batch <= 64 and W_hh rows of at most 512 retained weights); other shapes run
+ * (batch <= 64 and a multiple of 4, or batch <= 16; W_hh rows of at most 512
+ * retained weights); other shapes run
  * the recurrent product and the cell as two launches.  Both give the same result
  * within the product tolerance; the call is deterministic.  The workspace also
  * holds the second buffer of h that the steps alternate with `h`.
