@@ -57,34 +57,55 @@ def step_bytes(M, N, nnz, s_w, s_x, B):
     return {"encode": enc, "spmv": spmv, "spmm": spmm}
 
 
-def csrc_sha256():
-    """Hash of the library sources, to tell whether stored counters still apply."""
-    import glob
+# source file of each measured kernel; its local includes (the public header among them),
+# the C-ABI layer that lays out the plan and the build script (flags) are hashed with it
+KERNEL_SOURCES = {"encode": "encode.hip", "pack": "packed.hip", "spmv": "product.hip",
+                  "spmm": "product.hip", "spmv_packed": "product.hip",
+                  "spmm_packed": "product.hip", "prune": "prune.hip"}
+
+
+def kernel_sha256(kernel):
+    """Hash of the sources a kernel is built from, to tell whether stored counters of
+    that kernel still apply; None for a kernel with no known source."""
     import hashlib
+    import re
+    src = KERNEL_SOURCES.get(kernel)
+    if src is None:
+        return None
+    pkg = os.path.join(ROOT, "paper_1911_08020_amd")
+    dirs = (os.path.join(pkg, "csrc"), os.path.join(ROOT, "include"), pkg)
+    todo, seen = [src, "api.cpp", "build.py"], {}
+    while todo:
+        name = todo.pop(0)
+        if name in seen:
+            continue
+        path = next(os.path.join(d, name) for d in dirs if os.path.exists(os.path.join(d, name)))
+        with open(path, "rb") as f:
+            seen[name] = f.read()
+        todo += [m.decode() for m in re.findall(rb'#include\s+"([^"]+)"', seen[name])]
     h = hashlib.sha256()
-    for p in sorted(glob.glob(os.path.join(ROOT, "paper_1911_08020_amd", "csrc", "*"))):
-        h.update(os.path.basename(p).encode())
-        with open(p, "rb") as f:
-            h.update(f.read())
+    for name in sorted(seen):
+        h.update(name.encode())
+        h.update(seen[name])
     return h.hexdigest()
 
 
 def stored_traffic(workload, batch):
-    """HBM bytes per launch from the committed rocprofv3 --pmc summary, or {} when the
-    summary is missing, was taken on another workload, or the kernels changed since."""
+    """HBM bytes per launch from the committed rocprofv3 --pmc summary, for each kernel
+    whose sources are unchanged since the counters were taken; {} when the summary is
+    missing or was taken on another workload."""
     path = os.path.join(ROOT, "profiles", f"traffic_{workload}.txt")
     if batch != 64 or not os.path.exists(path):
         return {}
-    out, sha = {}, None
+    out = {}
     with open(path) as f:
         for ln in f:
             ln = ln.strip()
-            if ln.startswith("csrc_sha256="):
-                sha = ln.split("=", 1)[1]
-            elif ln.startswith("kernel="):
+            if ln.startswith("kernel="):
                 kv = dict(t.split("=", 1) for t in ln.split())
-                out[kv["kernel"]] = int(kv["traffic_bytes"])
-    return out if sha == csrc_sha256() else {}
+                if kv.get("sources_sha256") == kernel_sha256(kv["kernel"]):
+                    out[kv["kernel"]] = int(kv["traffic_bytes"])
+    return out
 
 
 def cpu_baseline(cfg, mi, x, X, seconds, bytes_per_step):
