@@ -17,11 +17,13 @@
 // xor butterfly in a fixed order (deterministic) and written in original row order.
 //
 // SpMM: lanes map to batch columns (X is [N x B] row-major, so one weight's
-// activations X[c, :] are contiguous), CPL columns per lane with 16-byte loads.
-// Each wave loads its rows' (value, column) pairs with coalesced loads and
-// broadcasts them across a row's lanes register to register (DPP, swizzle or
-// readlane), gathering X rows kSpmmBatch at a time; up to 8 waves split a row
-// group's weights and their partial sums meet in LDS in a fixed order.
+// activations X[c, :] are contiguous), CPL columns per lane with 16-byte loads
+// (one column per lane for batches up to 16, so small batches still spread over
+// many waves).  Each wave loads its rows' (value, column) pairs with coalesced
+// loads and broadcasts them across a row's lanes register to register (DPP,
+// swizzle or readlane), gathering X rows kSpmmBatch at a time; the next round's
+// pairs load while this round gathers.  Up to 8 waves split a row group's weights
+// and their partial sums meet in LDS in a fixed order.
 //
 // Both products read the offsets either as one byte per retained weight or in the
 // bit-packed form of section 4.2 (log2 b bits each, packed_bits.h); the two forms
@@ -349,6 +351,7 @@ __global__ __launch_bounds__(kSpmvThreads) void spmv_kernel(
 constexpr int kSpmmThreads = 512;
 constexpr int kSpmmWaves = kSpmmThreads / kWave;
 constexpr int kSpmmBatch = 8;         // X rows in flight per lane (more waves beat deeper batches)
+constexpr int kNarrowBatch = 16;      // batches up to this take one column per lane
 
 // CPL consecutive batch columns of one X row, loaded at once (16 bytes when CPL > 1).
 template <typename Tx, int CPL> struct XLoad;
@@ -404,20 +407,28 @@ template <int LGL, int T> __device__ __forceinline__ int group_bcast(int v) {
 // vector load each when the bin is aligned for it, element loads otherwise.
 template <typename Tw, int GM, bool PK> struct PairLoad {
     struct alignas(GM * sizeof(Tw)) VV { Tw e[GM]; };
+    using OV = Off<PK, GM>;
+    // the vector form as loaded, kept in registers while other loads are in flight
+    struct Raw { VV a; typename OV::Raw ob; };
     // vec: the caller guarantees k % GM == 0, k + GM <= nblk and nblk % GM == 0 (so
     // the group slot j0 + k is a multiple of GM); otherwise every element index is
     // clamped into the row [0, nblk).  j0 is the row's first slot in its group.
+    __device__ static Raw issue(const Tw *vr, const GroupOffsets &go, int64_t j0, int k) {
+        return Raw{*reinterpret_cast<const VV *>(vr + k), OV::load(go, j0 + k)};
+    }
+    __device__ static void decode(const Raw &r, const GroupOffsets &go, float (&v)[GM],
+                                  int (&o)[GM]) {
+        const typename OV::Bits b = OV::bits(r.ob, go);
+#pragma unroll
+        for (int i = 0; i < GM; ++i) {
+            v[i] = to_f32<Tw>(r.a.e[i]);
+            o[i] = OV::field(b, i, go);
+        }
+    }
     __device__ static void load(const Tw *vr, const GroupOffsets &go, int64_t j0, int k,
                                 int nblk, bool vec, float (&v)[GM], int (&o)[GM]) {
         if (vec) {
-            using OV = Off<PK, GM>;
-            const VV a = *reinterpret_cast<const VV *>(vr + k);
-            const typename OV::Bits b = OV::bits(OV::load(go, j0 + k), go);
-#pragma unroll
-            for (int i = 0; i < GM; ++i) {
-                v[i] = to_f32<Tw>(a.e[i]);
-                o[i] = OV::field(b, i, go);
-            }
+            decode(issue(vr, go, j0, k), go, v, o);
         } else {
             using OS = Off<PK, 1>;
 #pragma unroll
@@ -431,12 +442,14 @@ template <typename Tw, int GM, bool PK> struct PairLoad {
 };
 
 // One workgroup-sized tile of the SpMM: lanes map to batch columns (CPL per lane,
-// 2^LGL lanes per matrix row, 64 >> LGL rows per wave).  A wave owns a contiguous share [kbeg, kend) of its rows' weights
-// (KS waves split a row group).  The lanes of a row load S = max(2^LGL, 16) of the
-// row's (value, column) pairs per step, one pair per lane and group, straight from
-// HBM with coalesced loads, then broadcast each pair to the row's lanes with a
-// register-to-register exchange and gather its X row; kSpmmBatch gathers are in
-// flight per lane.  Partial sums of the KS waves meet in LDS (`part`, kSpmmThreads *
+// 2^LGL lanes per matrix row, 64 >> LGL rows per wave).  A wave owns a contiguous
+// share [kbeg, kend) of its rows' weights (KS waves split a row group).  The lanes
+// of a row load S = max(2^LGL, 16) of the row's (value, column) pairs per step, one
+// pair per lane and group, straight from HBM with coalesced loads, then broadcast
+// each pair to the row's lanes with a register-to-register exchange and gather its
+// X row; kSpmmBatch gathers are in flight per lane.  With aligned pairs the loads
+// are software pipelined: a round's pairs are issued right after the previous
+// round's last gathers, so their HBM latency overlaps those gathers.  Partial sums of the KS waves meet in LDS (`part`, kSpmmThreads *
 // CPL floats) in a fixed order.  The finished rows go to
 //     epi(row_ok, col_ok, original row, first column, acc[CPL], lane in row),
 // called by every lane of the waves that hold finished rows (wave-uniform), so an
@@ -455,6 +468,9 @@ __device__ __forceinline__ void spmm_tile(
     // 11 % faster at 16 lanes, batch 64), two when the offsets are packed (their word
     // windows take more registers); a 64-lane row's step already spans 64 weights
     constexpr int DEPTH = (L >= kWave || GM >= 4) ? 1 : (PK ? 2 : 4) / GM;
+    constexpr int T = DEPTH * S;                          // weights per row per round
+    constexpr int NB = kSpmmBatch;                        // X-row gathers in flight per lane
+    static_assert(S % NB == 0, "a gather batch lies inside one step");
 
     const int g = block_group(sch, tile);
     const int wave = wave_uniform(int(threadIdx.x) / kWave);
@@ -497,52 +513,94 @@ __device__ __forceinline__ void spmm_tile(
     for (int q = 0; q < CPL; ++q) acc[q] = 0.0f;
 
     const bool vec_pairs = pick(sch.vec, g) != 0;
-    // the pairs of DEPTH steps are loaded together (one HBM round trip), then gathered
-    for (int k0 = kbeg; k0 < kend; k0 += DEPTH * S) {
-        // step st's pairs: lane `sub` of the row holds weights k0 + st*S + sub*GM + gi
-        float vl[DEPTH][GM];
-        int cl[DEPTH][GM];
+    using PL = PairLoad<Tw, GM, PK>;
+    // a round's pairs (DEPTH steps) as values and clamped columns; -1 marks no weight
+    auto settle = [&](int k0, int st, const float (&v)[GM], const int (&o)[GM],
+                      float (&vl)[DEPTH][GM], int (&cl)[DEPTH][GM]) {
+        const int k = k0 + st * S + sub * GM;
+        const bool ok = row_ok && k < kend;
+#pragma unroll
+        for (int gi = 0; gi < GM; ++gi) {
+            const bool okg = ok && k + gi < kend;         // element test for the scalar path
+            vl[st][gi] = okg ? v[gi] : 0.0f;
+            const int c = ((k + gi) << lb) + o[gi];
+            cl[st][gi] = okg ? (c < N ? c : N - 1) : -1;   // the encode gives c < N
+        }
+    };
+    // vector pair loads of the round at k0 (lanes past the share or the rows load a
+    // valid slot of their row block and are masked when settled)
+    auto issue_round = [&](int k0, typename PL::Raw (&raw)[DEPTH]) {
 #pragma unroll
         for (int st = 0; st < DEPTH; ++st) {
             const int k = k0 + st * S + sub * GM;
-            const bool ok = row_ok && k < kend;
-            float v[GM];
-            int o[GM];
-            PairLoad<Tw, GM, PK>::load(vr, go, j0, ok ? k : kbeg, nblk, vec_pairs, v, o);
-#pragma unroll
-            for (int gi = 0; gi < GM; ++gi) {
-                const bool okg = ok && k + gi < kend;     // element test for the scalar path
-                vl[st][gi] = okg ? v[gi] : 0.0f;
-                const int c = ((k + gi) << lb) + o[gi];
-                cl[st][gi] = okg ? (c < N ? c : N - 1) : -1;   // the encode gives c < N
-            }
+            raw[st] = PL::issue(vr, go, j0, row_ok && k < kend ? k : kbeg);
         }
-        static_for<0, DEPTH>([&](auto stc) {
-            constexpr int st = decltype(stc)::value;
-            if (k0 + st * S >= kend) return;               // wave-uniform
-            static_for<0, S / kSpmmBatch>([&](auto bc) {
-                constexpr int b0 = decltype(bc)::value * kSpmmBatch;
-                float vv[kSpmmBatch];
-                int cc[kSpmmBatch];
-                typename XL::V xv[kSpmmBatch];
-                static_for<0, kSpmmBatch>([&](auto uc) {
-                    constexpr int f = b0 + decltype(uc)::value;   // weight k0 + st*S + f
-                    vv[f - b0] = __builtin_bit_cast(
-                        float, group_bcast<LGL, f / GM>(__builtin_bit_cast(int, vl[st][f % GM])));
-                    cc[f - b0] = group_bcast<LGL, f / GM>(cl[st][f % GM]);
-                    const int64_t c = cc[f - b0] >= 0 ? cc[f - b0] : 0;
-                    xv[f - b0] = XL::load(X + c * ldx + col_c);
-                });
-#pragma unroll
-                for (int u = 0; u < kSpmmBatch; ++u) {
-                    if (cc[u] >= 0 && col_ok) {
-#pragma unroll
-                        for (int q = 0; q < CPL; ++q)
-                            acc[q] = fmaf(vv[u], XL::get(xv[u], q), acc[q]);
-                    }
-                }
+    };
+    // gathers of one round (DEPTH steps of S weights), NB X rows in flight per lane;
+    // `after` runs right after the round's last gathers are issued (the next round's
+    // pair loads go there, so they overlap these gathers without delaying their use)
+    auto gather_round = [&](int k0, const float (&vl)[DEPTH][GM], const int (&cl)[DEPTH][GM],
+                            auto &&after) {
+        static_for<0, T / NB>([&](auto bc) {
+            constexpr int b0 = decltype(bc)::value * NB;
+            if (k0 + (b0 / S) * S >= kend) return;         // wave-uniform: past the share
+            float vv[NB];
+            int cc[NB];
+            typename XL::V xv[NB];
+            static_for<0, NB>([&](auto uc) {
+                constexpr int f = b0 + decltype(uc)::value;   // weight k0 + f of the round
+                constexpr int st = f / S, fs = f % S;
+                vv[f - b0] = __builtin_bit_cast(
+                    float, group_bcast<LGL, fs / GM>(__builtin_bit_cast(int, vl[st][fs % GM])));
+                cc[f - b0] = group_bcast<LGL, fs / GM>(cl[st][fs % GM]);
+                const int64_t c = cc[f - b0] >= 0 ? cc[f - b0] : 0;
+                xv[f - b0] = XL::load(X + c * ldx + col_c);
             });
+            if constexpr (b0 + NB == T) after();
+#pragma unroll
+            for (int u = 0; u < NB; ++u) {
+                if (cc[u] >= 0 && col_ok) {
+#pragma unroll
+                    for (int q = 0; q < CPL; ++q)
+                        acc[q] = fmaf(vv[u], XL::get(xv[u], q), acc[q]);
+                }
+            }
         });
+    };
+
+    if (vec_pairs) {
+        // software pipelined: the pairs of round i + 1 load while round i gathers
+        typename PL::Raw raw[DEPTH];
+        if (kbeg < kend) issue_round(kbeg, raw);          // wave-uniform
+        for (int k0 = kbeg; k0 < kend; k0 += DEPTH * S) {
+            float vl[DEPTH][GM];
+            int cl[DEPTH][GM];
+#pragma unroll
+            for (int st = 0; st < DEPTH; ++st) {
+                float v[GM];
+                int o[GM];
+                PL::decode(raw[st], go, v, o);
+                settle(k0, st, v, o, vl, cl);
+            }
+            const int k1 = k0 + DEPTH * S;
+            gather_round(k0, vl, cl, [&] {
+                if (k1 < kend) issue_round(k1, raw);      // wave-uniform
+            });
+        }
+    } else {
+        for (int k0 = kbeg; k0 < kend; k0 += DEPTH * S) {
+            float vl[DEPTH][GM];
+            int cl[DEPTH][GM];
+#pragma unroll
+            for (int st = 0; st < DEPTH; ++st) {
+                const int k = k0 + st * S + sub * GM;
+                float v[GM];
+                int o[GM];
+                PL::load(vr, go, j0, row_ok && k < kend ? k : kbeg, nblk, false, v, o);
+                settle(k0, st, v, o, vl, cl);
+            }
+            gather_round(k0, vl, cl, [] {});
+        }
     }
 
     // combine the KS partial sums of each row group in a fixed order
@@ -1049,13 +1107,16 @@ hipError_t launch_spmm_t(const darb_plan &p, const void *values, const uint8_t *
         }
     }
     ProductSchedule s;
-    if (!spmm_schedule(p, B, vec ? CPL : 1, sizeof(Tw), values, offsets, s))
+    // up to kNarrowBatch columns, one column per lane: a row takes up to 16 lanes
+    // instead of B / CPL, so waves cover fewer rows and a launch has more of them
+    const bool wide = vec && B > kNarrowBatch;
+    if (!spmm_schedule(p, B, wide ? CPL : 1, sizeof(Tw), values, offsets, s))
         return hipErrorInvalidConfiguration;
     if (s.block_begin[s.nbins] == 0) return hipSuccess;
     const Tw *v = static_cast<const Tw *>(values);
     const void *offs = offset_source(p, offsets, packed);
     const Tx *x = static_cast<const Tx *>(X);
-    if (vec) return launch_spmm_cpl<Tw, Tx, CPL, PK>(p, s, v, offs, B, x, ldx, Y, ldy, st);
+    if (wide) return launch_spmm_cpl<Tw, Tx, CPL, PK>(p, s, v, offs, B, x, ldx, Y, ldy, st);
     return launch_spmm_cpl<Tw, Tx, 1, PK>(p, s, v, offs, B, x, ldx, Y, ldy, st);
 }
 
