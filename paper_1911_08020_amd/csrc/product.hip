@@ -17,9 +17,9 @@
 // xor butterfly in a fixed order (deterministic) and written in original row order.
 //
 // SpMM: lanes map to batch columns (X is [N x B] row-major, so one weight's
-// activations X[c, :] are contiguous), CPL columns per lane with 16-byte loads
-// (one column per lane for batches up to 16, so small batches still spread over
-// many waves).  Each wave loads its rows' (value, column) pairs with coalesced
+// activations X[c, :] are contiguous), CPL columns per lane with 16-byte loads, or
+// narrower ones for small batches so that a row still spreads over up to 16 lanes
+// and the launch over many waves.  Each wave loads its rows' (value, column) pairs with coalesced
 // loads and broadcasts them across a row's lanes register to register (DPP,
 // swizzle or readlane), gathering X rows kSpmmBatch at a time; the next round's
 // pairs load while this round gathers.  Up to 8 waves split a row group's weights
@@ -41,6 +41,7 @@ namespace darb {
 namespace {
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
@@ -351,7 +352,7 @@ __global__ __launch_bounds__(kSpmvThreads) void spmv_kernel(
 constexpr int kSpmmThreads = 512;
 constexpr int kSpmmWaves = kSpmmThreads / kWave;
 constexpr int kSpmmBatch = 8;         // X rows in flight per lane (more waves beat deeper batches)
-constexpr int kNarrowBatch = 16;      // batches up to this take one column per lane
+constexpr int kRowLanes = 16;         // lanes per row that narrow columns aim at
 
 // CPL consecutive batch columns of one X row, loaded at once (16 bytes when CPL > 1).
 template <typename Tx, int CPL> struct XLoad;
@@ -364,6 +365,24 @@ template <> struct XLoad<float, 4> {
     using V = f32x4;
     __device__ static V load(const float *p) { return *reinterpret_cast<const f32x4 *>(p); }
     __device__ static float get(const V &v, int i) { return v[i]; }
+};
+template <> struct XLoad<float, 2> {
+    using V = f32x2;
+    __device__ static V load(const float *p) { return *reinterpret_cast<const f32x2 *>(p); }
+    __device__ static float get(const V &v, int i) { return v[i]; }
+};
+template <> struct XLoad<__half, 2> {
+    using V = uint32_t;
+    __device__ static V load(const __half *p) { return *reinterpret_cast<const uint32_t *>(p); }
+    __device__ static float get(const V &v, int i) { return half_bits_to_f32(i ? v >> 16 : v); }
+};
+template <> struct XLoad<__half, 4> {
+    using V = u32x2;
+    __device__ static V load(const __half *p) { return *reinterpret_cast<const u32x2 *>(p); }
+    __device__ static float get(const V &v, int i) {
+        const uint32_t w = v[i >> 1];
+        return half_bits_to_f32((i & 1) ? (w >> 16) : w);
+    }
 };
 template <> struct XLoad<__half, 8> {
     using V = u32x4;
@@ -499,9 +518,10 @@ __device__ __forceinline__ void spmm_tile(
     const int64_t col0 = (int64_t(slab) * L + sub) * CPL;
     const bool col_ok = col0 < B;                         // CPL > 1 only when CPL divides B
     const int64_t col_c = col_ok ? col0 : 0;
-    // each wave's share is a whole number of steps, so a lane's GM-vector of weights is
-    // either entirely inside [kbeg, kend) or entirely outside
-    const int share = (((nblk + KS - 1) / KS) + S - 1) / S * S;
+    // each wave's share is a multiple of 16 weights (of GM, so a lane's GM-vector of
+    // weights is either entirely inside [kbeg, kend) or entirely outside); the split
+    // points do not depend on the lanes per row, so neither do the sums
+    const int share = (((nblk + KS - 1) / KS) + 15) / 16 * 16;
     const int kbeg = ks * share;
     const int kend = kbeg + share < nblk ? kbeg + share : nblk;
     const int64_t j0 = (row0 + (row_ok ? rl : 0)) * nblk;   // the row's first slot in its group
@@ -1044,14 +1064,19 @@ hipError_t launch_spmm_cpl(const darb_plan &p, const ProductSchedule &s, const T
                            int64_t ldy, hipStream_t st) {
     const int blocks = s.block_begin[s.nbins];
     const int N = int(p.N);
+    const int lgl = s.log2_lanes[0];
+    // the widths between one column and 16 bytes are chosen only for rows of more
+    // than 8 lanes, so only those kernels exist
+    constexpr bool kEvery = CPL == 1 || CPL * int(sizeof(Tx)) == 16;
+    if (!kEvery && lgl < 4) return hipErrorInvalidConfiguration;
 #define DARB_SPMM(LGL)                                                                    \
     hipLaunchKernelGGL((spmm_kernel<Tw, Tx, CPL, LGL, PK>), dim3(blocks), dim3(kSpmmThreads), \
                        0, st, v, offs, x, ldx, B, Y, ldy, p.d_perm, N, p.bins, s)
-    switch (s.log2_lanes[0]) {
-        case 0: DARB_SPMM(0); break;
-        case 1: DARB_SPMM(1); break;
-        case 2: DARB_SPMM(2); break;
-        case 3: DARB_SPMM(3); break;
+    switch (lgl) {
+        case 0: if constexpr (kEvery) DARB_SPMM(0); break;
+        case 1: if constexpr (kEvery) DARB_SPMM(1); break;
+        case 2: if constexpr (kEvery) DARB_SPMM(2); break;
+        case 3: if constexpr (kEvery) DARB_SPMM(3); break;
         case 4: DARB_SPMM(4); break;
         case 5: DARB_SPMM(5); break;
         default: DARB_SPMM(6); break;
@@ -1076,9 +1101,9 @@ hipError_t launch_spmm_t(const darb_plan &p, const void *values, const uint8_t *
                          const uint32_t *packed, int64_t B, const void *X, int64_t ldx, float *Y,
                          int64_t ldy, hipStream_t st) {
     constexpr int CPL = 16 / int(sizeof(Tx));
-    const bool vec = (reinterpret_cast<uintptr_t>(X) % 16 == 0) &&
-                     ((ldx * int64_t(sizeof(Tx))) % 16 == 0) && (B % CPL == 0);
     if constexpr (std::is_same<Tx, float>::value && !PK) {
+        const bool vec = (reinterpret_cast<uintptr_t>(X) % 16 == 0) &&
+                         ((ldx * int64_t(sizeof(Tx))) % 16 == 0) && (B % CPL == 0);
         int lgl = vec ? xlds_lgl(p, B) : -1;
         // every row's steps of 16 pairs load as 16-byte vectors
         bool aligned16 = reinterpret_cast<uintptr_t>(values) % (kXldsStep * sizeof(Tw)) == 0 &&
@@ -1106,18 +1131,34 @@ hipError_t launch_spmm_t(const darb_plan &p, const void *values, const uint8_t *
             return hipGetLastError();
         }
     }
+    // columns per lane: 16 bytes of X when that leaves a row at least 5 lanes (a
+    // group of 8); for smaller batches the fewest columns that keep a row within 16
+    // lanes, so the launch still has many waves.  The width must divide B and keep
+    // the loads aligned.  (Measured: 16-byte loads on 8 lanes beat 8-byte loads on 16;
+    // rows of 2 or 4 lanes leave too few waves.)
+    auto fits = [&](int c) {
+        const int64_t bytes = int64_t(c) * int64_t(sizeof(Tx));
+        return B % c == 0 && reinterpret_cast<uintptr_t>(X) % bytes == 0 &&
+               (ldx * int64_t(sizeof(Tx))) % bytes == 0;
+    };
+    int cpl = 1;
+    if ((B + CPL - 1) / CPL > 4 && fits(CPL)) {
+        cpl = CPL;
+    } else {
+        while (cpl < CPL && (B + cpl - 1) / cpl > kRowLanes && fits(2 * cpl)) cpl *= 2;
+    }
     ProductSchedule s;
-    // up to kNarrowBatch columns, one column per lane: a row takes up to 16 lanes
-    // instead of B / CPL, so waves cover fewer rows and a launch has more of them
-    const bool wide = vec && B > kNarrowBatch;
-    if (!spmm_schedule(p, B, wide ? CPL : 1, sizeof(Tw), values, offsets, s))
+    if (!spmm_schedule(p, B, cpl, sizeof(Tw), values, offsets, s))
         return hipErrorInvalidConfiguration;
     if (s.block_begin[s.nbins] == 0) return hipSuccess;
     const Tw *v = static_cast<const Tw *>(values);
     const void *offs = offset_source(p, offsets, packed);
     const Tx *x = static_cast<const Tx *>(X);
-    if (wide) return launch_spmm_cpl<Tw, Tx, CPL, PK>(p, s, v, offs, B, x, ldx, Y, ldy, st);
-    return launch_spmm_cpl<Tw, Tx, 1, PK>(p, s, v, offs, B, x, ldx, Y, ldy, st);
+    if (cpl == 1) return launch_spmm_cpl<Tw, Tx, 1, PK>(p, s, v, offs, B, x, ldx, Y, ldy, st);
+    if (cpl == 2) return launch_spmm_cpl<Tw, Tx, 2, PK>(p, s, v, offs, B, x, ldx, Y, ldy, st);
+    if (cpl == 4) return launch_spmm_cpl<Tw, Tx, 4, PK>(p, s, v, offs, B, x, ldx, Y, ldy, st);
+    if constexpr (CPL == 8) return launch_spmm_cpl<Tw, Tx, 8, PK>(p, s, v, offs, B, x, ldx, Y, ldy, st);
+    return hipErrorInvalidConfiguration;
 }
 
 template <typename Tw, typename Tx>

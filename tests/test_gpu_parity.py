@@ -190,6 +190,34 @@ def test_spmm_batches(darb, B, wx):
         check_product(host(y), vals, offs, lay, X[:, 0], wdt, "spmv")
 
 
+@pytest.mark.parametrize("B", [8, 20, 24, 32, 48, 64, 96, 128])
+@pytest.mark.parametrize("wx", [("f32", "f32"), ("f16", "f16"), ("f16", "f32")])
+def test_spmm_column_widths(darb, B, wx):
+    # a lane takes 1, 2, 4 (or 8 fp16) columns depending on B and on the alignment of
+    # X's rows: 16-byte rows (ldx = B), rows aligned to 4 columns only (ldx = B + 4:
+    # 16 bytes for fp32, 8 for fp16), to 2 columns (ldx = B + 2) or to one.  Every
+    # width sums each column in the same order, so all four results are bitwise equal.
+    wdt, xdt = {"f32": np.float32, "f16": np.float16}[wx[0]], {"f32": np.float32,
+                                                              "f16": np.float16}[wx[1]]
+    say(f"spmm column widths B={B} w={wx[0]} x={wx[1]}")
+    rng = np.random.default_rng(1000 + B)
+    M, N = 400, 1536
+    W = rng.standard_normal((M, N)).astype(wdt)
+    d = rng.integers(0, N // 3, size=M) / N
+    plan, lay, vals, offs = encode_both(darb, W, d, 0.1, 0, 2, 64)
+    X = rng.standard_normal((N, B)).astype(xdt)
+    vd, od = dev(vals), dev(offs)
+    outs = []
+    for pad in (0, 4, 2, 1):
+        Xbig = np.zeros((N, B + pad), dtype=xdt)
+        Xbig[:, :B] = X
+        Xd = dev(Xbig)[:, :B]
+        outs.append(host(plan.spmm(vd, od, Xd)))
+    check_product(outs[0], vals, offs, lay, X, wdt, f"B={B} aligned")
+    for o in outs[1:]:
+        assert np.array_equal(o.view(np.uint32), outs[0].view(np.uint32))
+
+
 @pytest.mark.parametrize("case", ["all_empty_rows", "b_one", "b_wider_than_row", "one_row",
                                   "wide_no_lds", "odd_nblk", "fp16_odd"])
 def test_product_edge_cases(darb, case):
