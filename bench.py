@@ -58,7 +58,7 @@ def step_bytes(M, N, nnz, s_w, s_x, B):
 
 
 # source file of each measured kernel; its local includes (the public header among them),
-# the C-ABI layer that lays out the plan and the build script (flags) are hashed with it
+# the C-ABI layer that lays out the plan and the compile flags are hashed with it
 KERNEL_SOURCES = {"encode": "encode.hip", "pack": "packed.hip", "spmv": "product.hip",
                   "spmm": "product.hip", "spmv_packed": "product.hip",
                   "spmm_packed": "product.hip", "prune": "prune.hip"}
@@ -72,9 +72,10 @@ def kernel_sha256(kernel):
     src = KERNEL_SOURCES.get(kernel)
     if src is None:
         return None
+    from paper_1911_08020_amd import build as _build
     pkg = os.path.join(ROOT, "paper_1911_08020_amd")
-    dirs = (os.path.join(pkg, "csrc"), os.path.join(ROOT, "include"), pkg)
-    todo, seen = [src, "api.cpp", "build.py"], {}
+    dirs = (os.path.join(pkg, "csrc"), os.path.join(ROOT, "include"))
+    todo, seen = [src, "api.cpp"], {"compile flags": repr(_build.HIPCC_FLAGS).encode()}
     while todo:
         name = todo.pop(0)
         if name in seen:
