@@ -16,6 +16,8 @@ in fp64 (``lstm_forward``).  Functions and the paper passages they follow:
 * ``decode``       -- the masked dense matrix the format stands for
 * ``spmm``         -- section 2 / 3.2, product over retained weights, offsets select activations
 * ``pack_offsets``  -- section 4.2, log2(b)-bit indices (and ``unpack_offsets``)
+* ``quantize_i8``  -- section 4.2's storage accounting (INT8 weights): per-row
+                      symmetric codes and scales (``spmm_i8`` is their product)
 * ``prune_counts`` -- section 3.2's first step (irregular top-K magnitude pruning,
                       section 2), per-row kept counts that give the row densities
 * ``dense_masked_product`` -- the plain definition of the product: a dense fp64 matmul
@@ -254,6 +256,63 @@ def prune_counts(W: np.ndarray, k: int) -> np.ndarray:
     if rc != 0:
         raise ValueError("invalid pruning arguments")
     return counts
+
+
+# Rows whose largest retained magnitude is below this quantise to zero: 127 / absmax
+# must stay finite in fp32.
+I8_MIN_ABSMAX = np.float32(2.0 ** -120)
+
+
+def quantize_i8(values: np.ndarray, lay: Layout):
+    """INT8 retained weights (section 4.2's storage accounting assumes INT8 weights).
+
+    Reading of the paper, which does not fix the scheme: symmetric, one scale per
+    row over the row's retained weights.  With a = max |v| over the row (fp32),
+    inv = 127 / a and every code is q = rint(v * inv) (round half to even), clamped to
+    [-127, 127]; the row's scale is s = a / 127 so that v ~ s * q.  Every operation
+    is a single correctly rounded fp32 operation, in this order.  Rows with
+    a < 2^-120 (all zero, or so small that 127 / a would overflow) get s = 0 and
+    q = 0.  Values must be finite.
+
+    Returns (codes int8 [nnz] in the format's slot order, scales float32 [M] by
+    original row).
+    """
+    v32 = np.ascontiguousarray(values).astype(np.float32)   # fp16 -> fp32 is exact
+    if not np.all(np.isfinite(v32)):
+        raise ValueError("INT8 quantisation needs finite values")
+    codes = np.zeros(lay.nnz, dtype=np.int8)
+    scales = np.zeros(lay.M, dtype=np.float32)
+    nblk = lay.nblk
+    c127 = np.float32(127.0)
+    for r in range(lay.M):
+        s0, n = int(lay.row_start[r]), int(nblk[r])
+        row = v32[s0:s0 + n]
+        a = np.max(np.abs(row)) if n else np.float32(0.0)
+        if not a >= I8_MIN_ABSMAX:
+            continue
+        inv = np.float32(c127 / a)
+        q = np.rint(row * inv)                                # fp32 product, half to even
+        codes[s0:s0 + n] = np.clip(q, -127, 127).astype(np.int8)
+        scales[r] = np.float32(a / c127)
+    return codes, scales
+
+
+def spmm_i8(codes: np.ndarray, scales: np.ndarray, offsets: np.ndarray, lay: Layout,
+            X: np.ndarray) -> np.ndarray:
+    """fp64 product of the INT8 format: y[r] = s_r * sum_k q[r,k] * x[k*b_r + off]."""
+    q = np.ascontiguousarray(codes, dtype=np.int8).astype(np.float32)   # exact
+    Y = spmm(q, offsets, lay, X)
+    s = np.asarray(scales, dtype=np.float64)
+    return Y * (s if Y.ndim == 1 else s[:, None])
+
+
+def spmm_i8_absdot(codes: np.ndarray, scales: np.ndarray, offsets: np.ndarray, lay: Layout,
+                   X: np.ndarray) -> np.ndarray:
+    """fp64 |s_r| * sum_k |q * x|: the rounding-error scale of the INT8 product."""
+    q = np.ascontiguousarray(codes, dtype=np.int8).astype(np.float32)
+    A = spmm_absdot(q, offsets, lay, X)
+    s = np.abs(np.asarray(scales, dtype=np.float64))
+    return A * (s if A.ndim == 1 else s[:, None])
 
 
 def dense_masked_product(Wm: np.ndarray, X: np.ndarray) -> np.ndarray:

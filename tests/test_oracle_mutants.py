@@ -1,8 +1,8 @@
 """Plant mistakes in copies of the oracle and check that the pins catch each one.
 
-Each mutant is a textual change to a copy of oracle/darb_oracle.c, compiled on
-the CPU into a temporary library and driven through a fresh copy of the oracle's
-Python wrapper.  The real oracle must pass ``pin_suite``; every mutant must fail it.
+Each mutant is a textual change to a copy of oracle/darb_oracle.c (compiled on
+the CPU into a temporary library) or of the oracle's Python wrapper, driven
+through a fresh copy of that wrapper.  The real oracle must pass ``pin_suite``; every mutant must fail it.
 """
 import importlib.util
 import os
@@ -40,18 +40,32 @@ MUTANTS = {
                          "key = ((const uint32_t *)W)[r * ldw + c];")],
     "prune_keeps_one_less": [("for (int64_t i = 0; i < k; ++i) counts",
                               "for (int64_t i = 1; i < k; ++i) counts")],
+    # INT8 values (edits of the Python wrapper, where that arithmetic lives)
+    "i8_round_half_up": [("py", "q = np.rint(row * inv)",
+                          "q = np.floor(row * inv + np.float32(0.5))")],
+    "i8_scale_128": [("py", "inv = np.float32(c127 / a)", "inv = np.float32(np.float32(128.0) / a)")],
+    "i8_matrix_absmax": [("py", "a = np.max(np.abs(row)) if n else np.float32(0.0)",
+                          "a = np.max(np.abs(v32))")],
+    "i8_scale_inverted": [("py", "scales[r] = np.float32(a / c127)",
+                           "scales[r] = np.float32(c127 / a)")],
 }
 
 
 def _load_variant(tmp_path, name, edits):
+    """Edits are (old, new) on darb_oracle.c or ("py", old, new) on __init__.py."""
     src = open(os.path.join(ORACLE_DIR, "darb_oracle.c")).read()
-    for old, new in edits:
-        assert old in src, (name, old)
-        src = src.replace(old, new)
+    py = open(os.path.join(ORACLE_DIR, "__init__.py")).read()
+    for e in edits:
+        if e[0] == "py":
+            assert e[1] in py, (name, e[1])
+            py = py.replace(e[1], e[2])
+        else:
+            assert e[0] in src, (name, e[0])
+            src = src.replace(e[0], e[1])
     d = tmp_path / name
     d.mkdir()
     (d / "darb_oracle.c").write_text(src)
-    shutil.copy(os.path.join(ORACLE_DIR, "__init__.py"), d / "__init__.py")
+    (d / "__init__.py").write_text(py)
     spec = importlib.util.spec_from_file_location(f"oracle_mutant_{name}", str(d / "__init__.py"))
     mod = importlib.util.module_from_spec(spec)
     sys.modules[spec.name] = mod          # dataclasses look their module up here
@@ -106,6 +120,15 @@ def pin_suite(orc):
         W = (rng.integers(-3, 4, size=(4, 9)) * 0.5).astype(dtype)
         for k in (0, 1, 5, 17, 36):
             assert orc.prune_counts(W, k).tolist() == prune_brute(W, k), (dtype, k)
+    # INT8 values: the hand example (ties to even, per-row scale, zero row)
+    lay = orc.layout(8, np.array([1, 2, 3], dtype=np.uint8))
+    vals = np.zeros(lay.nnz, dtype=np.float32)
+    for r, row in enumerate([[127.0, 2.5, -3.5, 0.5], [-2.0, 1.0], [0.0]]):
+        vals[int(lay.row_start[r]):int(lay.row_start[r]) + len(row)] = row
+    q, s = orc.quantize_i8(vals, lay)
+    assert [q[int(lay.row_start[r]):int(lay.row_start[r]) + int(lay.nblk[r])].tolist()
+            for r in range(3)] == [[127, 2, -4, 0], [-127, 64], [0]]
+    assert s.tolist() == [1.0, float(np.float32(2.0) / np.float32(127.0)), 0.0]
     # fp16 decoding of a few bit patterns against numpy
     for bits in [0x3C00, 0x0001, 0x7BFF, 0xC000, 0x0400]:
         assert orc.half_to_double(bits) == float(np.array([bits], np.uint16).view(np.float16)[0])

@@ -447,3 +447,86 @@ def test_prune_counts_invariants_and_generator_agreement():
     mi = workloads.make_matrix(256, 512, wdtype="f16", dist="normal", sigma=0.7, keep=0.05,
                                seed=3)
     assert np.array_equal(oracle.prune_counts(mi.W, mi.k), mi.mask.sum(axis=1))
+
+
+# --------------------------------------------------------------------------------
+# INT8 values (section 4.2's storage accounting assumes INT8 weights; the scheme is
+# the reading documented on oracle.quantize_i8)
+# --------------------------------------------------------------------------------
+
+def _rows_to_slots(lay, rows):
+    """values in slot order from a list of per-original-row value lists."""
+    vals = np.zeros(lay.nnz, dtype=np.float32)
+    for r, row in enumerate(rows):
+        s = int(lay.row_start[r])
+        vals[s:s + len(row)] = row
+    return vals
+
+
+def test_int8_hand_example():
+    # row 0 (b = 2, four blocks): absmax 127, so 127 / a = 1 and the codes are rint of
+    # the values: 2.5 -> 2 and -3.5 -> -4 (ties to even), 0.5 -> 0; scale 1.
+    # row 1 (b = 4, two blocks): absmax 2, 127 / 2 = 63.5 exactly: -2 -> -127,
+    # 1 -> 63.5 -> 64 (even); scale 2 / 127.  row 2: all zero -> scale 0, codes 0.
+    lay = oracle.layout(8, np.array([1, 2, 3], dtype=np.uint8))
+    vals = _rows_to_slots(lay, [[127.0, 2.5, -3.5, 0.5], [-2.0, 1.0], [0.0]])
+    q, s = oracle.quantize_i8(vals, lay)
+    got = [q[int(lay.row_start[r]):int(lay.row_start[r]) + int(lay.nblk[r])].tolist()
+           for r in range(3)]
+    assert got == [[127, 2, -4, 0], [-127, 64], [0]]
+    assert s.dtype == np.float32
+    assert s[0] == np.float32(1.0) and s[1] == np.float32(2.0) / np.float32(127.0) and s[2] == 0
+
+
+def test_int8_small_absmax_threshold():
+    # one row of two blocks (b = 1): absmax exactly 2^-120 still quantises (127 / a
+    # is finite), half of it does not
+    lay = oracle.layout(2, np.array([0], dtype=np.uint8))
+    t = float(oracle.I8_MIN_ABSMAX)
+    q, s = oracle.quantize_i8(np.array([t, -t / 2], dtype=np.float32), lay)
+    assert q.tolist() == [127, -64] and s[0] > 0        # -63.5 -> -64 (ties to even)
+    q, s = oracle.quantize_i8(np.array([t / 2, 0.0], dtype=np.float32), lay)
+    assert q.tolist() == [0, 0] and s.tolist() == [0.0]
+    with pytest.raises(ValueError):
+        oracle.quantize_i8(np.array([np.inf, 1.0], dtype=np.float32), lay)
+
+
+@pytest.mark.parametrize("dtype", [np.float32, np.float16])
+def test_int8_invariants_and_error_bound(dtype):
+    rng = np.random.default_rng(5)
+    M, N = 40, 300
+    W = (rng.standard_normal((M, N)) * np.exp(rng.uniform(-6, 3, size=(M, 1)))).astype(dtype)
+    lay = oracle.layout(N, rng.integers(0, 7, size=M).astype(np.uint8))
+    vals, _ = oracle.encode(W, lay)
+    q, s = oracle.quantize_i8(vals, lay)
+    v = vals.astype(np.float64)
+    for r in range(M):
+        sl = slice(int(lay.row_start[r]), int(lay.row_start[r]) + int(lay.nblk[r]))
+        qa = np.abs(q[sl].astype(np.int64))
+        assert qa.max() == 127                                    # the largest maps to 127
+        # round to nearest: |s q - v| <= s / 2, up to the two fp32 roundings of s and v*inv
+        err = np.abs(float(s[r]) * q[sl].astype(np.float64) - v[sl])
+        assert (err <= float(s[r]) * (0.5 + 1e-5) + 1e-30).all()
+    # fp16 values quantise exactly as the same values widened to fp32
+    if dtype == np.float16:
+        q2, s2 = oracle.quantize_i8(vals.astype(np.float32), lay)
+        assert np.array_equal(q, q2) and np.array_equal(s, s2)
+
+
+def test_int8_product_is_dequantised_masked_column():
+    # y = W_i8 e_c picks column c of the dequantised masked matrix s_r * q
+    rng = np.random.default_rng(8)
+    M, N = 12, 40
+    W = rng.standard_normal((M, N)).astype(np.float32)
+    lay = oracle.layout(N, rng.integers(0, 4, size=M).astype(np.uint8))
+    vals, offs = oracle.encode(W, lay)
+    q, s = oracle.quantize_i8(vals, lay)
+    Dq = oracle.decode(q.astype(np.float32), offs, lay).astype(np.float64) * \
+        s.astype(np.float64)[:, None]
+    for c in range(N):
+        e = np.zeros(N, dtype=np.float32)
+        e[c] = 1.0
+        assert np.array_equal(oracle.spmm_i8(q, s, offs, lay, e), Dq[:, c])
+    X = rng.standard_normal((N, 3)).astype(np.float32)
+    assert np.allclose(oracle.spmm_i8(q, s, offs, lay, X), Dq @ X.astype(np.float64),
+                       rtol=0, atol=1e-12)
