@@ -219,6 +219,34 @@ int darb_spmm_packed(const darb_plan *plan, int wdtype, const void *values,
                      float *Y, int64_t ldy, void *stream);
 
 /*
+ * INT8 retained weights.  Section 4.2's storage accounting assumes weights
+ * quantised to INT8 without fixing a scheme; this one is symmetric with one fp32
+ * scale per row.  For row r with a = max |v| over its retained values (fp32, fp16
+ * widened exactly): inv = 127 / a, code q = rint(v * inv) (ties to even) clamped to
+ * [-127, 127], scale s_r = a / 127 -- each a single correctly rounded fp32
+ * operation, so the codes are exact.  Rows with a < 2^-120 (127 / a would
+ * overflow) get s_r = 0 and all-zero codes.  Values must be finite.
+ *   darb_quantize_i8
+ *     values   device, the format's values (wdtype DARB_F32 or DARB_F16), nnz
+ *     codes    device int8 [nnz], slot order like values, overwritten
+ *     scales   device fp32 [M], indexed by original row, overwritten
+ *   darb_spmv_i8 / darb_spmm_i8: y[r] = s_r * sum_k q[r,k] * x[k * b_r + off[r,k]],
+ *     summed in fp32 and scaled once; as darb_spmv / darb_spmm (same layouts, x/X
+ *     fp32 or fp16, Y fp32) with the offsets from exactly one of `offsets` (one byte
+ *     each) and `packed` (darb_pack_offsets' words; with offsets NULL, packed may be
+ *     NULL only when the plan has no packed words).  Passing both is an error.
+ * Errors: DARB_E_INVALID, DARB_E_DTYPE, DARB_E_NOT_UPLOADED, DARB_E_HIP.
+ */
+int darb_quantize_i8(const darb_plan *plan, int wdtype, const void *values, int8_t *codes,
+                     float *scales, void *stream);
+int darb_spmv_i8(const darb_plan *plan, const int8_t *codes, const float *scales,
+                 const uint8_t *offsets, const uint32_t *packed, int xdtype, const void *x,
+                 float *y, void *stream);
+int darb_spmm_i8(const darb_plan *plan, const int8_t *codes, const float *scales,
+                 const uint8_t *offsets, const uint32_t *packed, int xdtype, int64_t B,
+                 const void *X, int64_t ldx, float *Y, int64_t ldy, void *stream);
+
+/*
  * Irregular magnitude pruning, the step DARB starts from (section 3.2: the
  * irregular mask is computed only to measure each row's density; irregular
  * pruning keeps the K largest-magnitude weights, section 2).  Keeps the k

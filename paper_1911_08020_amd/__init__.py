@@ -93,6 +93,9 @@ def _load_library():
         "darb_unpack_offsets": ([P, P, P, P], I),
         "darb_spmv_packed": ([P, I, P, P, I, P, P, P], I),
         "darb_spmm_packed": ([P, I, P, P, I, I64, P, I64, P, I64, P], I),
+        "darb_quantize_i8": ([P, I, P, P, P, P], I),
+        "darb_spmv_i8": ([P, P, P, P, P, I, P, P, P], I),
+        "darb_spmm_i8": ([P, P, P, P, P, I, I64, P, I64, P, I64, P], I),
         "darb_lstm_layer": ([P, P, P, P, P, P, I, I64, I64, I64, P, P, P, P, P, I64, P], I),
         "darb_lstm_workspace": ([I64, I64, I64, ctypes.POINTER(I64)], I),
         "darb_stream_read": ([P, I64, P, P], I),
@@ -112,7 +115,8 @@ EXPORTED = ("darb_plan_create", "darb_plan_create_counts", "darb_prune_workspace
             "darb_prune_counts", "darb_plan_info", "darb_plan_export", "darb_plan_upload",
             "darb_plan_destroy", "darb_encode", "darb_decode", "darb_spmv", "darb_spmm",
             "darb_pack_offsets", "darb_unpack_offsets", "darb_spmv_packed", "darb_spmm_packed",
-            "darb_lstm_layer", "darb_lstm_workspace", "darb_stream_read", "darb_stream_copy", "darb_strerror",
+            "darb_quantize_i8", "darb_spmv_i8", "darb_spmm_i8", "darb_lstm_layer",
+            "darb_lstm_workspace", "darb_stream_read", "darb_stream_copy", "darb_strerror",
             "darb_last_error", "darb_version")
 
 
@@ -349,7 +353,63 @@ class Plan:
                                      _stream_ptr(stream)), "darb_spmm_packed")
         return Y
 
+    # -- INT8 values ------------------------------------------------------------------
+    def quantize_i8(self, values, codes=None, scales=None, stream=None):
+        """Retained values -> (codes int8 [nnz], scales fp32 [M] by original row).
+
+        Per-row symmetric INT8 (section 4.2 assumes INT8 weights): s_r = max|v| / 127,
+        q = rint(v * 127 / max|v|); see darb_quantize_i8 in include/darb.h.
+        """
+        torch = _torch()
+        _require_cuda(values)
+        self._check_values(values)
+        if codes is None:
+            codes = torch.empty(self.nnz, dtype=torch.int8, device=values.device)
+        if scales is None:
+            scales = torch.empty(self.M, dtype=torch.float32, device=values.device)
+        self._check_i8(codes, scales)
+        _check(_lib.darb_quantize_i8(self._h, _dtype_code(values), _ptr(values), _ptr(codes),
+                                     _ptr(scales), _stream_ptr(stream)), "darb_quantize_i8")
+        return codes, scales
+
+    def _i8_offsets(self, offsets, packed):
+        if (offsets is None) == (packed is None):
+            raise ValueError("pass exactly one of offsets (bytes) and packed (words)")
+        if offsets is not None:
+            _require_cuda(offsets)
+            _check_format(offsets, self.nnz, "offsets", (_torch().uint8,))
+            return _ptr(offsets), None
+        _require_cuda(packed)
+        self._check_packed(packed)
+        return None, _ptr(packed)
+
+    def spmv_i8(self, codes, scales, x, offsets=None, packed=None, y=None, stream=None):
+        """y = diag(scales) (W_i8 x), offsets as bytes or packed words."""
+        _require_cuda(codes, scales, x)
+        self._check_i8(codes, scales)
+        po, pp = self._i8_offsets(offsets, packed)
+        y = self._vector_out(x, y)
+        _check(_lib.darb_spmv_i8(self._h, _ptr(codes), _ptr(scales), po, pp, _dtype_code(x),
+                                 _ptr(x), _ptr(y), _stream_ptr(stream)), "darb_spmv_i8")
+        return y
+
+    def spmm_i8(self, codes, scales, X, offsets=None, packed=None, Y=None, stream=None):
+        """Y = diag(scales) (W_i8 X), offsets as bytes or packed words."""
+        _require_cuda(codes, scales, X)
+        self._check_i8(codes, scales)
+        po, pp = self._i8_offsets(offsets, packed)
+        B, ldx, Y, ldy = self._matrix_out(X, Y)
+        _check(_lib.darb_spmm_i8(self._h, _ptr(codes), _ptr(scales), po, pp, _dtype_code(X), B,
+                                 _ptr(X), ldx, _ptr(Y), ldy, _stream_ptr(stream)),
+               "darb_spmm_i8")
+        return Y
+
     # -- argument checks --------------------------------------------------------------
+    def _check_i8(self, codes, scales):
+        torch = _torch()
+        _check_format(codes, self.nnz, "codes", (torch.int8,))
+        _check_format(scales, self.M, "scales", (torch.float32,))
+
     def _check_values(self, values):
         torch = _torch()
         _check_format(values, self.nnz, "values", (torch.float32, torch.float16))

@@ -56,7 +56,7 @@ using namespace darb;
 
 extern "C" {
 
-int darb_version(void) { return 200; }
+int darb_version(void) { return 300; }
 
 const char *darb_strerror(int code) {
     switch (code) {
@@ -401,6 +401,55 @@ int darb_spmm_packed(const darb_plan *p, int wdtype, const void *values, const u
     if (rc) return rc;
     return launched(launch_spmm(*p, wdtype, values, nullptr, packed, xdtype, B, X, ldx, Y, ldy,
                                 static_cast<hipStream_t>(stream)), "spmm (packed) launch");
+}
+
+int darb_quantize_i8(const darb_plan *p, int wdtype, const void *values, int8_t *codes,
+                     float *scales, void *stream) {
+    clear_error();
+    int rc = check_uploaded(p);
+    if (rc) return rc;
+    if (!valid_dtype(wdtype)) return fail(DARB_E_DTYPE, "unknown weight dtype");
+    if (!values || !codes || !scales) return fail(DARB_E_INVALID, "NULL buffer");
+    return launched(launch_quantize_i8(*p, wdtype, values, codes, scales,
+                                       static_cast<hipStream_t>(stream)), "quantize launch");
+}
+
+// INT8 products: the offsets come from exactly one of `offsets` (bytes) and
+// `packed`; with offsets NULL, packed follows the packed products' rules.
+static int check_i8_product(const darb_plan *p, const int8_t *codes, const float *scales,
+                            const uint8_t *offsets, const uint32_t *packed, int xdtype) {
+    if (!valid_dtype(xdtype)) return fail(DARB_E_DTYPE, "unknown activation dtype");
+    if (!codes || !scales) return fail(DARB_E_INVALID, "NULL buffer");
+    if (offsets && packed) return fail(DARB_E_INVALID, "pass offsets or packed, not both");
+    return offsets ? DARB_OK : check_packed(p, packed);
+}
+
+int darb_spmv_i8(const darb_plan *p, const int8_t *codes, const float *scales,
+                 const uint8_t *offsets, const uint32_t *packed, int xdtype, const void *x,
+                 float *y, void *stream) {
+    clear_error();
+    int rc = check_uploaded(p);
+    if (rc) return rc;
+    rc = check_i8_product(p, codes, scales, offsets, packed, xdtype);
+    if (rc) return rc;
+    if (!x || !y) return fail(DARB_E_INVALID, "NULL buffer");
+    return launched(launch_spmv_i8(*p, codes, scales, offsets, packed, xdtype, x, y,
+                                   static_cast<hipStream_t>(stream)), "spmv (int8) launch");
+}
+
+int darb_spmm_i8(const darb_plan *p, const int8_t *codes, const float *scales,
+                 const uint8_t *offsets, const uint32_t *packed, int xdtype, int64_t B,
+                 const void *X, int64_t ldx, float *Y, int64_t ldy, void *stream) {
+    clear_error();
+    int rc = check_uploaded(p);
+    if (rc) return rc;
+    rc = check_i8_product(p, codes, scales, offsets, packed, xdtype);
+    if (rc) return rc;
+    if (!X || !Y) return fail(DARB_E_INVALID, "NULL buffer");
+    rc = check_batch(B, ldx, ldy);
+    if (rc) return rc;
+    return launched(launch_spmm_i8(*p, codes, scales, offsets, packed, xdtype, B, X, ldx, Y, ldy,
+                                   static_cast<hipStream_t>(stream)), "spmm (int8) launch");
 }
 
 int darb_prune_workspace(int64_t M, int64_t N, int wdtype, int64_t *bytes) {

@@ -75,6 +75,16 @@ hipError_t launch_spmv(const darb_plan &p, int wdtype, const void *values,
 hipError_t launch_spmm(const darb_plan &p, int wdtype, const void *values,
                        const uint8_t *offsets, const uint32_t *packed, int xdtype, int64_t B,
                        const void *X, int64_t ldx, float *Y, int64_t ldy, hipStream_t s);
+// INT8 values: per-row codes and scales, and the products on them (scales indexed
+// by original row, applied to each row's fp32 sum).
+hipError_t launch_quantize_i8(const darb_plan &p, int wdtype, const void *values, int8_t *codes,
+                              float *scales, hipStream_t s);
+hipError_t launch_spmv_i8(const darb_plan &p, const int8_t *codes, const float *scales,
+                          const uint8_t *offsets, const uint32_t *packed, int xdtype,
+                          const void *x, float *y, hipStream_t s);
+hipError_t launch_spmm_i8(const darb_plan &p, const int8_t *codes, const float *scales,
+                          const uint8_t *offsets, const uint32_t *packed, int xdtype, int64_t B,
+                          const void *X, int64_t ldx, float *Y, int64_t ldy, hipStream_t s);
 hipError_t launch_pack_offsets(const darb_plan &p, const uint8_t *offsets, uint32_t *packed,
                                hipStream_t s);
 hipError_t launch_unpack_offsets(const darb_plan &p, const uint32_t *packed, uint8_t *offsets,

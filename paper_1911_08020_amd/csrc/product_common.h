@@ -1,0 +1,1069 @@
+// DARB products on gfx950: y = W_darb x (SpMV) and Y = W_darb X (SpMM) -- the
+// kernels and their launch templates, instantiated by product.hip (fp32 and fp16
+// weights) and product_i8.hip (INT8 weights).
+//
+// Only retained weights are read (section 2), and each retained weight's
+// in-block offset selects the one activation it multiplies (section 3.2):
+//     y[r] = sum_k v[r,k] * x[k * b_r + off[r,k]].
+// The grouped layout makes every block-size group a dense [rows x nblk] array.
+// Every workgroup works inside one group, so the group's geometry is uniform:
+// it is read with scalar loads, and the per-lane work starts with the loads that
+// matter.  Loads are never placed under per-lane branches: addresses are clamped
+// into the buffer and the unused lanes' results are masked, so a wave issues all
+// of its loads back to back.
+//
+// SpMV: `lanes` lanes per row, 64 / lanes rows per wave; each lane holds up to
+// kVmax 16-byte vectors of values (plus their offset bytes) in registers.  The
+// workgroup stages x into LDS after issuing those loads, so HBM latency overlaps
+// the staging; the gathers then hit LDS.  A row's partial sums are combined by an
+// xor butterfly in a fixed order (deterministic) and written in original row order.
+//
+// SpMM: lanes map to batch columns (X is [N x B] row-major, so one weight's
+// activations X[c, :] are contiguous), CPL columns per lane with 16-byte loads, or
+// narrower ones for small batches so that a row still spreads over up to 16 lanes
+// and the launch over many waves.  Each wave loads its rows' (value, column)
+// pairs with coalesced loads and broadcasts them across a row's lanes register to
+// register (DPP, swizzle or readlane), gathering X rows kSpmmBatch at a time; the
+// next round's pairs load while this round gathers.  Up to 8 waves split a row group's weights
+// and their partial sums meet in LDS in a fixed order.
+//
+// Both products read the offsets either as one byte per retained weight or in the
+// bit-packed form of section 4.2 (log2 b bits each, packed_bits.h); the two forms
+// share every other step, so their results are bitwise identical.
+#pragma once
+#include <hip/hip_fp16.h>
+
+#include <type_traits>
+#include <utility>
+
+#include "darb_internal.h"
+#include "packed_bits.h"
+
+namespace darb {
+namespace {
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+template <typename T> __device__ __forceinline__ float to_f32(T v);
+template <> __device__ __forceinline__ float to_f32<float>(float v) { return v; }
+template <> __device__ __forceinline__ float to_f32<__half>(__half v) { return __half2float(v); }
+template <> __device__ __forceinline__ float to_f32<int8_t>(int8_t v) { return float(v); }
+
+// INT8 weights carry one fp32 scale per row, applied once to the row's sum.
+template <typename Tw> constexpr bool kScaled = std::is_same<Tw, int8_t>::value;
+
+__device__ __forceinline__ float half_bits_to_f32(uint32_t h) {
+    return __half2float(__ushort_as_half(uint16_t(h & 0xFFFFu)));
+}
+
+__device__ __forceinline__ int wave_uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
+
+// Uniform selection of a per-group table entry (compile-time indices only, so the
+// table stays in scalar registers).
+template <typename T>
+__device__ __forceinline__ T pick(const T (&a)[kMaxBins], int g) {
+    T r = a[0];
+#pragma unroll
+    for (int b = 1; b < kMaxBins; ++b) r = (b == g) ? a[b] : r;
+    return r;
+}
+
+// The block-size group that workgroup `tile` of a launch belongs to.
+__device__ __forceinline__ int block_group(const ProductSchedule &s, int tile) {
+    int g = 0;
+#pragma unroll
+    for (int b = 1; b < kMaxBins; ++b)
+        if (b < s.nbins && tile >= s.block_begin[b]) g = b;
+    return g;
+}
+
+__device__ __forceinline__ int block_begin_of(const ProductSchedule &s, int g) {
+    int r = s.block_begin[0];
+#pragma unroll
+    for (int b = 1; b < kMaxBins; ++b) r = (b == g) ? s.block_begin[b] : r;
+    return r;
+}
+
+// ---------------------------------------------------------------------------------
+// Offset sources.  A lane loads the indices of NV consecutive retained weights of a
+// group (group slots j .. j + NV - 1, j a multiple of NV) as `Raw`, keeps them in
+// registers while other loads are in flight, turns them into `Bits` when it needs
+// them and reads index q with field().
+// ---------------------------------------------------------------------------------
+
+struct GroupOffsets {
+    const uint8_t *u8;     // byte form: the group's first slot
+    PackedGroup pk;        // packed form
+};
+
+__device__ __forceinline__ GroupOffsets group_offsets(const void *offs, const BinTable &bins,
+                                                      int g) {
+    GroupOffsets go;
+    go.u8 = static_cast<const uint8_t *>(offs) + pick(bins.first_elem, g);
+    go.pk = packed_group(static_cast<const uint32_t *>(offs), pick(bins.first_word, g),
+                         pick(bins.log2b, g));
+    return go;
+}
+
+template <int NV> struct U8Vec;
+template <> struct U8Vec<1> { using T = uint8_t; };
+template <> struct U8Vec<2> { using T = uint16_t; };
+template <> struct U8Vec<4> { using T = uint32_t; };
+template <> struct U8Vec<8> { using T = u32x2; };
+template <> struct U8Vec<16> { using T = u32x4; };
+
+template <bool PK, int NV> struct Off;
+
+// one byte per weight: one NV-byte load (the caller guarantees its alignment)
+template <int NV> struct Off<false, NV> {
+    using Raw = typename U8Vec<NV>::T;
+    using Bits = Raw;
+    __device__ static Raw load(const GroupOffsets &go, int64_t j) {
+        return *reinterpret_cast<const Raw *>(go.u8 + j);
+    }
+    __device__ static Bits bits(const Raw &r, const GroupOffsets &) { return r; }
+    __device__ static int field(const Bits &b, int q, const GroupOffsets &) {
+        if constexpr (NV <= 4) return int((uint32_t(b) >> (8 * q)) & 0xFFu);
+        else return int((b[q >> 2] >> (8 * (q & 3))) & 0xFFu);
+    }
+};
+
+// packed, up to 4 indices (<= 28 bits): two words
+template <int NV> struct Off<true, NV> {
+    static_assert(NV <= 4, "wider vectors have their own specialisations");
+    using Raw = PackedWords2;
+    using Bits = uint32_t;
+    __device__ static Raw load(const GroupOffsets &go, int64_t j) { return packed_load2(go.pk, j); }
+    __device__ static Bits bits(const Raw &r, const GroupOffsets &) { return packed_bits32(r); }
+    __device__ static int field(Bits b, int q, const GroupOffsets &go) {
+        return packed_field(b, q, go.pk);
+    }
+};
+
+// packed, 8 indices (<= 56 bits): three words
+template <> struct Off<true, 8> {
+    using Raw = PackedWords3;
+    using Bits = uint64_t;
+    __device__ static Raw load(const GroupOffsets &go, int64_t j) { return packed_load3(go.pk, j); }
+    __device__ static Bits bits(const Raw &r, const GroupOffsets &) { return packed_bits64(r); }
+    __device__ static int field(Bits b, int q, const GroupOffsets &go) {
+        return packed_field(b, q, go.pk);
+    }
+};
+
+// packed, 16 indices: two 8-index windows (j is a multiple of 16, so both lie in
+// one run)
+template <> struct Off<true, 16> {
+    struct Raw { PackedWords3 lo, hi; };
+    struct Bits { uint64_t lo, hi; };
+    __device__ static Raw load(const GroupOffsets &go, int64_t j) {
+        return Raw{packed_load3(go.pk, j), packed_load3(go.pk, j + 8)};
+    }
+    __device__ static Bits bits(const Raw &r, const GroupOffsets &) {
+        return Bits{packed_bits64(r.lo), packed_bits64(r.hi)};
+    }
+    __device__ static int field(const Bits &b, int q, const GroupOffsets &go) {
+        return q < 8 ? packed_field(b.lo, q, go.pk) : packed_field(b.hi, q - 8, go.pk);
+    }
+};
+
+// ---------------------------------------------------------------------------------
+// SpMV
+// ---------------------------------------------------------------------------------
+
+constexpr int kSpmvThreads = 256;
+constexpr int kSpmvWaves = kSpmvThreads / kWave;
+constexpr int kVmax = 8;                         // vectors per lane per round
+constexpr int kLdsMaxFloats = 16384;             // x staged in LDS up to 64 KiB
+
+template <typename Tw> struct WVec;
+template <> struct WVec<float> {
+    static constexpr int VEC = 4;
+    using V = f32x4;        // 4 values, 16 bytes
+    __device__ static float get(const V &v, int i) { return v[i]; }
+};
+template <> struct WVec<__half> {
+    static constexpr int VEC = 8;
+    using V = u32x4;        // 8 fp16 values, 16 bytes
+    __device__ static float get(const V &v, int i) {
+        const uint32_t w = v[i >> 1];
+        return half_bits_to_f32((i & 1) ? (w >> 16) : w);
+    }
+};
+template <> struct WVec<int8_t> {
+    static constexpr int VEC = 8;
+    using V = u32x2;        // 8 INT8 codes, 8 bytes (with their 8 offset bytes: 16)
+    __device__ static float get(const V &v, int i) {
+        // sign-extend byte i & 3 of word i >> 2
+        return float(int32_t(v[i >> 2] << (24 - 8 * (i & 3))) >> 24);
+    }
+};
+
+// Copy x (N elements) into LDS as fp32: SB 16-byte loads per thread in flight
+// (addresses clamped, stores masked), then the scalar tail.
+template <typename Tx, int SB>
+__device__ __forceinline__ void stage_x(float *xs, const Tx *__restrict__ x, int N) {
+    constexpr int E = 16 / int(sizeof(Tx));
+    const bool aligned = (reinterpret_cast<uintptr_t>(x) & 15) == 0;
+    const int nv = aligned ? N / E : 0;
+    const u32x4 *x4 = reinterpret_cast<const u32x4 *>(x);
+    for (int base = 0; base < nv; base += SB * kSpmvThreads) {
+        u32x4 t[SB];
+#pragma unroll
+        for (int u = 0; u < SB; ++u) {
+            if (base + u * kSpmvThreads < nv) {          // wave-uniform: skip empty rounds
+                const int i = base + u * kSpmvThreads + int(threadIdx.x);
+                t[u] = x4[i < nv ? i : nv - 1];
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < SB; ++u) {
+            const int i = base + u * kSpmvThreads + int(threadIdx.x);
+            if (i < nv) {
+                if constexpr (sizeof(Tx) == 4) {
+                    *reinterpret_cast<u32x4 *>(xs + i * E) = t[u];
+                } else {
+#pragma unroll
+                    for (int h = 0; h < 4; ++h) {
+                        xs[i * E + 2 * h] = half_bits_to_f32(t[u][h]);
+                        xs[i * E + 2 * h + 1] = half_bits_to_f32(t[u][h] >> 16);
+                    }
+                }
+            }
+        }
+    }
+    for (int c = nv * E + int(threadIdx.x); c < N; c += kSpmvThreads) xs[c] = to_f32<Tx>(x[c]);
+}
+
+// fp32 x straight into LDS: each wave moves 1 KiB chunks with direct global-to-LDS
+// loads (lane i's 16 bytes land at chunk + 16 i), so no registers hold x on the way;
+// the rest (a partial chunk, a tail shorter than 16 bytes) goes through registers.
+// The caller waits for the loads and synchronises the workgroup.
+__device__ __forceinline__ void stage_x_direct(float *xs, const float *__restrict__ x, int N) {
+    typedef __attribute__((address_space(1))) const float *gptr;
+    typedef __attribute__((address_space(3))) void *lptr;
+    const int wave = wave_uniform(int(threadIdx.x) / kWave);
+    const int lane = int(threadIdx.x) & (kWave - 1);
+    const int chunks = N / (kWave * 4);
+    for (int j = wave; j < chunks; j += kSpmvWaves)
+        __builtin_amdgcn_global_load_lds((gptr)(x + (j * kWave + lane) * 4),
+                                         (lptr)(xs + j * kWave * 4), 16, 0, 0);
+    for (int c = chunks * kWave * 4 + int(threadIdx.x); c < N; c += kSpmvThreads) xs[c] = x[c];
+}
+
+template <typename Tw, typename Tx, bool LDS, int SB, bool PK>
+__global__ __launch_bounds__(kSpmvThreads) void spmv_kernel(
+    const Tw *__restrict__ values, const void *__restrict__ offs,
+    const Tx *__restrict__ x, float *__restrict__ y, const int32_t *__restrict__ perm,
+    int N, BinTable bins, ProductSchedule sch, const float *__restrict__ scales) {
+    using WV = WVec<Tw>;
+    constexpr int VEC = WV::VEC;
+    using OV = Off<PK, VEC>;
+    using OS = Off<PK, 1>;
+    extern __shared__ float xs[];
+
+    const int g = block_group(sch, int(blockIdx.x));
+    const int wave = wave_uniform(int(threadIdx.x) / kWave);
+    const int lane = int(threadIdx.x) & (kWave - 1);
+    const int lgL = pick(sch.log2_lanes, g);
+    const int L = 1 << lgL;
+    const int lb = pick(bins.log2b, g);
+    const int nblk = int(pick(bins.nblk, g));
+    const int64_t rows = pick(bins.rows, g);
+    const int64_t first_row = pick(bins.first_row, g);
+    const int64_t first_elem = pick(bins.first_elem, g);
+    const bool vec_path = pick(sch.vec, g) == VEC;
+
+    const int64_t tile = int64_t(int(blockIdx.x) - block_begin_of(sch, g)) * kSpmvWaves + wave;
+    const int64_t row = (tile << (6 - lgL)) + (lane >> lgL);
+    const bool row_ok = row < rows;
+    const int64_t row_c = row_ok ? row : rows - 1;
+    const int sub = lane & (L - 1);
+    const int64_t j0 = row_c * nblk;                     // the row's first slot in its group
+    const int64_t e0 = first_elem + j0;
+    const int nvec = vec_path ? nblk / VEC : nblk;
+    const GroupOffsets go = group_offsets(offs, bins, g);
+
+    // the destination row and the first round of this lane's vectors, issued
+    // before x is staged
+    const int32_t dest = perm[first_row + row_c];
+    const float scale = kScaled<Tw> ? scales[dest] : 1.0f;
+    typename WV::V wv[kVmax];
+    typename OV::Raw ov[kVmax];
+    const typename WV::V *vrow = reinterpret_cast<const typename WV::V *>(values + e0);
+    if (vec_path) {
+#pragma unroll
+        for (int t = 0; t < kVmax; ++t) {
+            if (t * L < nvec) {                          // wave-uniform
+                const int vi = sub + t * L;
+                const int vc = vi < nvec ? vi : nvec - 1;
+                wv[t] = __builtin_nontemporal_load(vrow + vc);
+                ov[t] = OV::load(go, j0 + int64_t(vc) * VEC);
+            }
+        }
+    }
+
+    if constexpr (LDS) {
+        if constexpr (SB == 0 && std::is_same<Tx, float>::value) {   // fp32 x, 16 B aligned
+            stage_x_direct(xs, x, N);
+            __builtin_amdgcn_s_waitcnt(0);                // the direct loads have landed
+        } else {
+            stage_x<Tx, SB>(xs, x, N);
+        }
+        __syncthreads();
+    }
+    auto xat = [&](int c) -> float {
+        // offsets from the encode always give c < N; the global path clamps anyway
+        // so a malformed offset cannot read outside x
+        if constexpr (LDS) return xs[c];
+        else return to_f32<Tx>(x[c < N ? c : N - 1]);
+    };
+
+    float acc = 0.0f;
+    if (vec_path) {
+        for (int base = 0;; base += L * kVmax) {
+#pragma unroll
+            for (int t = 0; t < kVmax; ++t) {
+                const int vi = base + sub + t * L;
+                if (vi < nvec) {
+                    const typename OV::Bits ob = OV::bits(ov[t], go);
+#pragma unroll
+                    for (int q = 0; q < VEC; ++q) {
+                        const int c = ((vi * VEC + q) << lb) + OV::field(ob, q, go);
+                        acc = fmaf(WV::get(wv[t], q), xat(c), acc);
+                    }
+                }
+            }
+            if (base + L * kVmax >= nvec) break;
+#pragma unroll
+            for (int t = 0; t < kVmax; ++t) {
+                if (base + L * kVmax + t * L < nvec) {   // wave-uniform
+                    const int vi = base + L * kVmax + sub + t * L;
+                    const int vc = vi < nvec ? vi : nvec - 1;
+                    wv[t] = __builtin_nontemporal_load(vrow + vc);
+                    ov[t] = OV::load(go, j0 + int64_t(vc) * VEC);
+                }
+            }
+        }
+    } else {
+        const Tw *vr = values + e0;
+        for (int k = sub; k < nblk; k += L) {
+            const int o = OS::field(OS::bits(OS::load(go, j0 + k), go), 0, go);
+            acc = fmaf(to_f32<Tw>(vr[k]), xat((k << lb) + o), acc);
+        }
+    }
+
+    for (int m = L >> 1; m >= 1; m >>= 1) acc += __shfl_xor(acc, m, kWave);
+    if (row_ok && sub == 0) y[dest] = kScaled<Tw> ? acc * scale : acc;
+}
+
+// ---------------------------------------------------------------------------------
+// SpMM
+// ---------------------------------------------------------------------------------
+
+constexpr int kSpmmThreads = 512;
+constexpr int kSpmmWaves = kSpmmThreads / kWave;
+constexpr int kSpmmBatch = 8;         // X rows in flight per lane (more waves beat deeper batches)
+constexpr int kRowLanes = 16;         // lanes per row that narrow columns aim at
+
+// CPL consecutive batch columns of one X row, loaded at once (16 bytes when CPL > 1).
+template <typename Tx, int CPL> struct XLoad;
+template <typename Tx> struct XLoad<Tx, 1> {
+    using V = Tx;
+    __device__ static V load(const Tx *p) { return *p; }
+    __device__ static float get(const V &v, int) { return to_f32<Tx>(v); }
+};
+template <> struct XLoad<float, 4> {
+    using V = f32x4;
+    __device__ static V load(const float *p) { return *reinterpret_cast<const f32x4 *>(p); }
+    __device__ static float get(const V &v, int i) { return v[i]; }
+};
+template <> struct XLoad<float, 2> {
+    using V = f32x2;
+    __device__ static V load(const float *p) { return *reinterpret_cast<const f32x2 *>(p); }
+    __device__ static float get(const V &v, int i) { return v[i]; }
+};
+template <> struct XLoad<__half, 2> {
+    using V = uint32_t;
+    __device__ static V load(const __half *p) { return *reinterpret_cast<const uint32_t *>(p); }
+    __device__ static float get(const V &v, int i) { return half_bits_to_f32(i ? v >> 16 : v); }
+};
+template <> struct XLoad<__half, 4> {
+    using V = u32x2;
+    __device__ static V load(const __half *p) { return *reinterpret_cast<const u32x2 *>(p); }
+    __device__ static float get(const V &v, int i) {
+        const uint32_t w = v[i >> 1];
+        return half_bits_to_f32((i & 1) ? (w >> 16) : w);
+    }
+};
+template <> struct XLoad<__half, 8> {
+    using V = u32x4;
+    __device__ static V load(const __half *p) { return *reinterpret_cast<const u32x4 *>(p); }
+    __device__ static float get(const V &v, int i) {
+        const uint32_t w = v[i >> 1];
+        return half_bits_to_f32((i & 1) ? (w >> 16) : w);
+    }
+};
+
+template <int Base, typename F, int... Is>
+__device__ __forceinline__ void static_for_impl(F &&f, std::integer_sequence<int, Is...>) {
+    (f(std::integral_constant<int, Base + Is>{}), ...);
+}
+// f(integral_constant<int, i>) for i = Base .. Base + Count - 1, unrolled at compile time
+template <int Base, int Count, typename F> __device__ __forceinline__ void static_for(F &&f) {
+    static_for_impl<Base>(f, std::make_integer_sequence<int, Count>{});
+}
+
+// Value of lane T of the caller's group of 2^LGL consecutive lanes, for every lane
+// of the group (T is a compile-time lane index inside the group).
+template <int LGL, int T> __device__ __forceinline__ int group_bcast(int v) {
+    if constexpr (LGL == 0) {
+        return v;
+    } else if constexpr (LGL == 1) {                      // DPP quad_perm [T, T, 2+T, 2+T]
+        return __builtin_amdgcn_update_dpp(0, v, T | (T << 2) | ((2 + T) << 4) | ((2 + T) << 6),
+                                           0xF, 0xF, false);
+    } else if constexpr (LGL == 2) {                      // DPP quad_perm [T, T, T, T]
+        return __builtin_amdgcn_update_dpp(0, v, T * 0x55, 0xF, 0xF, false);
+    } else if constexpr (LGL == 4) {                      // DPP row_newbcast:T (16-lane rows)
+        return __builtin_amdgcn_update_dpp(0, v, 0x150 + T, 0xF, 0xF, false);
+    } else if constexpr (LGL == 6) {                      // whole wave: through a scalar register
+        return __builtin_amdgcn_readlane(v, T);
+    } else {                                              // 8 or 32 lanes: ds_swizzle bitmask mode
+        constexpr int and_mask = 0x1F & ~((1 << LGL) - 1);
+        return __builtin_amdgcn_ds_swizzle(v, (T << 5) | and_mask);
+    }
+}
+
+// GM consecutive retained weights of a row (values and offsets) for one lane: one
+// vector load each when the bin is aligned for it, element loads otherwise.
+template <typename Tw, int GM, bool PK> struct PairLoad {
+    struct alignas(GM * sizeof(Tw)) VV { Tw e[GM]; };
+    using OV = Off<PK, GM>;
+    // the vector form as loaded, kept in registers while other loads are in flight
+    struct Raw { VV a; typename OV::Raw ob; };
+    // vec: the caller guarantees k % GM == 0, k + GM <= nblk and nblk % GM == 0 (so
+    // the group slot j0 + k is a multiple of GM); otherwise every element index is
+    // clamped into the row [0, nblk).  j0 is the row's first slot in its group.
+    __device__ static Raw issue(const Tw *vr, const GroupOffsets &go, int64_t j0, int k) {
+        return Raw{*reinterpret_cast<const VV *>(vr + k), OV::load(go, j0 + k)};
+    }
+    __device__ static void decode(const Raw &r, const GroupOffsets &go, float (&v)[GM],
+                                  int (&o)[GM]) {
+        const typename OV::Bits b = OV::bits(r.ob, go);
+#pragma unroll
+        for (int i = 0; i < GM; ++i) {
+            v[i] = to_f32<Tw>(r.a.e[i]);
+            o[i] = OV::field(b, i, go);
+        }
+    }
+    __device__ static void load(const Tw *vr, const GroupOffsets &go, int64_t j0, int k,
+                                int nblk, bool vec, float (&v)[GM], int (&o)[GM]) {
+        if (vec) {
+            decode(issue(vr, go, j0, k), go, v, o);
+        } else {
+            using OS = Off<PK, 1>;
+#pragma unroll
+            for (int i = 0; i < GM; ++i) {
+                const int kk = k + i < nblk ? k + i : nblk - 1;
+                v[i] = to_f32<Tw>(vr[kk]);
+                o[i] = OS::field(OS::bits(OS::load(go, j0 + kk), go), 0, go);
+            }
+        }
+    }
+};
+
+// One workgroup-sized tile of the SpMM: lanes map to batch columns (CPL per lane,
+// 2^LGL lanes per matrix row, 64 >> LGL rows per wave).  A wave owns a contiguous
+// share [kbeg, kend) of its rows' weights (KS waves split a row group).  The lanes
+// of a row load S = max(2^LGL, 16) of the row's (value, column) pairs per step, one
+// pair per lane and group, straight from HBM with coalesced loads, then broadcast
+// each pair to the row's lanes with a register-to-register exchange and gather its
+// X row; kSpmmBatch gathers are in flight per lane.  With aligned pairs the loads
+// are software pipelined: a round's pairs are issued right after the previous
+// round's last gathers, so their HBM latency overlaps those gathers.  Partial sums
+// of the KS waves meet in LDS (`part`, kSpmmThreads * CPL floats) in a fixed order.
+// The finished rows go to
+//     epi(row_ok, col_ok, original row, first column, acc[CPL], lane in row),
+// called by every lane of the waves that hold finished rows (wave-uniform), so an
+// epilogue may exchange values between the lanes of a row.
+template <typename Tw, typename Tx, int CPL, int LGL, bool PK, typename Epi>
+__device__ __forceinline__ void spmm_tile(
+    int tile, const Tw *__restrict__ values, const void *__restrict__ offs,
+    const Tx *__restrict__ X, int64_t ldx, int64_t B, const int32_t *__restrict__ perm, int N,
+    const BinTable &bins, const ProductSchedule &sch, float *part, Epi &&epi) {
+    using XL = XLoad<Tx, CPL>;
+    constexpr int L = 1 << LGL;
+    constexpr int R = kWave >> LGL;                       // rows per wave
+    constexpr int GM = L >= 16 ? 1 : 16 / L;              // pair groups per lane per step
+    constexpr int S = L * GM;                             // weights per row per step
+    // steps whose pairs load together: four for rows of 16 or fewer lanes (measured
+    // 11 % faster at 16 lanes, batch 64), two when the offsets are packed (their word
+    // windows take more registers); a 64-lane row's step already spans 64 weights
+    constexpr int DEPTH = (L >= kWave || GM >= 4) ? 1 : (PK ? 2 : 4) / GM;
+    constexpr int T = DEPTH * S;                          // weights per row per round
+    constexpr int NB = kSpmmBatch;                        // X-row gathers in flight per lane
+    static_assert(S % NB == 0, "a gather batch lies inside one step");
+
+    const int g = block_group(sch, tile);
+    const int wave = wave_uniform(int(threadIdx.x) / kWave);
+    const int lane = int(threadIdx.x) & (kWave - 1);
+    const int KS = pick(sch.ksplit, g);
+    const int rows_pb = R * (kSpmmWaves / KS);
+    const int lb = pick(bins.log2b, g);
+    const int nblk = int(pick(bins.nblk, g));
+    const int64_t rows = pick(bins.rows, g);
+    const int64_t first_row = pick(bins.first_row, g);
+    const int64_t first_elem = pick(bins.first_elem, g);
+
+    // column slab outermost: the workgroups in flight together share one slab of X,
+    // which stays in L2 even when all of X does not
+    const int local = tile - block_begin_of(sch, g);
+    const int row_blks = int((rows + rows_pb - 1) / rows_pb);
+    const int slab = local / row_blks;
+    const int row_blk = local - slab * row_blks;
+    const int64_t row0 = int64_t(row_blk) * rows_pb;
+    const int rows_here = int(rows - row0 < rows_pb ? rows - row0 : rows_pb);
+
+    const int rg = wave / KS, ks = wave - (wave / KS) * KS;
+    const int rl = rg * R + (lane >> LGL);                // row of this lane in the block
+    const bool row_ok = rl < rows_here;
+    const int sub = lane & (L - 1);
+    const int64_t col0 = (int64_t(slab) * L + sub) * CPL;
+    const bool col_ok = col0 < B;                         // CPL > 1 only when CPL divides B
+    const int64_t col_c = col_ok ? col0 : 0;
+    // each wave's share is a multiple of 16 weights (of GM, so a lane's GM-vector of
+    // weights is either entirely inside [kbeg, kend) or entirely outside); the split
+    // points do not depend on the lanes per row, so neither do the sums
+    const int share = (((nblk + KS - 1) / KS) + 15) / 16 * 16;
+    const int kbeg = ks * share;
+    const int kend = kbeg + share < nblk ? kbeg + share : nblk;
+    const int64_t j0 = (row0 + (row_ok ? rl : 0)) * nblk;   // the row's first slot in its group
+    const Tw *vr = values + first_elem + j0;
+    const GroupOffsets go = group_offsets(offs, bins, g);
+
+    float acc[CPL];
+#pragma unroll
+    for (int q = 0; q < CPL; ++q) acc[q] = 0.0f;
+
+    const bool vec_pairs = pick(sch.vec, g) != 0;
+    using PL = PairLoad<Tw, GM, PK>;
+    // a round's pairs (DEPTH steps) as values and clamped columns; -1 marks no weight
+    auto settle = [&](int k0, int st, const float (&v)[GM], const int (&o)[GM],
+                      float (&vl)[DEPTH][GM], int (&cl)[DEPTH][GM]) {
+        const int k = k0 + st * S + sub * GM;
+        const bool ok = row_ok && k < kend;
+#pragma unroll
+        for (int gi = 0; gi < GM; ++gi) {
+            const bool okg = ok && k + gi < kend;         // element test for the scalar path
+            vl[st][gi] = okg ? v[gi] : 0.0f;
+            const int c = ((k + gi) << lb) + o[gi];
+            cl[st][gi] = okg ? (c < N ? c : N - 1) : -1;   // the encode gives c < N
+        }
+    };
+    // vector pair loads of the round at k0 (lanes past the share or the rows load a
+    // valid slot of their row block and are masked when settled)
+    auto issue_round = [&](int k0, typename PL::Raw (&raw)[DEPTH]) {
+#pragma unroll
+        for (int st = 0; st < DEPTH; ++st) {
+            const int k = k0 + st * S + sub * GM;
+            raw[st] = PL::issue(vr, go, j0, row_ok && k < kend ? k : kbeg);
+        }
+    };
+    // gathers of one round (DEPTH steps of S weights), NB X rows in flight per lane;
+    // `after` runs right after the round's last gathers are issued (the next round's
+    // pair loads go there, so they overlap these gathers without delaying their use)
+    auto gather_round = [&](int k0, const float (&vl)[DEPTH][GM], const int (&cl)[DEPTH][GM],
+                            auto &&after) {
+        static_for<0, T / NB>([&](auto bc) {
+            constexpr int b0 = decltype(bc)::value * NB;
+            if (k0 + (b0 / S) * S >= kend) return;         // wave-uniform: past the share
+            float vv[NB];
+            int cc[NB];
+            typename XL::V xv[NB];
+            static_for<0, NB>([&](auto uc) {
+                constexpr int f = b0 + decltype(uc)::value;   // weight k0 + f of the round
+                constexpr int st = f / S, fs = f % S;
+                vv[f - b0] = __builtin_bit_cast(
+                    float, group_bcast<LGL, fs / GM>(__builtin_bit_cast(int, vl[st][fs % GM])));
+                cc[f - b0] = group_bcast<LGL, fs / GM>(cl[st][fs % GM]);
+                const int64_t c = cc[f - b0] >= 0 ? cc[f - b0] : 0;
+                xv[f - b0] = XL::load(X + c * ldx + col_c);
+            });
+            if constexpr (b0 + NB == T) after();
+#pragma unroll
+            for (int u = 0; u < NB; ++u) {
+                if (cc[u] >= 0 && col_ok) {
+#pragma unroll
+                    for (int q = 0; q < CPL; ++q)
+                        acc[q] = fmaf(vv[u], XL::get(xv[u], q), acc[q]);
+                }
+            }
+        });
+    };
+
+    if (vec_pairs) {
+        // software pipelined: the pairs of round i + 1 load while round i gathers
+        typename PL::Raw raw[DEPTH];
+        if (kbeg < kend) issue_round(kbeg, raw);          // wave-uniform
+        for (int k0 = kbeg; k0 < kend; k0 += DEPTH * S) {
+            float vl[DEPTH][GM];
+            int cl[DEPTH][GM];
+#pragma unroll
+            for (int st = 0; st < DEPTH; ++st) {
+                float v[GM];
+                int o[GM];
+                PL::decode(raw[st], go, v, o);
+                settle(k0, st, v, o, vl, cl);
+            }
+            const int k1 = k0 + DEPTH * S;
+            gather_round(k0, vl, cl, [&] {
+                if (k1 < kend) issue_round(k1, raw);      // wave-uniform
+            });
+        }
+    } else {
+        for (int k0 = kbeg; k0 < kend; k0 += DEPTH * S) {
+            float vl[DEPTH][GM];
+            int cl[DEPTH][GM];
+#pragma unroll
+            for (int st = 0; st < DEPTH; ++st) {
+                const int k = k0 + st * S + sub * GM;
+                float v[GM];
+                int o[GM];
+                PL::load(vr, go, j0, row_ok && k < kend ? k : kbeg, nblk, false, v, o);
+                settle(k0, st, v, o, vl, cl);
+            }
+            gather_round(k0, vl, cl, [] {});
+        }
+    }
+
+    // combine the KS partial sums of each row group in a fixed order
+    if (KS > 1) {
+#pragma unroll
+        for (int q = 0; q < CPL; ++q) part[(wave * kWave + lane) * CPL + q] = acc[q];
+        __syncthreads();
+        if (ks == 0) {
+            for (int s2 = 1; s2 < KS; ++s2) {
+#pragma unroll
+                for (int q = 0; q < CPL; ++q)
+                    acc[q] += part[((wave + s2) * kWave + lane) * CPL + q];
+            }
+        }
+    }
+    if (ks == 0) epi(row_ok, col_ok, row_ok ? perm[first_row + row0 + rl] : 0, col0, acc, sub);
+}
+
+template <typename Tw, typename Tx, int CPL, int LGL, bool PK>
+__global__ __launch_bounds__(kSpmmThreads) void spmm_kernel(
+    const Tw *__restrict__ values, const void *__restrict__ offs,
+    const Tx *__restrict__ X, int64_t ldx, int64_t B, float *__restrict__ Y, int64_t ldy,
+    const int32_t *__restrict__ perm, int N, BinTable bins, ProductSchedule sch,
+    const float *__restrict__ scales) {
+    __shared__ float part[kSpmmThreads * CPL];
+    spmm_tile<Tw, Tx, CPL, LGL, PK>(
+        int(blockIdx.x), values, offs, X, ldx, B, perm, N, bins, sch, part,
+        [&](bool row_ok, bool col_ok, int32_t orig, int64_t col0, const float (&acc)[CPL], int) {
+            if (row_ok && col_ok) {
+                const float sc = kScaled<Tw> ? scales[orig] : 1.0f;
+                float *yrow = Y + int64_t(orig) * ldy + col0;
+#pragma unroll
+                for (int q = 0; q < CPL; ++q) yrow[q] = kScaled<Tw> ? acc[q] * sc : acc[q];
+            }
+        });
+}
+
+// ---------------------------------------------------------------------------------
+// SpMM for short rows of X and many batch columns (the recurrent workload's input
+// products: N = 1024, B = 6400).  A workgroup takes one slab of SC = 4L batch
+// columns, copies X[:, slab] (N x SC fp32, <= 128 KiB) into LDS once, then runs
+// every row of every group against it -- the X-row gathers hit LDS instead of L2.
+// The format is read by every workgroup, from L2.  One lane group of L lanes per
+// row, S weights per step, DEPTH steps of pairs per load round.
+// ---------------------------------------------------------------------------------
+
+constexpr int kXldsThreads = 1024;
+constexpr int kXldsWaves = kXldsThreads / kWave;
+constexpr int kXldsFloats = 32768;                  // 128 KiB of LDS
+constexpr int kXldsStep = 16;                       // weights per row per step
+constexpr int kXldsBatch = 16;                      // LDS gathers in flight per lane
+
+// 16 consecutive retained values of one row, loaded as 16-byte vectors.
+template <typename Tw> struct Step16;
+template <> struct Step16<float> {
+    f32x4 v[4];
+    __device__ static Step16 load(const float *p) {
+        Step16 s;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) s.v[i] = reinterpret_cast<const f32x4 *>(p)[i];
+        return s;
+    }
+    __device__ float get(int i) const { return v[i >> 2][i & 3]; }
+};
+template <> struct Step16<__half> {
+    u32x4 v[2];
+    __device__ static Step16 load(const __half *p) {
+        Step16 s;
+#pragma unroll
+        for (int i = 0; i < 2; ++i) s.v[i] = reinterpret_cast<const u32x4 *>(p)[i];
+        return s;
+    }
+    __device__ float get(int i) const {
+        const uint32_t w = v[i >> 3][(i >> 1) & 3];
+        return half_bits_to_f32((i & 1) ? (w >> 16) : w);
+    }
+};
+
+template <typename Tw, int LGL>
+__global__ __launch_bounds__(kXldsThreads) void spmm_xlds_kernel(
+    const Tw *__restrict__ values, const uint8_t *__restrict__ offsets,
+    const float *__restrict__ X, int64_t ldx, int64_t B, float *__restrict__ Y, int64_t ldy,
+    const int32_t *__restrict__ perm, int N, BinTable bins, ProductSchedule sch) {
+    constexpr int L = 1 << LGL;
+    constexpr int R = kWave >> LGL;
+    constexpr int SC = 4 * L;                           // slab columns
+    constexpr int kStage = 8;                           // 16-byte staging loads in flight
+    __shared__ float xs[kXldsFloats];
+    using XL = XLoad<float, 4>;
+
+    const int64_t colbase = int64_t(blockIdx.x) * SC;
+    // X[:, slab] -> xs[c * SC + j]; columns past B read as zero (4 divides B)
+    {
+        constexpr int per_row = SC / 4;
+        const int items = N * per_row;
+        for (int base = 0; base < items; base += kStage * kXldsThreads) {
+            f32x4 v[kStage];
+            bool in[kStage];
+#pragma unroll
+            for (int u = 0; u < kStage; ++u) {
+                const int i = base + u * kXldsThreads + int(threadIdx.x);
+                const int ic = i < items ? i : items - 1;
+                const int c = ic / per_row, q = ic - c * per_row;
+                const int64_t col = colbase + int64_t(q) * 4;
+                in[u] = i < items && col < B;
+                v[u] = XL::load(X + int64_t(c) * ldx + (col < B ? col : 0));
+            }
+#pragma unroll
+            for (int u = 0; u < kStage; ++u) {
+                const int i = base + u * kXldsThreads + int(threadIdx.x);
+                if (i < items) {
+                    const f32x4 z = {0.0f, 0.0f, 0.0f, 0.0f};
+                    *reinterpret_cast<f32x4 *>(xs + i * 4) = in[u] ? v[u] : z;
+                }
+            }
+        }
+    }
+    __syncthreads();
+
+    const int wave = wave_uniform(int(threadIdx.x) / kWave);
+    const int lane = int(threadIdx.x) & (kWave - 1);
+    const int sub = lane & (L - 1);
+    const int64_t col0 = colbase + int64_t(sub) * 4;
+    const bool col_ok = col0 < B;
+    const int xoff = sub * 4;
+    for (int g = 0; g < sch.nbins; ++g) {                // uniform
+        const int lb = pick(bins.log2b, g);
+        const int nblk = int(pick(bins.nblk, g));        // a multiple of kXldsStep
+        const int64_t rows = pick(bins.rows, g);
+        const int64_t first_row = pick(bins.first_row, g);
+        const int64_t first_elem = pick(bins.first_elem, g);
+        for (int64_t p0 = 0; p0 < rows; p0 += int64_t(kXldsWaves) * R) {
+            const int64_t rl = p0 + wave * R + (lane >> LGL);
+            const bool row_ok = rl < rows;
+            const int64_t e0 = first_elem + (row_ok ? rl : 0) * nblk;   // 16-aligned
+            float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+            // every lane of the row loads the step's 16 (value, offset) pairs itself
+            // (equal addresses within one load merge), so no lane exchange is needed;
+            // the next step's pairs load while this step gathers
+            Step16<Tw> w = Step16<Tw>::load(values + e0);
+            u32x4 ob = *reinterpret_cast<const u32x4 *>(offsets + e0);
+            for (int k0 = 0; k0 < nblk; k0 += kXldsStep) {
+                const int kn = k0 + kXldsStep < nblk ? k0 + kXldsStep : k0;
+                const Step16<Tw> w_next = Step16<Tw>::load(values + e0 + kn);
+                const u32x4 ob_next = *reinterpret_cast<const u32x4 *>(offsets + e0 + kn);
+                static_for<0, kXldsStep / kXldsBatch>([&](auto bc) {
+                    constexpr int b0 = decltype(bc)::value * kXldsBatch;
+                    f32x4 xv[kXldsBatch];
+                    static_for<0, kXldsBatch>([&](auto uc) {
+                        constexpr int f = b0 + decltype(uc)::value;
+                        const int o = int((ob[f >> 2] >> (8 * (f & 3))) & 0xFFu);
+                        int c = ((k0 + f) << lb) + o;
+                        c = c < N ? c : N - 1;                // the encode gives c < N
+                        xv[f - b0] = *reinterpret_cast<const f32x4 *>(xs + c * SC + xoff);
+                    });
+#pragma unroll
+                    for (int u = 0; u < kXldsBatch; ++u) {
+                        const float vw = w.get(b0 + u);
+#pragma unroll
+                        for (int q = 0; q < 4; ++q) acc[q] = fmaf(vw, xv[u][q], acc[q]);
+                    }
+                });
+                w = w_next;
+                ob = ob_next;
+            }
+            if (row_ok && col_ok) {
+                float *yrow = Y + int64_t(perm[first_row + rl]) * ldy + col0;
+#pragma unroll
+                for (int q = 0; q < 4; ++q) yrow[q] = acc[q];
+            }
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------------
+// host-side schedules and launches
+// ---------------------------------------------------------------------------------
+
+inline int ilog2_ceil(int64_t v) {
+    int l = 0;
+    while ((int64_t(1) << l) < v) ++l;
+    return l;
+}
+
+// The offsets argument of the kernels: the byte form, or the packed words.  A plan
+// without packed words has b = 1 everywhere; the kernels then still load one word
+// (and mask it to nothing), so they get the plan's row order, >= 4 readable bytes.
+inline const void *offset_source(const darb_plan &p, const uint8_t *offsets,
+                                 const uint32_t *packed) {
+    if (offsets) return offsets;
+    return p.packed_words > 0 ? static_cast<const void *>(packed)
+                              : static_cast<const void *>(p.d_perm);
+}
+
+// Byte offsets are loaded VEC at a time, so their address must be aligned for it;
+// packed offsets are loaded as whole words at any weight index.
+inline bool offsets_aligned(const uint8_t *offsets, int vec) {
+    return !offsets || reinterpret_cast<uintptr_t>(offsets) % vec == 0;
+}
+
+template <typename Tw>
+bool spmv_schedule(const darb_plan &p, const void *values, const uint8_t *offsets,
+                   ProductSchedule &s) {
+    constexpr int VEC = WVec<Tw>::VEC;
+    s = ProductSchedule{};
+    s.nbins = p.bins.nbins;
+    s.col_slabs = 1;
+    const bool ptr_ok =
+        (reinterpret_cast<uintptr_t>(values) % sizeof(typename WVec<Tw>::V) == 0) &&
+        offsets_aligned(offsets, VEC);
+    int64_t blocks = 0;
+    for (int g = 0; g < s.nbins; ++g) {
+        const int64_t nblk = p.bins.nblk[g];
+        const bool vec = ptr_ok && nblk % VEC == 0 && p.bins.first_elem[g] % VEC == 0;
+        s.vec[g] = vec ? VEC : 1;
+        const int64_t nvec = vec ? nblk / VEC : nblk;
+        int lgL = 0;     // fewest lanes per row that keep each lane within kVmax vectors
+        while (lgL < 6 && ((nvec + (int64_t(1) << lgL) - 1) >> lgL) > kVmax) ++lgL;
+        s.log2_lanes[g] = lgL;
+        s.block_begin[g] = int32_t(blocks);
+        const int64_t rows_per_wave = int64_t(kWave) >> lgL;
+        const int64_t tiles = (p.bins.rows[g] + rows_per_wave - 1) / rows_per_wave;
+        blocks += (tiles + kSpmvWaves - 1) / kSpmvWaves;
+        if (blocks > 0x7FFFFFFF) return false;
+    }
+    s.block_begin[s.nbins] = int32_t(blocks);
+    return true;
+}
+
+template <typename Tw, typename Tx, bool PK>
+hipError_t launch_spmv_t(const darb_plan &p, const void *values, const uint8_t *offsets,
+                         const uint32_t *packed, const void *x, float *y, const float *scales,
+                         hipStream_t st) {
+    ProductSchedule s;
+    if (!spmv_schedule<Tw>(p, values, offsets, s)) return hipErrorInvalidConfiguration;
+    const int blocks = s.block_begin[s.nbins];
+    if (blocks == 0) return hipSuccess;
+    const Tw *v = static_cast<const Tw *>(values);
+    const void *offs = offset_source(p, offsets, packed);
+    const Tx *xx = static_cast<const Tx *>(x);
+    const int N = int(p.N);
+    if (p.N <= kLdsMaxFloats) {
+        const size_t lds = size_t(p.N) * sizeof(float);
+        const int64_t nv = p.N / (16 / int64_t(sizeof(Tx)));
+        const int64_t per_thread = (nv + kSpmvThreads - 1) / kSpmvThreads;
+#define DARB_SPMV_LDS(SB)                                                                    \
+    hipLaunchKernelGGL((spmv_kernel<Tw, Tx, true, SB, PK>), dim3(blocks), dim3(kSpmvThreads), \
+                       lds, st, v, offs, xx, y, p.d_perm, N, p.bins, s, scales)
+        bool direct = false;
+        if constexpr (std::is_same<Tx, float>::value) {
+            direct = reinterpret_cast<uintptr_t>(x) % 16 == 0;
+            if (direct) DARB_SPMV_LDS(0);
+        }
+        if (direct) {
+        } else if (per_thread <= 1) DARB_SPMV_LDS(1);
+        else if (per_thread <= 2) DARB_SPMV_LDS(2);
+        else if (per_thread <= 4) DARB_SPMV_LDS(4);
+        else if (per_thread <= 8) DARB_SPMV_LDS(8);
+        else DARB_SPMV_LDS(16);
+#undef DARB_SPMV_LDS
+    } else {
+        hipLaunchKernelGGL((spmv_kernel<Tw, Tx, false, 1, PK>), dim3(blocks), dim3(kSpmvThreads),
+                           0, st, v, offs, xx, y, p.d_perm, N, p.bins, s, scales);
+    }
+    return hipGetLastError();
+}
+
+template <typename Tw, typename Tx>
+hipError_t launch_spmv_form(const darb_plan &p, const void *values, const uint8_t *offsets,
+                            const uint32_t *packed, const void *x, float *y, const float *scales,
+                            hipStream_t st) {
+    if (offsets)
+        return launch_spmv_t<Tw, Tx, false>(p, values, offsets, nullptr, x, y, scales, st);
+    return launch_spmv_t<Tw, Tx, true>(p, values, nullptr, packed, x, y, scales, st);
+}
+
+inline bool spmm_schedule(const darb_plan &p, int64_t B, int cpl, size_t wbytes,
+                          const void *values, const uint8_t *offsets, ProductSchedule &s) {
+    s = ProductSchedule{};
+    s.nbins = p.bins.nbins;
+    const int64_t lanes = (B + cpl - 1) / cpl;        // lanes needed for all columns
+    const int lgL = lanes >= kWave ? 6 : ilog2_ceil(lanes);
+    const int64_t slabs = (lanes + (int64_t(1) << lgL) - 1) >> lgL;
+    if (slabs > 0x7FFFFFFF) return false;
+    s.col_slabs = int32_t(slabs);
+    const int R = kWave >> lgL;
+    int64_t blocks = 0;
+    for (int g = 0; g < s.nbins; ++g) {
+        const int64_t nblk = p.bins.nblk[g];
+        // split a row group's weights over up to 8 waves, >= ~16 weights per wave: many
+        // small workgroups keep every CU's share of the gathers even
+        int lgKS = ilog2_ceil((nblk + 15) / 16);
+        if (lgKS > 3) lgKS = 3;
+        const int KS = 1 << lgKS;
+        const int rows_pb = R * (kSpmmWaves / KS);
+        s.log2_lanes[g] = lgL;
+        s.ksplit[g] = KS;
+        // pairs load as GM-element vectors when every lane's run is aligned for it
+        const int64_t GM = lgL >= 4 ? 1 : (16 >> lgL);
+        s.vec[g] = (GM > 1 && nblk % GM == 0 && p.bins.first_elem[g] % GM == 0 &&
+                    reinterpret_cast<uintptr_t>(values) % (GM * wbytes) == 0 &&
+                    offsets_aligned(offsets, int(GM))) ? 1 : 0;
+        s.block_begin[g] = int32_t(blocks);
+        blocks += (p.bins.rows[g] + rows_pb - 1) / rows_pb * slabs;
+        if (blocks > 0x7FFFFFFF) return false;
+    }
+    s.block_begin[s.nbins] = int32_t(blocks);
+    return true;
+}
+
+template <typename Tw, typename Tx, int CPL, bool PK>
+hipError_t launch_spmm_cpl(const darb_plan &p, const ProductSchedule &s, const Tw *v,
+                           const void *offs, int64_t B, const Tx *x, int64_t ldx, float *Y,
+                           int64_t ldy, const float *scales, hipStream_t st) {
+    const int blocks = s.block_begin[s.nbins];
+    const int N = int(p.N);
+    const int lgl = s.log2_lanes[0];
+    // the widths between one column and 16 bytes are chosen only for rows of more
+    // than 8 lanes, so only those kernels exist
+    constexpr bool kEvery = CPL == 1 || CPL * int(sizeof(Tx)) == 16;
+    if (!kEvery && lgl < 4) return hipErrorInvalidConfiguration;
+#define DARB_SPMM(LGL)                                                                    \
+    hipLaunchKernelGGL((spmm_kernel<Tw, Tx, CPL, LGL, PK>), dim3(blocks), dim3(kSpmmThreads), \
+                       0, st, v, offs, x, ldx, B, Y, ldy, p.d_perm, N, p.bins, s, scales)
+    switch (lgl) {
+        case 0: if constexpr (kEvery) DARB_SPMM(0); break;
+        case 1: if constexpr (kEvery) DARB_SPMM(1); break;
+        case 2: if constexpr (kEvery) DARB_SPMM(2); break;
+        case 3: if constexpr (kEvery) DARB_SPMM(3); break;
+        case 4: DARB_SPMM(4); break;
+        case 5: DARB_SPMM(5); break;
+        default: DARB_SPMM(6); break;
+    }
+#undef DARB_SPMM
+    return hipGetLastError();
+}
+
+// Lanes per row of the LDS-slab SpMM (slab = 4 * lanes columns), or -1 when it does
+// not apply: fp32 X with 16-byte rows, a slab of >= 32 columns whose N rows fit in
+// LDS, and enough slabs (>= 128) to give every CU a workgroup.
+inline int xlds_lgl(const darb_plan &p, int64_t B) {
+    for (int lgl = 4; lgl >= 3; --lgl) {
+        const int64_t sc = int64_t(4) << lgl;
+        if (p.N * sc <= kXldsFloats && (B + sc - 1) / sc >= 128) return lgl;
+    }
+    return -1;
+}
+
+template <typename Tw, typename Tx, bool PK>
+hipError_t launch_spmm_t(const darb_plan &p, const void *values, const uint8_t *offsets,
+                         const uint32_t *packed, int64_t B, const void *X, int64_t ldx, float *Y,
+                         int64_t ldy, const float *scales, hipStream_t st) {
+    constexpr int CPL = 16 / int(sizeof(Tx));
+    if constexpr (std::is_same<Tx, float>::value && !PK && !kScaled<Tw>) {
+        const bool vec = (reinterpret_cast<uintptr_t>(X) % 16 == 0) &&
+                         ((ldx * int64_t(sizeof(Tx))) % 16 == 0) && (B % CPL == 0);
+        int lgl = vec ? xlds_lgl(p, B) : -1;
+        // every row's steps of 16 pairs load as 16-byte vectors
+        bool aligned16 = reinterpret_cast<uintptr_t>(values) % (kXldsStep * sizeof(Tw)) == 0 &&
+                         offsets_aligned(offsets, kXldsStep);
+        for (int g = 0; g < p.bins.nbins; ++g)
+            aligned16 = aligned16 && p.bins.nblk[g] % kXldsStep == 0 &&
+                        p.bins.first_elem[g] % kXldsStep == 0;
+        if (!aligned16) lgl = -1;
+        if (lgl >= 0) {
+            ProductSchedule s;
+            if (!spmm_schedule(p, B, CPL, sizeof(Tw), values, offsets, s))
+                return hipErrorInvalidConfiguration;
+            const int64_t slabs = (B + (int64_t(4) << lgl) - 1) / (int64_t(4) << lgl);
+            if (slabs > 0x7FFFFFFF) return hipErrorInvalidConfiguration;
+            const Tw *v = static_cast<const Tw *>(values);
+            const float *x = static_cast<const float *>(X);
+            if (lgl == 4)
+                hipLaunchKernelGGL((spmm_xlds_kernel<Tw, 4>), dim3(unsigned(slabs)),
+                                   dim3(kXldsThreads), 0, st, v, offsets, x, ldx, B, Y, ldy,
+                                   p.d_perm, int(p.N), p.bins, s);
+            else
+                hipLaunchKernelGGL((spmm_xlds_kernel<Tw, 3>), dim3(unsigned(slabs)),
+                                   dim3(kXldsThreads), 0, st, v, offsets, x, ldx, B, Y, ldy,
+                                   p.d_perm, int(p.N), p.bins, s);
+            return hipGetLastError();
+        }
+    }
+    // columns per lane: 16 bytes of X when that leaves a row at least 5 lanes (a
+    // group of 8); for smaller batches the fewest columns that keep a row within 16
+    // lanes, so the launch still has many waves.  The width must divide B and keep
+    // the loads aligned.  (Measured: 16-byte loads on 8 lanes beat 8-byte loads on 16;
+    // rows of 2 or 4 lanes leave too few waves.)
+    auto fits = [&](int c) {
+        const int64_t bytes = int64_t(c) * int64_t(sizeof(Tx));
+        return B % c == 0 && reinterpret_cast<uintptr_t>(X) % bytes == 0 &&
+               (ldx * int64_t(sizeof(Tx))) % bytes == 0;
+    };
+    int cpl = 1;
+    if ((B + CPL - 1) / CPL > 4 && fits(CPL)) {
+        cpl = CPL;
+    } else {
+        while (cpl < CPL && (B + cpl - 1) / cpl > kRowLanes && fits(2 * cpl)) cpl *= 2;
+    }
+    ProductSchedule s;
+    if (!spmm_schedule(p, B, cpl, sizeof(Tw), values, offsets, s))
+        return hipErrorInvalidConfiguration;
+    if (s.block_begin[s.nbins] == 0) return hipSuccess;
+    const Tw *v = static_cast<const Tw *>(values);
+    const void *offs = offset_source(p, offsets, packed);
+    const Tx *x = static_cast<const Tx *>(X);
+    if (cpl == 1)
+        return launch_spmm_cpl<Tw, Tx, 1, PK>(p, s, v, offs, B, x, ldx, Y, ldy, scales, st);
+    if (cpl == 2)
+        return launch_spmm_cpl<Tw, Tx, 2, PK>(p, s, v, offs, B, x, ldx, Y, ldy, scales, st);
+    if (cpl == 4)
+        return launch_spmm_cpl<Tw, Tx, 4, PK>(p, s, v, offs, B, x, ldx, Y, ldy, scales, st);
+    if constexpr (CPL == 8)
+        return launch_spmm_cpl<Tw, Tx, 8, PK>(p, s, v, offs, B, x, ldx, Y, ldy, scales, st);
+    return hipErrorInvalidConfiguration;
+}
+
+template <typename Tw, typename Tx>
+hipError_t launch_spmm_form(const darb_plan &p, const void *values, const uint8_t *offsets,
+                            const uint32_t *packed, int64_t B, const void *X, int64_t ldx,
+                            float *Y, int64_t ldy, const float *scales, hipStream_t st) {
+    if (offsets)
+        return launch_spmm_t<Tw, Tx, false>(p, values, offsets, nullptr, B, X, ldx, Y, ldy,
+                                            scales, st);
+    return launch_spmm_t<Tw, Tx, true>(p, values, nullptr, packed, B, X, ldx, Y, ldy, scales,
+                                       st);
+}
+
+}  // namespace
+}  // namespace darb
