@@ -61,7 +61,9 @@ def step_bytes(M, N, nnz, s_w, s_x, B):
 # the C-ABI layer that lays out the plan and the compile flags are hashed with it
 KERNEL_SOURCES = {"encode": "encode.hip", "pack": "packed.hip", "spmv": "product.hip",
                   "spmm": "product.hip", "spmv_packed": "product.hip",
-                  "spmm_packed": "product.hip", "prune": "prune.hip"}
+                  "spmm_packed": "product.hip", "prune": "prune.hip",
+                  "quantize_i8": "product_i8.hip", "spmv_i8": "product_i8.hip",
+                  "spmv_i8_packed": "product_i8.hip", "spmm_i8_packed": "product_i8.hip"}
 
 
 def kernel_sha256(kernel):
@@ -445,7 +447,48 @@ def main(argv=None):
         packed_ctx[n] = {"avg_us": round(us, 3), "bytes": int(pk_bytes[n]), "gbps": round(gbps, 1),
                          "frac_hbm_peak": round(gbps / HBM_PEAK_GBPS, 4),
                          "traffic_bytes": traffic.get(n if n == "pack" else n + "_packed")}
-    del packed
+
+    # INT8 retained values (section 4.2's storage accounting assumes INT8 weights): the
+    # per-row quantisation of the format's values and both products on INT8 codes
+    # with the packed offsets -- the paper's full storage form, 8 + log2 b bits per
+    # weight -- and with byte offsets; same rotation
+    codes = [torch.empty(plan.nnz, dtype=torch.int8, device=dev) for _ in range(RE)]
+    scales = [torch.empty(cfg.M, dtype=torch.float32, device=dev) for _ in range(RE)]
+    for j in range(RE):
+        plan.quantize_i8(fmt[j][0], codes[j], scales[j])
+    torch.cuda.synchronize()
+    q_args = [(h, wcode, P(fmt[j][0].data_ptr()), P(codes[j].data_ptr()),
+               P(scales[j].data_ptr()), sp) for j in range(RE)]
+    i8_spmv = [(h, P(codes[j].data_ptr()), P(scales[j].data_ptr()), None,
+                P(packed[j].data_ptr()), xcode, P(xd[j].data_ptr()), P(y.data_ptr()), sp)
+               for j in range(RE)]
+    i8_spmv_b = [(h, P(codes[j].data_ptr()), P(scales[j].data_ptr()), P(fmt[j][1].data_ptr()),
+                  None, xcode, P(xd[j].data_ptr()), P(y.data_ptr()), sp) for j in range(RE)]
+    i8_spmm = [(h, P(codes[j].data_ptr()), P(scales[j].data_ptr()), None,
+                P(packed[j].data_ptr()), xcode, B, P(Xd[j].data_ptr()), B, P(Y.data_ptr()), B,
+                sp) for j in range(RE)]
+    i8_us = {"quantize": timed_launches(lib.darb_quantize_i8, q_args, K),
+             "spmv_byte_offsets": timed_launches(lib.darb_spmv_i8, i8_spmv_b, K),
+             "spmv": timed_launches(lib.darb_spmv_i8, i8_spmv, K)}
+    i8_err = {"spmv": float((y - y_ref).norm() / y_ref.norm())}
+    if with_spmm:
+        i8_us["spmm"] = timed_launches(lib.darb_spmm_i8, i8_spmm, K)
+        i8_err["spmm"] = float((Y - Y_ref).norm() / Y_ref.norm())
+    i8_fmt = plan.nnz + 4 * pw + 4 * cfg.M
+    i8_bytes = {"quantize": plan.nnz * (s_w + 1) + 8 * cfg.M,
+                "spmv_byte_offsets": 2 * plan.nnz + cfg.N * s_x + 12 * cfg.M,
+                "spmv": i8_fmt + cfg.N * s_x + 8 * cfg.M,
+                "spmm": i8_fmt + cfg.N * B * s_x + 4 * cfg.M * B + 4 * cfg.M}
+    int8_ctx = {"format_bytes": i8_fmt,
+                "bits_per_weight": round(8.0 * i8_fmt / plan.nnz, 3),
+                "rel_rms_vs_unquantised_product": {n: round(e, 6) for n, e in i8_err.items()}}
+    for n, us in i8_us.items():
+        gbps = i8_bytes[n] / (us * 1e-6) / 1e9
+        tkey = {"quantize": "quantize_i8", "spmv_byte_offsets": "spmv_i8"}.get(n, n + "_i8_packed")
+        int8_ctx[n] = {"avg_us": round(us, 3), "bytes": int(i8_bytes[n]), "gbps": round(gbps, 1),
+                       "frac_hbm_peak": round(gbps / HBM_PEAK_GBPS, 4),
+                       "traffic_bytes": traffic.get(tkey)}
+    del packed, codes, scales
 
     # HBM reference rates measured in the same process: a plain stream read over
     # 4 GiB, and over buffers the size of the SpMV's bytes rotated past the cache
@@ -565,6 +608,7 @@ def main(argv=None):
         "encode_frac_of_W_read": round(w_read_us / kernels["encode"]["avg_us"], 4),
         "spmv_frac_of_measured_read_peak": round(kernels["spmv"]["gbps"] / read_peak, 4),
         "packed_offsets": packed_ctx,
+        "int8_values": int8_ctx,
         "prune_counts": prune_ctx,
         "dense_masked_context": dense_ctx,
         "host": {"plan_ms": round(plan_ms, 3), "enqueue_us_per_step": round(host_us, 2)},

@@ -13,6 +13,7 @@ namespace darb {
 namespace {
 
 constexpr int kQuantThreads = 256;
+constexpr int kQuantUnroll = 8;
 constexpr float kI8MinAbsmax = 0x1p-120f;
 
 template <typename Tw>
@@ -34,15 +35,35 @@ __global__ __launch_bounds__(kQuantThreads) void quantize_i8_kernel(
     const int64_t nblk = pick(bins.nblk, g);
     const int64_t e0 = pick(bins.first_elem, g) + (i - pick(bins.first_row, g)) * nblk;
 
+    // kQuantUnroll loads in flight per lane (indices clamped into the row, masked)
     float a = 0.0f;
-    for (int64_t k = lane; k < nblk; k += kWave) a = fmaxf(a, fabsf(value_f32(values, e0 + k)));
+    for (int64_t k0 = lane; k0 < nblk; k0 += kQuantUnroll * kWave) {
+        float v[kQuantUnroll];
+#pragma unroll
+        for (int u = 0; u < kQuantUnroll; ++u) {
+            const int64_t k = k0 + u * kWave;
+            v[u] = value_f32(values, e0 + (k < nblk ? k : nblk - 1));
+        }
+#pragma unroll
+        for (int u = 0; u < kQuantUnroll; ++u) a = fmaxf(a, fabsf(v[u]));
+    }
     for (int m = kWave / 2; m >= 1; m >>= 1) a = fmaxf(a, __shfl_xor(a, m, kWave));
 
     const bool live = a >= kI8MinAbsmax;
     const float inv = live ? __fdiv_rn(127.0f, a) : 0.0f;
-    for (int64_t k = lane; k < nblk; k += kWave) {
-        const float q = rintf(__fmul_rn(value_f32(values, e0 + k), inv));
-        codes[e0 + k] = int8_t(fminf(fmaxf(q, -127.0f), 127.0f));
+    for (int64_t k0 = lane; k0 < nblk; k0 += kQuantUnroll * kWave) {
+        float v[kQuantUnroll];
+#pragma unroll
+        for (int u = 0; u < kQuantUnroll; ++u) {
+            const int64_t k = k0 + u * kWave;
+            v[u] = value_f32(values, e0 + (k < nblk ? k : nblk - 1));
+        }
+#pragma unroll
+        for (int u = 0; u < kQuantUnroll; ++u) {
+            const int64_t k = k0 + u * kWave;
+            const float q = rintf(__fmul_rn(v[u], inv));
+            if (k < nblk) codes[e0 + k] = int8_t(fminf(fmaxf(q, -127.0f), 127.0f));
+        }
     }
     if (lane == 0) scales[perm[i]] = live ? __fdiv_rn(a, 127.0f) : 0.0f;
 }
