@@ -162,3 +162,26 @@ def test_whole_pipeline_on_device(darb, name):
         scale = oracle.spmm_absdot(vr, orf, lay, act)
         err = np.abs(np.asarray(got, dtype=np.float64).reshape(ref.shape) - ref)
         assert (err <= tol * scale).all()
+
+
+@pytest.mark.parametrize("case", ["candidates_fit", "candidate_room_overflows",
+                                  "workgroup_lds_overflows"])
+def test_split_pass_paths(darb, case):
+    # after the first digit the pass copies the keys sharing the threshold's first
+    # digit (candidates) and later passes read only them; when they do not fit (the
+    # workspace's room, M*N/32 here, or one workgroup's LDS) later passes stream W
+    # again.  Both must give the oracle's counts.
+    rng = np.random.default_rng(31)
+    M, N = 128, 65536
+    W = rng.uniform(0.0, 0.5, size=(M, N)).astype(np.float32)
+    if case == "candidates_fit":
+        ties = rng.random((M, N)) < 1.0 / 256           # ~33 k equal keys: fit
+    elif case == "candidate_room_overflows":
+        ties = rng.random((M, N)) < 1.0 / 16            # ~524 k > the room of 262 k
+    else:
+        ties = np.zeros((M, N), dtype=bool)
+        ties[:2] = True                                 # 131 k ties in two rows: one
+    W[ties] = 1.0                                       # workgroup's share > its LDS
+    k = int(ties.sum()) // 2 + 7
+    say(f"split pass {case}: {int(ties.sum())} keys equal to the threshold, k = {k}")
+    assert np.array_equal(gpu_counts(darb, dev(W), k), oracle.prune_counts(W, k))
