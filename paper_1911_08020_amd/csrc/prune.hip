@@ -23,6 +23,8 @@
 // candidates only.  Each workgroup gathers its candidates in LDS and reserves room
 // for them with one atomic; if a workgroup's LDS or the workspace's candidate
 // room overflows, every later pass streams W instead (the result is the same).
+// Below 64 MiB of W the split pass is skipped: there a pass over W costs less than
+// the extra launches.
 // All state stays on the device; nothing returns to the host between passes.
 #include "darb_internal.h"
 
@@ -45,6 +47,7 @@ struct PruneState {
 
 constexpr int kSplitLds = 8192;                     // candidates a workgroup can hold
 constexpr int kCandPerThread = 16;                  // candidate passes: keys per thread
+constexpr int64_t kSplitMinBytes = int64_t(64) << 20;   // W size from which the split pays
 
 template <typename Bits> struct PruneTraits;
 template <> struct PruneTraits<uint32_t> {
@@ -417,10 +420,11 @@ __global__ __launch_bounds__(kHistThreads) void prune_finish_kernel(
 }
 
 // Zero counts, eq, gt1 and the digit totals, and set the state to (prefix 0,
-// k_rem = k, no candidates).
+// k_rem = k, no candidates; overflow set when the split pass will not run).
 __global__ __launch_bounds__(256) void prune_init_kernel(int64_t M, int64_t k, PruneState *st,
                                                          int64_t *counts, int64_t *eq,
-                                                         int64_t *gt1, uint64_t *total) {
+                                                         int64_t *gt1, uint64_t *total,
+                                                         int split) {
     const int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x;
     if (i < M) {
         counts[i] = 0;
@@ -430,7 +434,7 @@ __global__ __launch_bounds__(256) void prune_init_kernel(int64_t M, int64_t k, P
     if (i < (int64_t(1) << kMaxDigitBits)) total[i] = 0;
     if (i == 0 && st) {
         st->prefix = 0;
-        st->overflow = 0;
+        st->overflow = split ? 0u : 1u;
         st->k_rem = k;
         st->n_cand = 0;
     }
@@ -511,8 +515,11 @@ hipError_t launch_prune_t(int64_t M, int64_t N, const void *Wv, int64_t ldw, int
     const int64_t init_n = M > (int64_t(1) << kMaxDigitBits) ? M : (int64_t(1) << kMaxDigitBits);
     const int64_t init_blocks = (init_n + 255) / 256;
     if (init_blocks > 0x7FFFFFFF) return hipErrorInvalidConfiguration;
+    // the split pass pays for its extra launches only on large matrices: below
+    // kSplitMinBytes of W every pass streams W
+    const int split = M * N * int64_t(sizeof(Bits)) >= kSplitMinBytes ? 1 : 0;
     hipLaunchKernelGGL(prune_init_kernel, dim3(unsigned(init_blocks)), dim3(256), 0, s, M, k, st,
-                       counts, eq, w.gt1, w.total);
+                       counts, eq, w.gt1, w.total, split);
     if (k == 0) return hipGetLastError();               // nothing kept: counts stay 0
 
     const int64_t segs = segments<Bits>(N);
@@ -539,7 +546,7 @@ hipError_t launch_prune_t(int64_t M, int64_t N, const void *Wv, int64_t ldw, int
                                from_cand);
         hipLaunchKernelGGL(prune_select_kernel, dim3(1), dim3(kHistThreads), 0, s, w.total, width,
                            st);
-        if (p == 0) {                                   // first digit chosen: split W once
+        if (p == 0 && split) {                          // first digit chosen: split W once
             if (aligned)
                 hipLaunchKernelGGL((prune_split_kernel<Bits, true>), dim3(groups),
                                    dim3(kHistThreads), 0, s, W, ldw, M, N, segs, shift, st,

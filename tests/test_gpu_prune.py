@@ -169,15 +169,16 @@ def test_whole_pipeline_on_device(darb, name):
 def test_split_pass_paths(darb, case):
     # after the first digit the pass copies the keys sharing the threshold's first
     # digit (candidates) and later passes read only them; when they do not fit (the
-    # workspace's room, M*N/32 here, or one workgroup's LDS) later passes stream W
-    # again.  Both must give the oracle's counts.
+    # workspace's room, M*N/32, or one workgroup's LDS) later passes stream W
+    # again.  Both must give the oracle's counts.  (64 MiB of fp32: the smallest W
+    # that takes the split pass.)
     rng = np.random.default_rng(31)
-    M, N = 128, 65536
+    M, N = 256, 65536
     W = rng.uniform(0.0, 0.5, size=(M, N)).astype(np.float32)
     if case == "candidates_fit":
-        ties = rng.random((M, N)) < 1.0 / 256           # ~33 k equal keys: fit
+        ties = rng.random((M, N)) < 1.0 / 256           # ~66 k equal keys: fit
     elif case == "candidate_room_overflows":
-        ties = rng.random((M, N)) < 1.0 / 16            # ~524 k > the room of 262 k
+        ties = rng.random((M, N)) < 1.0 / 16            # ~1 M > the room of 524 k
     else:
         ties = np.zeros((M, N), dtype=bool)
         ties[:2] = True                                 # 131 k ties in two rows: one
