@@ -99,6 +99,8 @@ typedef struct {
  *   b_min, b_max powers of two, 1 <= b_min <= b_max <= 128; the block size is
  *                clamped to [b_min, b_max].  A row of density 0 gets b_max.
  *   out          receives the new plan (host memory), or NULL on error.
+ * 1 <= M < 2^31, 1 <= N <= 2^31 - 256, and the plan may hold at most 2^55
+ * retained weights.
  * Errors: DARB_E_INVALID, DARB_E_NOMEM.
  */
 int darb_plan_create(int64_t M, int64_t N, const double *row_density, double matrix_density,

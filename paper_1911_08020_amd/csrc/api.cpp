@@ -164,6 +164,11 @@ int darb_plan_create(int64_t M, int64_t N, const double *row_density, double mat
         // packed offsets (section 4.2): runs of 32 weights, log2 b words per run
         words += (count[l] * nblk + 31) / 32 * l;
     }
+    // the per-row table packs a slot index and log2 b into 64 bits (slot << 8)
+    if (elem >= (int64_t(1) << 55)) {
+        delete p;
+        return fail(DARB_E_INVALID, "more than 2^55 retained weights");
+    }
     p->nnz = elem;
     p->packed_words = words;
     for (int64_t r = 0; r < M; ++r) {
