@@ -527,6 +527,33 @@ def main(argv=None):
     w_args = [(P(t.data_ptr()), w_bytes, P(sink.data_ptr()), sp) for t in Wd]
     w_read_us = timed_launches(lib.darb_stream_read, w_args, K)
 
+    # the SpMV at larger sizes: the same rows tiled t times (t*M rows with the same
+    # densities, W tiled on the device), format copies rotated past the 256 MB cache.
+    # A single launch pays a fixed start-up and memory latency; these sizes show how
+    # far the kernel's own rate rises once that is amortised.
+    size_sweep = []
+    for t in (1, 4, 16):
+        Mt = cfg.M * t
+        plan_t = darb.Plan(Mt, cfg.N, np.tile(mi.row_density, t), mi.matrix_density,
+                           darb.ROUND_FLOOR, cfg.b_min, cfg.b_max).upload()
+        fbytes = plan_t.nnz * (s_w + 1)
+        reps = int(min(8, max(2, -(-(512 << 20) // fbytes))))
+        Wt = Wd[0].repeat(t, 1)
+        fmts = [plan_t.empty_format(wdt, dev) for _ in range(reps)]
+        for v_t, o_t in fmts:
+            plan_t.encode(Wt, v_t, o_t)
+        del Wt
+        y_t = torch.empty(Mt, dtype=torch.float32, device=dev)
+        sw_args = [(plan_t.handle, wcode, P(v_t.data_ptr()), P(o_t.data_ptr()), xcode,
+                    P(xd[0].data_ptr()), P(y_t.data_ptr()), sp) for v_t, o_t in fmts]
+        lib.darb_spmv(*sw_args[0])
+        us = timed_launches(lib.darb_spmv, sw_args, max(K // 2, 20))
+        sb = fbytes + cfg.N * s_x + 8 * Mt
+        gbps = sb / (us * 1e-6) / 1e9
+        size_sweep.append({"rows": Mt, "bytes": int(sb), "avg_us": round(us, 3),
+                           "gbps": round(gbps, 1), "frac_of_4GiB_read": round(gbps / read_peak, 4)})
+        del fmts, y_t, plan_t
+
     # context, not a target: the same masked matrix as a dense fp32/fp16 matrix through
     # torch (hipBLASLt / rocBLAS), rotated like the DARB format
     Wm = plan.decode(*fmt[0])
@@ -611,6 +638,7 @@ def main(argv=None):
                          "stream_read_W_gbps": round(w_bytes / (w_read_us * 1e-6) / 1e9, 1)},
         "encode_frac_of_W_read": round(w_read_us / kernels["encode"]["avg_us"], 4),
         "spmv_frac_of_measured_read_peak": round(kernels["spmv"]["gbps"] / read_peak, 4),
+        "spmv_size_sweep": size_sweep,
         "packed_offsets": packed_ctx,
         "int8_values": int8_ctx,
         "prune_counts": prune_ctx,

@@ -243,9 +243,13 @@ int darb_plan_upload(darb_plan *p, void *workspace, int64_t workspace_bytes, voi
     // the host vector dies on return: make sure the copies have consumed it
     if (e == hipSuccess) e = hipStreamSynchronize(s);
     if (e != hipSuccess) return fail(DARB_E_HIP, std::string("plan upload: ") + hipGetErrorString(e));
+    int cus = 0;
+    e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e != hipSuccess) return fail(DARB_E_HIP, std::string("device attribute: ") + hipGetErrorString(e));
     p->d_perm = d_perm;
     p->d_rowinfo = d_rowinfo;
     p->device = dev;
+    p->cus = cus;
     return DARB_OK;
 }
 

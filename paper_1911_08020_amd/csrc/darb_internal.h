@@ -54,6 +54,7 @@ struct darb_plan {
     int32_t *d_perm = nullptr;      // [M] original row stored i-th
     int64_t *d_rowinfo = nullptr;   // [M] (row_start[r] << 8) | log2b[r], original order
     int device = -1;
+    int cus = 0;                    // compute units of that device
 };
 
 namespace darb {

@@ -178,6 +178,7 @@ constexpr int kSpmvThreads = 256;
 constexpr int kSpmvWaves = kSpmvThreads / kWave;
 constexpr int kVmax = 8;                         // vectors per lane per round
 constexpr int kLdsMaxFloats = 16384;             // x staged in LDS up to 64 KiB
+constexpr int64_t kLdsPerCu = 160 * 1024;        // LDS of one gfx950 CU
 
 template <typename Tw> struct WVec;
 template <> struct WVec<float> {
@@ -254,58 +255,73 @@ __device__ __forceinline__ void stage_x_direct(float *xs, const float *__restric
     for (int c = chunks * kWave * 4 + int(threadIdx.x); c < N; c += kSpmvThreads) xs[c] = x[c];
 }
 
-template <typename Tw, typename Tx, bool LDS, int SB, bool PK>
+template <typename Tw, typename Tx, bool LDS, int SB, bool PK, bool LOOP>
 __global__ __launch_bounds__(kSpmvThreads) void spmv_kernel(
     const Tw *__restrict__ values, const void *__restrict__ offs,
     const Tx *__restrict__ x, float *__restrict__ y, const int32_t *__restrict__ perm,
-    int N, BinTable bins, ProductSchedule sch, const float *__restrict__ scales) {
+    int N, BinTable bins, ProductSchedule sch, const float *__restrict__ scales,
+    int total_blocks) {
     using WV = WVec<Tw>;
     constexpr int VEC = WV::VEC;
     using OV = Off<PK, VEC>;
     using OS = Off<PK, 1>;
     extern __shared__ float xs[];
 
-    const int g = block_group(sch, int(blockIdx.x));
     const int wave = wave_uniform(int(threadIdx.x) / kWave);
     const int lane = int(threadIdx.x) & (kWave - 1);
-    const int lgL = pick(sch.log2_lanes, g);
-    const int L = 1 << lgL;
-    const int lb = pick(bins.log2b, g);
-    const int nblk = int(pick(bins.nblk, g));
-    const int64_t rows = pick(bins.rows, g);
-    const int64_t first_row = pick(bins.first_row, g);
-    const int64_t first_elem = pick(bins.first_elem, g);
-    const bool vec_path = pick(sch.vec, g) == VEC;
 
-    const int64_t tile = int64_t(int(blockIdx.x) - block_begin_of(sch, g)) * kSpmvWaves + wave;
-    const int64_t row = (tile << (6 - lgL)) + (lane >> lgL);
-    const bool row_ok = row < rows;
-    const int64_t row_c = row_ok ? row : rows - 1;
-    const int sub = lane & (L - 1);
-    const int64_t j0 = row_c * nblk;                     // the row's first slot in its group
-    const int64_t e0 = first_elem + j0;
-    const int nvec = vec_path ? nblk / VEC : nblk;
-    const GroupOffsets go = group_offsets(offs, bins, g);
-
-    // the destination row and the first round of this lane's vectors, issued
-    // before x is staged
-    const int32_t dest = perm[first_row + row_c];
-    const float scale = kScaled<Tw> ? scales[dest] : 1.0f;
+    // A workgroup stages x once and then takes blocks blockIdx.x, + gridDim.x, ...
+    // (LOOP; otherwise the grid has one workgroup per block, and the kernel keeps
+    // no state across blocks, so it needs fewer registers); each block is
+    // kSpmvWaves tiles of one group.  setup() reads a block's group geometry and
+    // issues the first round of the lane's vectors.
+    int g, lgL, L, lb, nblk, sub, nvec;
+    int64_t rows, first_row, first_elem, row, j0, e0;
+    bool vec_path, row_ok;
+    GroupOffsets go;
+    int32_t dest;
+    float scale;
+    const typename WV::V *vrow;
     typename WV::V wv[kVmax];
     typename OV::Raw ov[kVmax];
-    const typename WV::V *vrow = reinterpret_cast<const typename WV::V *>(values + e0);
-    if (vec_path) {
+    auto setup = [&](int blk) {
+        g = block_group(sch, blk);
+        lgL = pick(sch.log2_lanes, g);
+        L = 1 << lgL;
+        lb = pick(bins.log2b, g);
+        nblk = int(pick(bins.nblk, g));
+        rows = pick(bins.rows, g);
+        first_row = pick(bins.first_row, g);
+        first_elem = pick(bins.first_elem, g);
+        vec_path = pick(sch.vec, g) == VEC;
+        const int64_t tile = int64_t(blk - block_begin_of(sch, g)) * kSpmvWaves + wave;
+        row = (tile << (6 - lgL)) + (lane >> lgL);
+        row_ok = row < rows;
+        const int64_t row_c = row_ok ? row : rows - 1;
+        sub = lane & (L - 1);
+        j0 = row_c * nblk;                                // the row's first slot in its group
+        e0 = first_elem + j0;
+        nvec = vec_path ? nblk / VEC : nblk;
+        go = group_offsets(offs, bins, g);
+        dest = perm[first_row + row_c];
+        scale = kScaled<Tw> ? scales[dest] : 1.0f;
+        vrow = reinterpret_cast<const typename WV::V *>(values + e0);
+        if (vec_path) {
 #pragma unroll
-        for (int t = 0; t < kVmax; ++t) {
-            if (t * L < nvec) {                          // wave-uniform
-                const int vi = sub + t * L;
-                const int vc = vi < nvec ? vi : nvec - 1;
-                wv[t] = __builtin_nontemporal_load(vrow + vc);
-                ov[t] = OV::load(go, j0 + int64_t(vc) * VEC);
+            for (int t = 0; t < kVmax; ++t) {
+                if (t * L < nvec) {                      // wave-uniform
+                    const int vi = sub + t * L;
+                    const int vc = vi < nvec ? vi : nvec - 1;
+                    wv[t] = __builtin_nontemporal_load(vrow + vc);
+                    ov[t] = OV::load(go, j0 + int64_t(vc) * VEC);
+                }
             }
         }
-    }
+    };
 
+    // the first block's vectors are issued before x is staged
+    int blk = int(blockIdx.x);
+    setup(blk);
     if constexpr (LDS) {
         if constexpr (SB == 0 && std::is_same<Tx, float>::value) {   // fp32 x, 16 B aligned
             stage_x_direct(xs, x, N);
@@ -322,42 +338,49 @@ __global__ __launch_bounds__(kSpmvThreads) void spmv_kernel(
         else return to_f32<Tx>(x[c < N ? c : N - 1]);
     };
 
-    float acc = 0.0f;
-    if (vec_path) {
-        for (int base = 0;; base += L * kVmax) {
+    for (;;) {
+        float acc = 0.0f;
+        if (vec_path) {
+            for (int base = 0;; base += L * kVmax) {
 #pragma unroll
-            for (int t = 0; t < kVmax; ++t) {
-                const int vi = base + sub + t * L;
-                if (vi < nvec) {
-                    const typename OV::Bits ob = OV::bits(ov[t], go);
+                for (int t = 0; t < kVmax; ++t) {
+                    const int vi = base + sub + t * L;
+                    if (vi < nvec) {
+                        const typename OV::Bits ob = OV::bits(ov[t], go);
 #pragma unroll
-                    for (int q = 0; q < VEC; ++q) {
-                        const int c = ((vi * VEC + q) << lb) + OV::field(ob, q, go);
-                        acc = fmaf(WV::get(wv[t], q), xat(c), acc);
+                        for (int q = 0; q < VEC; ++q) {
+                            const int c = ((vi * VEC + q) << lb) + OV::field(ob, q, go);
+                            acc = fmaf(WV::get(wv[t], q), xat(c), acc);
+                        }
+                    }
+                }
+                if (base + L * kVmax >= nvec) break;
+#pragma unroll
+                for (int t = 0; t < kVmax; ++t) {
+                    if (base + L * kVmax + t * L < nvec) {   // wave-uniform
+                        const int vi = base + L * kVmax + sub + t * L;
+                        const int vc = vi < nvec ? vi : nvec - 1;
+                        wv[t] = __builtin_nontemporal_load(vrow + vc);
+                        ov[t] = OV::load(go, j0 + int64_t(vc) * VEC);
                     }
                 }
             }
-            if (base + L * kVmax >= nvec) break;
-#pragma unroll
-            for (int t = 0; t < kVmax; ++t) {
-                if (base + L * kVmax + t * L < nvec) {   // wave-uniform
-                    const int vi = base + L * kVmax + sub + t * L;
-                    const int vc = vi < nvec ? vi : nvec - 1;
-                    wv[t] = __builtin_nontemporal_load(vrow + vc);
-                    ov[t] = OV::load(go, j0 + int64_t(vc) * VEC);
-                }
+        } else {
+            const Tw *vr = values + e0;
+            for (int k = sub; k < nblk; k += L) {
+                const int o = OS::field(OS::bits(OS::load(go, j0 + k), go), 0, go);
+                acc = fmaf(to_f32<Tw>(vr[k]), xat((k << lb) + o), acc);
             }
         }
-    } else {
-        const Tw *vr = values + e0;
-        for (int k = sub; k < nblk; k += L) {
-            const int o = OS::field(OS::bits(OS::load(go, j0 + k), go), 0, go);
-            acc = fmaf(to_f32<Tw>(vr[k]), xat((k << lb) + o), acc);
-        }
-    }
 
-    for (int m = L >> 1; m >= 1; m >>= 1) acc += __shfl_xor(acc, m, kWave);
-    if (row_ok && sub == 0) y[dest] = kScaled<Tw> ? acc * scale : acc;
+        for (int m = L >> 1; m >= 1; m >>= 1) acc += __shfl_xor(acc, m, kWave);
+        if (row_ok && sub == 0) y[dest] = kScaled<Tw> ? acc * scale : acc;
+
+        if constexpr (!LOOP) break;
+        blk += int(gridDim.x);
+        if (blk >= total_blocks) break;                  // uniform
+        setup(blk);
+    }
 }
 
 // ---------------------------------------------------------------------------------
@@ -878,13 +901,28 @@ hipError_t launch_spmv_t(const darb_plan &p, const void *values, const uint8_t *
     const void *offs = offset_source(p, offsets, packed);
     const Tx *xx = static_cast<const Tx *>(x);
     const int N = int(p.N);
+    // Every workgroup stages x once: launch no more of them than fit on the chip at
+    // once (by LDS, at most 8 per CU) and let each take several blocks.
+    const int64_t lds_per_group = p.N <= kLdsMaxFloats ? p.N * int64_t(sizeof(float)) : 0;
+    int64_t per_cu = lds_per_group > 0 ? kLdsPerCu / lds_per_group : 8;
+    per_cu = per_cu < 1 ? 1 : (per_cu > 8 ? 8 : per_cu);
+    const int64_t resident = int64_t(p.cus > 0 ? p.cus : 256) * per_cu;
+    const int grid = int(blocks < resident ? blocks : resident);
     if (p.N <= kLdsMaxFloats) {
         const size_t lds = size_t(p.N) * sizeof(float);
         const int64_t nv = p.N / (16 / int64_t(sizeof(Tx)));
         const int64_t per_thread = (nv + kSpmvThreads - 1) / kSpmvThreads;
 #define DARB_SPMV_LDS(SB)                                                                    \
-    hipLaunchKernelGGL((spmv_kernel<Tw, Tx, true, SB, PK>), dim3(blocks), dim3(kSpmvThreads), \
-                       lds, st, v, offs, xx, y, p.d_perm, N, p.bins, s, scales)
+    do {                                                                                    \
+        if (grid < blocks)                                                                  \
+            hipLaunchKernelGGL((spmv_kernel<Tw, Tx, true, SB, PK, true>), dim3(grid),       \
+                               dim3(kSpmvThreads), lds, st, v, offs, xx, y, p.d_perm, N,    \
+                               p.bins, s, scales, blocks);                                  \
+        else                                                                                \
+            hipLaunchKernelGGL((spmv_kernel<Tw, Tx, true, SB, PK, false>), dim3(grid),      \
+                               dim3(kSpmvThreads), lds, st, v, offs, xx, y, p.d_perm, N,    \
+                               p.bins, s, scales, blocks);                                  \
+    } while (0)
         bool direct = false;
         if constexpr (std::is_same<Tx, float>::value) {
             direct = reinterpret_cast<uintptr_t>(x) % 16 == 0;
@@ -898,8 +936,14 @@ hipError_t launch_spmv_t(const darb_plan &p, const void *values, const uint8_t *
         else DARB_SPMV_LDS(16);
 #undef DARB_SPMV_LDS
     } else {
-        hipLaunchKernelGGL((spmv_kernel<Tw, Tx, false, 1, PK>), dim3(blocks), dim3(kSpmvThreads),
-                           0, st, v, offs, xx, y, p.d_perm, N, p.bins, s, scales);
+        if (grid < blocks)
+            hipLaunchKernelGGL((spmv_kernel<Tw, Tx, false, 1, PK, true>), dim3(grid),
+                               dim3(kSpmvThreads), 0, st, v, offs, xx, y, p.d_perm, N, p.bins, s,
+                               scales, blocks);
+        else
+            hipLaunchKernelGGL((spmv_kernel<Tw, Tx, false, 1, PK, false>), dim3(grid),
+                               dim3(kSpmvThreads), 0, st, v, offs, xx, y, p.d_perm, N, p.bins, s,
+                               scales, blocks);
     }
     return hipGetLastError();
 }
