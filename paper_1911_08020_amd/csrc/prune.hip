@@ -43,6 +43,7 @@ struct PruneState {
     uint32_t overflow;      // the candidates did not fit: later passes stream W
     int64_t k_rem;          // keys still to take at or below the prefix
     unsigned long long n_cand;   // candidates stored
+    unsigned long long n_last;   // keys matching the prefix after the latest digit
 };
 
 constexpr int kSplitLds = 8192;                     // candidates a workgroup can hold
@@ -316,6 +317,7 @@ __global__ __launch_bounds__(kHistThreads) void prune_select_kernel(
         }
         st->prefix = (prefix << width) | d;
         st->k_rem = int64_t(k - above);
+        st->n_last = d == uint32_t(d0) ? a : b;
     }
 }
 
@@ -328,6 +330,10 @@ __global__ __launch_bounds__(kHistThreads) void prune_count_kernel(
     unsigned long long *__restrict__ eq, const uint64_t *__restrict__ cand,
     const unsigned long long *__restrict__ gt1) {
     const uint32_t t = st->prefix;
+    // when every key equal to t is taken (always, without ties), they count with the
+    // keys above t and the finish scan has nothing to do
+    unsigned long long *__restrict__ eqc =
+        st->n_last == (unsigned long long)st->k_rem ? gt : eq;
     if (!st->overflow) {                                // uniform
         // one candidate per thread; a workgroup's candidates are stored together and
         // cover few rows, so a wave's 64 usually share one row: then one atomic each
@@ -349,11 +355,11 @@ __global__ __launch_bounds__(kHistThreads) void prune_count_kernel(
                 }
                 if (lane == __ffsll((unsigned long long)__ballot(1)) - 1) {
                     if (g) atomicAdd(&gt[r0], (unsigned long long)g);
-                    if (e) atomicAdd(&eq[r0], (unsigned long long)e);
+                    if (e) atomicAdd(&eqc[r0], (unsigned long long)e);
                 }
             } else {
                 if (g) atomicAdd(&gt[r], 1ull);
-                if (e) atomicAdd(&eq[r], 1ull);
+                if (e) atomicAdd(&eqc[r], 1ull);
             }
         }
         for (uint64_t r = first; r < uint64_t(M); r += stride)
@@ -372,7 +378,7 @@ __global__ __launch_bounds__(kHistThreads) void prune_count_kernel(
         }
         if (lane == 0 && cur >= 0) {
             if (g) atomicAdd(&gt[cur], (unsigned long long)g);
-            if (e) atomicAdd(&eq[cur], (unsigned long long)e);
+            if (e) atomicAdd(&eqc[cur], (unsigned long long)e);
         }
         n_gt = n_eq = 0;
     };
@@ -400,6 +406,7 @@ __global__ __launch_bounds__(kHistThreads) void prune_finish_kernel(
     __shared__ uint64_t wave_tot[kHistWaves];
     __shared__ int64_t tile_total;
     const int64_t need = st->k_rem;
+    if (st->n_last == uint64_t(need)) return;           // all taken by the count pass
     int64_t carry = 0;                                   // keys == t in rows before the tile
     for (int64_t base = 0; base < M; base += kHistThreads) {
         const int64_t r = base + threadIdx.x;
@@ -437,6 +444,7 @@ __global__ __launch_bounds__(256) void prune_init_kernel(int64_t M, int64_t k, P
         st->overflow = split ? 0u : 1u;
         st->k_rem = k;
         st->n_cand = 0;
+        st->n_last = 0;
     }
 }
 
