@@ -550,9 +550,24 @@ def main(argv=None):
         us = timed_launches(lib.darb_spmv, sw_args, max(K // 2, 20))
         sb = fbytes + cfg.N * s_x + 8 * Mt
         gbps = sb / (us * 1e-6) / 1e9
-        size_sweep.append({"rows": Mt, "bytes": int(sb), "avg_us": round(us, 3),
-                           "gbps": round(gbps, 1), "frac_of_4GiB_read": round(gbps / read_peak, 4)})
-        del fmts, y_t, plan_t
+        entry = {"rows": Mt, "bytes": int(sb), "avg_us": round(us, 3), "gbps": round(gbps, 1),
+                 "frac_of_4GiB_read": round(gbps / read_peak, 4)}
+        # the same rows in the paper's storage form: INT8 codes + log2 b-bit offsets
+        i8 = []
+        for v_t, o_t in fmts:
+            q_t, sc_t = plan_t.quantize_i8(v_t)
+            i8.append((q_t, sc_t, plan_t.pack_offsets(o_t)))
+        del fmts
+        i8_args = [(plan_t.handle, P(q_t.data_ptr()), P(sc_t.data_ptr()), None,
+                    P(pk_t.data_ptr()), xcode, P(xd[0].data_ptr()), P(y_t.data_ptr()), sp)
+                   for q_t, sc_t, pk_t in i8]
+        lib.darb_spmv_i8(*i8_args[0])
+        us8 = timed_launches(lib.darb_spmv_i8, i8_args, max(K // 2, 20))
+        sb8 = plan_t.nnz + 4 * plan_t.packed_words + 4 * Mt + cfg.N * s_x + 8 * Mt
+        entry["int8_packed"] = {"bytes": int(sb8), "avg_us": round(us8, 3),
+                                "gbps": round(sb8 / (us8 * 1e-6) / 1e9, 1)}
+        size_sweep.append(entry)
+        del i8, y_t, plan_t
 
     # context, not a target: the same masked matrix as a dense fp32/fp16 matrix through
     # torch (hipBLASLt / rocBLAS), rotated like the DARB format
