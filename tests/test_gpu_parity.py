@@ -406,3 +406,29 @@ def test_bench_prints_contract_json(darb, capsys):
     assert d["roofline"]["bound"] == "hbm" and 0 < d["roofline"]["frac"] < 1.5
     assert d["cpu_baseline"]["kind"] == "oracle" and d["cpu_baseline"]["cores"] >= 1
     assert "workload" in d["config"]
+
+
+def test_spmv_workgroups_take_several_blocks(darb):
+    # 5000 rows of 16 384 columns at b = 8: 1250 blocks of 4 rows (625 of 8 rows with
+    # INT8 codes), while x (64 KiB of LDS per workgroup) lets only 2 workgroups per
+    # CU fit (512 on 256 CUs), so each workgroup stages x once and loops over several
+    # blocks.  Byte, packed and INT8 forms.
+    say("spmv with looping workgroups")
+    rng = np.random.default_rng(77)
+    M, N = 5000, 16384
+    W = rng.standard_normal((M, N)).astype(np.float32)
+    d = np.full(M, 1.0 / 8)
+    plan, lay, vals, offs = encode_both(darb, W, d, 0.125, 0, 1, 128)
+    assert int(np.unique(lay.log2b)[0]) == 3
+    x = rng.standard_normal(N).astype(np.float32)
+    vd, od = dev(vals), dev(offs)
+    y = host(plan.spmv(vd, od, dev(x)))
+    check_product(y, vals, offs, lay, x, np.float32, "looping spmv")
+    packed = plan.pack_offsets(od)
+    yp = host(plan.spmv_packed(vd, packed, dev(x)))
+    assert np.array_equal(y.view(np.uint32), yp.view(np.uint32))
+    q, s = oracle.quantize_i8(vals, lay)
+    y8 = host(plan.spmv_i8(dev(q), dev(s), dev(x), packed=packed))
+    ref = oracle.spmm_i8(q, s, offs, lay, x)
+    scale = oracle.spmm_i8_absdot(q, s, offs, lay, x)
+    assert (np.abs(y8.astype(np.float64) - ref) <= 1e-5 * scale).all()
