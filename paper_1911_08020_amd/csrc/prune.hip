@@ -25,6 +25,9 @@
 // room overflows, every later pass streams W instead (the result is the same).
 // Below 64 MiB of W the split pass is skipped: there a pass over W costs less than
 // the extra launches.
+// Each histogram pass picks its digit in the workgroup that finishes last (a
+// counter in the state tells it), and the count pass's last workgroup takes the
+// keys equal to t, so a call is six launches.
 // All state stays on the device; nothing returns to the host between passes.
 #include "darb_internal.h"
 
@@ -35,7 +38,7 @@ constexpr int kHistThreads = 1024;
 constexpr int kHistWaves = kHistThreads / kWave;
 constexpr int kMaxDigitBits = 11;
 constexpr int kCopies = 4;                          // LDS histogram copies per workgroup
-constexpr int kMaxHistGroups = 512;
+constexpr int kMaxHistGroups = 256;                 // one 1024-thread workgroup per CU
 
 // Radix-select state, in the workspace.
 struct PruneState {
@@ -44,6 +47,8 @@ struct PruneState {
     int64_t k_rem;          // keys still to take at or below the prefix
     unsigned long long n_cand;   // candidates stored
     unsigned long long n_last;   // keys matching the prefix after the latest digit
+    uint32_t done;          // workgroups finished in the running pass (0 between passes)
+    uint32_t pad;
 };
 
 constexpr int kSplitLds = 8192;                     // candidates a workgroup can hold
@@ -53,77 +58,97 @@ constexpr int64_t kSplitMinBytes = int64_t(64) << 20;   // W size from which the
 template <typename Bits> struct PruneTraits;
 template <> struct PruneTraits<uint32_t> {
     static constexpr int VEC = 4;
+    static constexpr int UNROLL = 4;        // 16-byte loads per lane per round
     static constexpr int KEY_BITS = 31;
     static constexpr uint32_t MAG = 0x7FFFFFFFu;
 };
 template <> struct PruneTraits<uint16_t> {
     static constexpr int VEC = 8;
+    static constexpr int UNROLL = 2;        // 16 keys per lane per round, as for fp32
     static constexpr int KEY_BITS = 15;
     static constexpr uint32_t MAG = 0x7FFFu;
 };
-constexpr int kUnroll = 4;
 
 template <typename Bits, int VEC> struct alignas(16) PVec { Bits e[VEC]; };
 
-// A wave's work unit is one segment of one row: kSegRounds rounds of kUnroll
-// 16-byte loads per lane.
-constexpr int kSegRounds = 4;
-template <typename Bits> constexpr int64_t seg_width() {
-    return int64_t(kSegRounds) * kUnroll * kWave * PruneTraits<Bits>::VEC;
+// Work is split evenly over the waves: W is taken as M rows padded to whole
+// VEC-element vectors, flattened, and wave w streams elements [w * per_wave,
+// (w + 1) * per_wave) of that (per_wave a multiple of kWave * VEC, so every piece
+// starts on a vector boundary), in pieces of one row each.
+template <typename Bits> constexpr int64_t round_width() {
+    return int64_t(PruneTraits<Bits>::UNROLL) * kWave * PruneTraits<Bits>::VEC;
+}
+template <typename Bits> __host__ __device__ constexpr int64_t padded_n(int64_t N) {
+    return (N + PruneTraits<Bits>::VEC - 1) / PruneTraits<Bits>::VEC * PruneTraits<Bits>::VEC;
 }
 
-// Stream the wave's segments: on_unit(r) when the wave starts a segment of row r
-// (all lanes together), then round(keys, valid) for every round of the segment
+// Stream the wave's pieces: on_unit(r) when the wave starts a piece of row r
+// (all lanes together), then round(keys, valid) for every round of the piece
 // (all lanes together): the lane's kUnroll * VEC keys and a mask of those inside
-// the segment.
+// the row.
 template <typename Bits, bool ALIGNED, typename U, typename R>
 __device__ __forceinline__ void for_each_round(const Bits *__restrict__ W, int64_t ldw,
-                                               int64_t M, int64_t N, int64_t segs, U &&on_unit,
-                                               R &&round) {
+                                               int64_t M, int64_t N, int64_t per_wave,
+                                               U &&on_unit, R &&round) {
     using Tr = PruneTraits<Bits>;
     constexpr int VEC = Tr::VEC;
-    constexpr int64_t STEP = int64_t(kUnroll) * kWave * VEC;
+    constexpr int kUnroll = Tr::UNROLL;
+    constexpr int64_t STEP = round_width<Bits>();
     const int lane = int(threadIdx.x) & (kWave - 1);
-    const int64_t gw = int64_t(blockIdx.x) * (blockDim.x / kWave) + threadIdx.x / kWave;
+    // the wave's index, made visibly wave-uniform so the loop state stays scalar
+    const int wave = __builtin_amdgcn_readfirstlane(int(threadIdx.x) / kWave);
+    const int64_t gw = int64_t(blockIdx.x) * (blockDim.x / kWave) + wave;
     const int64_t tw = int64_t(gridDim.x) * (blockDim.x / kWave);
-    const int64_t units = M * segs;
-    for (int64_t u = gw; u < units; u += tw) {          // wave-uniform
-        const int64_t r = u / segs;
-        const int64_t c_begin = (u - r * segs) * seg_width<Bits>();
-        const int64_t c_end = c_begin + seg_width<Bits>() < N ? c_begin + seg_width<Bits>() : N;
-        const Bits *row = W + r * ldw;
-        on_unit(r);
-        for (int64_t c0 = c_begin; c0 < c_end; c0 += STEP) {
-            PVec<Bits, VEC> v[kUnroll];
-            uint32_t valid[kUnroll];                  // bit e: element e is inside the segment
+    const int64_t Np = padded_n<Bits>(N);
+    const int64_t total = M * Np;
+    for (int64_t a = gw * per_wave; a < total; a += tw * per_wave) {   // wave-uniform
+        const int64_t b = a + per_wave < total ? a + per_wave : total;
+        int64_t r = a / Np;
+        int64_t c = a - r * Np;
+        for (int64_t at = a; at < b; ++r, c = 0) {
+            const int64_t c_piece = c + (b - at) < Np ? c + (b - at) : Np;
+            const int64_t c_end = c_piece < N ? c_piece : N;
+            at += c_piece - c;
+            const Bits *row = W + r * ldw;
+            on_unit(r);
+            for (int64_t c0 = c; c0 < c_end; c0 += STEP) {
+                PVec<Bits, VEC> v[kUnroll];
+                uint32_t valid[kUnroll];              // bit e: element e is inside the row
 #pragma unroll
-            for (int q = 0; q < kUnroll; ++q) {
-                const int64_t c = c0 + int64_t(q) * kWave * VEC + int64_t(lane) * VEC;
-                if (ALIGNED && c + VEC <= c_end) {
-                    typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-                    const u32x4 t = __builtin_nontemporal_load(
-                        reinterpret_cast<const u32x4 *>(row + c));
-                    v[q] = __builtin_bit_cast(PVec<Bits, VEC>, t);
-                    valid[q] = (1u << VEC) - 1u;
-                } else {
-                    valid[q] = 0;
+                for (int q = 0; q < kUnroll; ++q) {
+                    const int64_t cc = c0 + int64_t(q) * kWave * VEC + int64_t(lane) * VEC;
+                    // a vector wholly past the end costs nothing (and, unlike the
+                    // element path, does not wait for the round's other loads)
+                    if (cc >= c_end) {
+                        v[q] = PVec<Bits, VEC>{};
+                        valid[q] = 0;
+                    } else if (ALIGNED && cc + VEC <= c_end) {
+                        typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+                        const u32x4 t = __builtin_nontemporal_load(
+                            reinterpret_cast<const u32x4 *>(row + cc));
+                        v[q] = __builtin_bit_cast(PVec<Bits, VEC>, t);
+                        valid[q] = (1u << VEC) - 1u;
+                    } else {
+                        valid[q] = 0;
 #pragma unroll
-                    for (int e = 0; e < VEC; ++e) {
-                        const bool in = c + e < c_end;
-                        v[q].e[e] = in ? row[c + e] : Bits(0);
-                        valid[q] |= in ? (1u << e) : 0u;
+                        for (int e = 0; e < VEC; ++e) {
+                            const bool in = cc + e < c_end;
+                            v[q].e[e] = in ? row[cc + e] : Bits(0);
+                            valid[q] |= in ? (1u << e) : 0u;
+                        }
                     }
                 }
-            }
-            uint32_t keys[kUnroll * VEC];
-            uint32_t mask = 0;
+                uint32_t keys[kUnroll * VEC];
+                uint32_t mask = 0;
 #pragma unroll
-            for (int q = 0; q < kUnroll; ++q) {
+                for (int q = 0; q < kUnroll; ++q) {
 #pragma unroll
-                for (int e = 0; e < VEC; ++e) keys[q * VEC + e] = uint32_t(v[q].e[e]) & Tr::MAG;
-                mask |= valid[q] << (q * VEC);
+                    for (int e = 0; e < VEC; ++e)
+                        keys[q * VEC + e] = uint32_t(v[q].e[e]) & Tr::MAG;
+                    mask |= valid[q] << (q * VEC);
+                }
+                round(keys, mask);
             }
-            round(keys, mask);
         }
     }
 }
@@ -131,9 +156,9 @@ __device__ __forceinline__ void for_each_round(const Bits *__restrict__ W, int64
 // As for_each_round, with f(key) for every element inside the segment (per lane).
 template <typename Bits, bool ALIGNED, typename U, typename F>
 __device__ __forceinline__ void for_each_key(const Bits *__restrict__ W, int64_t ldw, int64_t M,
-                                             int64_t N, int64_t segs, U &&on_unit, F &&f) {
-    constexpr int K = kUnroll * PruneTraits<Bits>::VEC;
-    for_each_round<Bits, ALIGNED>(W, ldw, M, N, segs, on_unit,
+                                             int64_t N, int64_t per_wave, U &&on_unit, F &&f) {
+    constexpr int K = PruneTraits<Bits>::UNROLL * PruneTraits<Bits>::VEC;
+    for_each_round<Bits, ALIGNED>(W, ldw, M, N, per_wave, on_unit,
                                   [&](const uint32_t (&keys)[K], uint32_t mask) {
 #pragma unroll
                                       for (int j = 0; j < K; ++j)
@@ -141,46 +166,137 @@ __device__ __forceinline__ void for_each_key(const Bits *__restrict__ W, int64_t
                                   });
 }
 
+// Block-wide inclusive scan of one value per thread (kHistThreads threads).
+__device__ __forceinline__ uint64_t block_inclusive_scan(uint64_t v, uint64_t *wave_tot) {
+    const int lane = int(threadIdx.x) & (kWave - 1);
+    const int wave = int(threadIdx.x) / kWave;
+#pragma unroll
+    for (int d = 1; d < kWave; d <<= 1) {
+        const uint64_t o = __shfl_up(v, d, kWave);
+        if (lane >= d) v += o;
+    }
+    if (lane == kWave - 1) wave_tot[wave] = v;
+    __syncthreads();
+    uint64_t before = 0;
+    for (int w = 0; w < wave; ++w) before += wave_tot[w];
+    __syncthreads();
+    return v + before;
+}
+
+// Called by every thread of a workgroup after its global atomics: true in the
+// one workgroup that finishes the pass last, which also clears the counter for
+// the next pass.  Every value that crosses workgroups goes through device-wide
+// read-modify-write atomics, which are coherent across the chip's L2 caches: each
+// thread waits until its own atomics are acknowledged before the barrier, so they
+// precede the workgroup's increment of the counter, and the last workgroup reads
+// the totals with read-modify-write atomics too.  (An agent-scope fence would
+// write back and invalidate the L2 in every wave of every workgroup.)
+__device__ __forceinline__ bool last_workgroup(PruneState *st, uint32_t *flag) {
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        const uint32_t before = atomicAdd(&st->done, 1u);
+        const bool last = before == gridDim.x - 1;
+        if (last) atomicExch(&st->done, 0u);
+        *flag = last ? 1u : 0u;
+    }
+    __syncthreads();
+    return *flag != 0;
+}
+
+// One workgroup, after a histogram pass: find the digit d where the count of
+// matching keys with digit > d is < k_rem <= that count plus total[d], append it
+// to the prefix, and clear `total` for the next pass.
+__device__ __forceinline__ void select_digit(unsigned long long *__restrict__ total, int width,
+                                             PruneState *__restrict__ st, uint64_t *tot,
+                                             uint64_t *wave_tot) {
+    const int bins = 1 << width;
+    for (int b = int(threadIdx.x); b < bins; b += kHistThreads) tot[b] = atomicExch(&total[b], 0ull);
+    __syncthreads();
+    const int64_t k_rem = st->k_rem;
+    const uint32_t prefix = st->prefix;
+    __syncthreads();                                    // every thread has read the state
+    // thread t owns the digits bins-1-2t and bins-2-2t (descending order)
+    const int d0 = bins - 1 - 2 * int(threadIdx.x), d1 = d0 - 1;
+    const uint64_t a = d0 >= 0 ? tot[d0] : 0, b = d1 >= 0 ? tot[d1] : 0;
+    const uint64_t incl = block_inclusive_scan(a + b, wave_tot);
+    const uint64_t excl = incl - a - b;
+    const uint64_t k = uint64_t(k_rem);
+    if (excl < k && k <= incl) {                        // exactly one thread
+        uint32_t d;
+        uint64_t above;
+        if (k <= excl + a) {
+            d = uint32_t(d0);
+            above = excl;
+        } else {
+            d = uint32_t(d1);
+            above = excl + a;
+        }
+        st->prefix = (prefix << width) | d;
+        st->k_rem = int64_t(k - above);
+        st->n_last = d == uint32_t(d0) ? a : b;
+    }
+}
+
 // Histogram of digit (key >> shift) & (2^width - 1) over keys whose higher bits
-// (key >> (shift + width)) equal state.prefix, added into `total` (zeroed before
-// the pass): each workgroup adds its non-zero bins once.  The keys come from W
-// (all of it) or, when `from_cand` and the candidates fit, from the candidates.
+// (key >> (shift + width)) equal state.prefix, added into `total` (zero at the
+// start): each workgroup adds its non-zero bins once, and the last workgroup to
+// finish picks the digit.  The keys come from W (all of it) or, when
+// `from_cand` and the candidates fit, from the candidates.
 template <typename Bits, bool ALIGNED>
 __global__ __launch_bounds__(kHistThreads) void prune_hist_kernel(
-    const Bits *__restrict__ W, int64_t ldw, int64_t M, int64_t N, int64_t segs, int shift,
-    int width, const PruneState *__restrict__ st, unsigned long long *__restrict__ total,
+    const Bits *__restrict__ W, int64_t ldw, int64_t M, int64_t N, int64_t per_wave, int shift,
+    int width, PruneState *__restrict__ st, unsigned long long *__restrict__ total,
     const uint64_t *__restrict__ cand, int from_cand) {
     constexpr int kStride = (1 << kMaxDigitBits) + 1;   // copies land in different banks
     __shared__ uint32_t hist[kCopies * kStride];
+    __shared__ uint64_t tot[1 << kMaxDigitBits];
+    __shared__ uint64_t wave_tot[kHistWaves];
+    __shared__ uint32_t flag;
     const int bins = 1 << width;
-    for (int i = int(threadIdx.x); i < kCopies * kStride; i += kHistThreads) hist[i] = 0;
-    __syncthreads();
-    const uint32_t prefix = st->prefix;
-    const int hi = shift + width;                       // <= key bits <= 31
-    const uint32_t dmask = uint32_t(bins - 1);
-    uint32_t *mine = hist + (int(threadIdx.x) & (kCopies - 1)) * kStride;
-    auto add = [&](uint32_t key) {
-        if ((key >> hi) == prefix) atomicAdd(&mine[(key >> shift) & dmask], 1u);
-    };
-    if (from_cand && !st->overflow) {                   // uniform
-        // kCandPerThread candidates per thread: few workgroups, so few bins to flush
-        const uint64_t n = st->n_cand;
-        const uint64_t per_group = uint64_t(kCandPerThread) * kHistThreads;
-        if (uint64_t(blockIdx.x) * per_group >= n && blockIdx.x > 0) return;   // uniform
-        const uint64_t groups = (n + per_group - 1) / per_group;
-        const uint64_t stride = (groups < gridDim.x ? groups : gridDim.x) * kHistThreads;
-        for (uint64_t i = uint64_t(blockIdx.x) * kHistThreads + threadIdx.x; i < n; i += stride)
-            add(uint32_t(cand[i]));
-    } else {
-        for_each_key<Bits, ALIGNED>(W, ldw, M, N, segs, [](int64_t) {}, add);
-    }
-    __syncthreads();
-    for (int b = int(threadIdx.x); b < bins; b += kHistThreads) {
-        uint32_t s = 0;
+    const bool cands = from_cand && !st->overflow;     // uniform
+    const uint64_t n = cands ? uint64_t(st->n_cand) : 0;
+    // kCandPerThread candidates per thread: few workgroups, so few bins to flush
+    const uint64_t per_group = uint64_t(kCandPerThread) * kHistThreads;
+    const bool idle = cands && blockIdx.x > 0 && uint64_t(blockIdx.x) * per_group >= n;
+    if (!idle) {                                        // uniform
+        for (int i = int(threadIdx.x); i < kCopies * kStride; i += kHistThreads) hist[i] = 0;
+        __syncthreads();
+        const uint32_t prefix = st->prefix;
+        const int hi = shift + width;                   // <= key bits <= 31
+        const uint32_t dmask = uint32_t(bins - 1);
+        uint32_t *mine = hist + (int(threadIdx.x) & (kCopies - 1)) * kStride;
+        auto add = [&](uint32_t key) {
+            if ((key >> hi) == prefix) atomicAdd(&mine[(key >> shift) & dmask], 1u);
+        };
+        if (cands) {
+            const uint64_t groups = (n + per_group - 1) / per_group;
+            const uint64_t stride = (groups < gridDim.x ? groups : gridDim.x) * kHistThreads;
+            // all of a thread's loads issued before its LDS atomics
+            for (uint64_t i0 = uint64_t(blockIdx.x) * kHistThreads + threadIdx.x; i0 < n;
+                 i0 += stride * kCandPerThread) {
+                uint32_t kk[kCandPerThread];
 #pragma unroll
-        for (int c = 0; c < kCopies; ++c) s += hist[c * kStride + b];
-        if (s) atomicAdd(&total[b], (unsigned long long)s);
+                for (int j = 0; j < kCandPerThread; ++j) {
+                    const uint64_t i = i0 + uint64_t(j) * stride;
+                    kk[j] = i < n ? uint32_t(cand[i]) : 0u;
+                }
+#pragma unroll
+                for (int j = 0; j < kCandPerThread; ++j)
+                    if (i0 + uint64_t(j) * stride < n) add(kk[j]);
+            }
+        } else {
+            for_each_key<Bits, ALIGNED>(W, ldw, M, N, per_wave, [](int64_t) {}, add);
+        }
+        __syncthreads();
+        for (int b = int(threadIdx.x); b < bins; b += kHistThreads) {
+            uint32_t s = 0;
+#pragma unroll
+            for (int c = 0; c < kCopies; ++c) s += hist[c * kStride + b];
+            if (s) atomicAdd(&total[b], (unsigned long long)s);
+        }
     }
+    if (last_workgroup(st, &flag)) select_digit(total, width, st, tot, wave_tot);
 }
 
 // The split pass, after the first digit d (= state.prefix) is chosen: per row, the
@@ -190,7 +306,7 @@ __global__ __launch_bounds__(kHistThreads) void prune_hist_kernel(
 // state's overflow flag sends the later passes back to W.
 template <typename Bits, bool ALIGNED>
 __global__ __launch_bounds__(kHistThreads) void prune_split_kernel(
-    const Bits *__restrict__ W, int64_t ldw, int64_t M, int64_t N, int64_t segs, int shift,
+    const Bits *__restrict__ W, int64_t ldw, int64_t M, int64_t N, int64_t per_wave, int shift,
     PruneState *__restrict__ st, unsigned long long *__restrict__ gt1,
     uint64_t *__restrict__ cand, uint64_t cap) {
     __shared__ uint64_t buf[kSplitLds];
@@ -209,9 +325,9 @@ __global__ __launch_bounds__(kHistThreads) void prune_split_kernel(
         if (lane == 0 && cur >= 0 && g) atomicAdd(&gt1[cur], (unsigned long long)g);
         n_gt = 0;
     };
-    constexpr int K = kUnroll * PruneTraits<Bits>::VEC;
+    constexpr int K = PruneTraits<Bits>::UNROLL * PruneTraits<Bits>::VEC;
     for_each_round<Bits, ALIGNED>(
-        W, ldw, M, N, segs,
+        W, ldw, M, N, per_wave,
         [&](int64_t r) {
             if (r != cur) {
                 flush();
@@ -267,163 +383,115 @@ __global__ __launch_bounds__(kHistThreads) void prune_split_kernel(
         for (uint32_t i = threadIdx.x; i < n; i += kHistThreads) cand[base + i] = buf[i];
 }
 
-// Block-wide inclusive scan of one value per thread (kHistThreads threads).
-__device__ __forceinline__ uint64_t block_inclusive_scan(uint64_t v, uint64_t *wave_tot) {
-    const int lane = int(threadIdx.x) & (kWave - 1);
-    const int wave = int(threadIdx.x) / kWave;
-#pragma unroll
-    for (int d = 1; d < kWave; d <<= 1) {
-        const uint64_t o = __shfl_up(v, d, kWave);
-        if (lane >= d) v += o;
-    }
-    if (lane == kWave - 1) wave_tot[wave] = v;
-    __syncthreads();
-    uint64_t before = 0;
-    for (int w = 0; w < wave; ++w) before += wave_tot[w];
-    __syncthreads();
-    return v + before;
-}
-
-// One workgroup: find the digit d where the count of matching keys with digit > d
-// is < k_rem <= that count plus total[d]; then clear `total` for the next pass.
-__global__ __launch_bounds__(kHistThreads) void prune_select_kernel(
-    uint64_t *__restrict__ total, int width, PruneState *__restrict__ st) {
-    __shared__ uint64_t tot[1 << kMaxDigitBits];
-    __shared__ uint64_t wave_tot[kHistWaves];
-    const int bins = 1 << width;
-    for (int b = int(threadIdx.x); b < bins; b += kHistThreads) {
-        tot[b] = total[b];
-        total[b] = 0;
-    }
-    __syncthreads();
-    const int64_t k_rem = st->k_rem;
-    const uint32_t prefix = st->prefix;
-    __syncthreads();                                    // every thread has read the state
-    // thread t owns the digits bins-1-2t and bins-2-2t (descending order)
-    const int d0 = bins - 1 - 2 * int(threadIdx.x), d1 = d0 - 1;
-    const uint64_t a = d0 >= 0 ? tot[d0] : 0, b = d1 >= 0 ? tot[d1] : 0;
-    const uint64_t incl = block_inclusive_scan(a + b, wave_tot);
-    const uint64_t excl = incl - a - b;
-    const uint64_t k = uint64_t(k_rem);
-    if (excl < k && k <= incl) {                        // exactly one thread
-        uint32_t d;
-        uint64_t above;
-        if (k <= excl + a) {
-            d = uint32_t(d0);
-            above = excl;
-        } else {
-            d = uint32_t(d1);
-            above = excl + a;
-        }
-        st->prefix = (prefix << width) | d;
-        st->k_rem = int64_t(k - above);
-        st->n_last = d == uint32_t(d0) ? a : b;
-    }
-}
-
-// Per-row counts of keys > t (into counts) and == t (into eq); t = state.prefix.
-// From the candidates when they fit (plus the split pass's gt1), else from W.
-template <typename Bits, bool ALIGNED>
-__global__ __launch_bounds__(kHistThreads) void prune_count_kernel(
-    const Bits *__restrict__ W, int64_t ldw, int64_t M, int64_t N, int64_t segs,
-    const PruneState *__restrict__ st, unsigned long long *__restrict__ gt,
-    unsigned long long *__restrict__ eq, const uint64_t *__restrict__ cand,
-    const unsigned long long *__restrict__ gt1) {
-    const uint32_t t = st->prefix;
-    // when every key equal to t is taken (always, without ties), they count with the
-    // keys above t and the finish scan has nothing to do
-    unsigned long long *__restrict__ eqc =
-        st->n_last == (unsigned long long)st->k_rem ? gt : eq;
-    if (!st->overflow) {                                // uniform
-        // one candidate per thread; a workgroup's candidates are stored together and
-        // cover few rows, so a wave's 64 usually share one row: then one atomic each
-        const uint64_t n = st->n_cand;
-        const uint64_t stride = uint64_t(gridDim.x) * kHistThreads;
-        const uint64_t first = uint64_t(blockIdx.x) * kHistThreads + threadIdx.x;
-        const int lane = int(threadIdx.x) & (kWave - 1);
-        for (uint64_t i = first; i < n; i += stride) {
-            const uint64_t c = cand[i];
-            const uint32_t key = uint32_t(c);
-            const int32_t r = int32_t(c >> 32);
-            uint32_t g = key > t ? 1u : 0u, e = key == t ? 1u : 0u;
-            const int32_t r0 = __builtin_amdgcn_readfirstlane(r);
-            if (__all(r == r0)) {                       // wave-uniform
-#pragma unroll
-                for (int m = kWave / 2; m >= 1; m >>= 1) {
-                    g += __shfl_xor(g, m, kWave);
-                    e += __shfl_xor(e, m, kWave);
-                }
-                if (lane == __ffsll((unsigned long long)__ballot(1)) - 1) {
-                    if (g) atomicAdd(&gt[r0], (unsigned long long)g);
-                    if (e) atomicAdd(&eqc[r0], (unsigned long long)e);
-                }
-            } else {
-                if (g) atomicAdd(&gt[r], 1ull);
-                if (e) atomicAdd(&eqc[r], 1ull);
-            }
-        }
-        for (uint64_t r = first; r < uint64_t(M); r += stride)
-            if (gt1[r]) atomicAdd(&gt[r], gt1[r]);
-        return;
-    }
-    const int lane = int(threadIdx.x) & (kWave - 1);
-    int64_t cur = -1;
-    uint32_t n_gt = 0, n_eq = 0;
-    auto flush = [&]() {
-        uint32_t g = n_gt, e = n_eq;
-#pragma unroll
-        for (int d = kWave / 2; d >= 1; d >>= 1) {
-            g += __shfl_xor(g, d, kWave);
-            e += __shfl_xor(e, d, kWave);
-        }
-        if (lane == 0 && cur >= 0) {
-            if (g) atomicAdd(&gt[cur], (unsigned long long)g);
-            if (e) atomicAdd(&eqc[cur], (unsigned long long)e);
-        }
-        n_gt = n_eq = 0;
-    };
-    // a unit is one segment of one row: flush the previous row's counts when the
-    // wave moves on (all lanes take part in the reduction)
-    for_each_key<Bits, ALIGNED>(
-        W, ldw, M, N, segs,
-        [&](int64_t r) {
-            if (r != cur) {
-                flush();
-                cur = r;
-            }
-        },
-        [&](uint32_t key) {
-            n_gt += key > t ? 1u : 0u;
-            n_eq += key == t ? 1u : 0u;
-        });
-    flush();
-}
-
-// counts[r] (= keys > t) += the keys == t taken in ascending row order, need in total.
-__global__ __launch_bounds__(kHistThreads) void prune_finish_kernel(
-    int64_t M, const PruneState *__restrict__ st, int64_t *__restrict__ counts,
-    const int64_t *__restrict__ eq) {
-    __shared__ uint64_t wave_tot[kHistWaves];
-    __shared__ int64_t tile_total;
+// counts[r] (= keys > t) += the keys == t taken in ascending row order, need in
+// total; one workgroup.
+__device__ __forceinline__ void take_ties(int64_t M, const PruneState *__restrict__ st,
+                                          unsigned long long *__restrict__ counts,
+                                          unsigned long long *__restrict__ eq,
+                                          uint64_t *wave_tot, int64_t *tile_total) {
     const int64_t need = st->k_rem;
-    if (st->n_last == uint64_t(need)) return;           // all taken by the count pass
     int64_t carry = 0;                                   // keys == t in rows before the tile
     for (int64_t base = 0; base < M; base += kHistThreads) {
         const int64_t r = base + threadIdx.x;
-        const int64_t e = r < M ? eq[r] : 0;
+        const int64_t e = r < M ? int64_t(atomicAdd(&eq[r], 0ull)) : 0;
         const int64_t incl = int64_t(block_inclusive_scan(uint64_t(e), wave_tot));
         const int64_t before = carry + incl - e;
         if (r < M) {
             int64_t take = need - before;
             take = take < 0 ? 0 : (take > e ? e : take);
-            counts[r] += take;
+            if (take) atomicAdd(&counts[r], (unsigned long long)take);
         }
         // the tile total, from the last thread's inclusive sum
-        if (threadIdx.x == kHistThreads - 1) tile_total = incl;
+        if (threadIdx.x == kHistThreads - 1) *tile_total = incl;
         __syncthreads();
-        carry += tile_total;
+        carry += *tile_total;
         __syncthreads();
     }
+}
+
+// Per-row counts of keys > t (into counts) and == t (into eq); t = state.prefix.
+// From the candidates when they fit (plus the split pass's gt1), else from W.
+// The last workgroup to finish then adds the keys == t that are kept.
+template <typename Bits, bool ALIGNED>
+__global__ __launch_bounds__(kHistThreads) void prune_count_kernel(
+    const Bits *__restrict__ W, int64_t ldw, int64_t M, int64_t N, int64_t per_wave,
+    PruneState *__restrict__ st, unsigned long long *__restrict__ gt,
+    unsigned long long *__restrict__ eq, const uint64_t *__restrict__ cand,
+    const unsigned long long *__restrict__ gt1) {
+    __shared__ uint64_t wave_tot[kHistWaves];
+    __shared__ int64_t tile_total;
+    __shared__ uint32_t flag;
+    const uint32_t t = st->prefix;
+    // when every key equal to t is taken (always, without ties), they count with the
+    // keys above t and nothing is left for the last workgroup
+    const bool all_ties = st->n_last == (unsigned long long)st->k_rem;
+    unsigned long long *__restrict__ eqc = all_ties ? gt : eq;
+    const int lane = int(threadIdx.x) & (kWave - 1);
+    if (!st->overflow) {                                // uniform
+        // a wave's 64 candidates come in runs from few rows (each run is one
+        // wave-round of the split pass): one atomic per row present and kind
+        const uint64_t n = st->n_cand;
+        const uint64_t stride = uint64_t(gridDim.x) * kHistThreads;
+        const uint64_t first = uint64_t(blockIdx.x) * kHistThreads + threadIdx.x;
+        for (uint64_t i0 = first - uint64_t(lane); i0 < n; i0 += stride) {   // wave-uniform
+            const uint64_t i = i0 + uint64_t(lane);
+            const uint64_t c = i < n ? cand[i] : 0;
+            const uint32_t key = uint32_t(c);
+            const int32_t r = int32_t(c >> 32);
+            const bool g = i < n && key > t, e = i < n && key == t;
+            uint64_t todo = __ballot(g || e);
+            while (todo) {                              // wave-uniform
+                const int l = __ffsll((unsigned long long)todo) - 1;
+                const int32_t r0 = __shfl(r, l, kWave);
+                const bool same = ((todo >> lane) & 1u) && r == r0;
+                const uint64_t ng = __popcll(__ballot(same && g));
+                const uint64_t ne = __popcll(__ballot(same && e));
+                if (lane == l) {
+                    if (all_ties) {
+                        atomicAdd(&gt[r0], (unsigned long long)(ng + ne));
+                    } else {
+                        if (ng) atomicAdd(&gt[r0], (unsigned long long)ng);
+                        if (ne) atomicAdd(&eq[r0], (unsigned long long)ne);
+                    }
+                }
+                todo &= ~__ballot(same);
+            }
+        }
+        for (uint64_t r = first; r < uint64_t(M); r += stride)
+            if (gt1[r]) atomicAdd(&gt[r], gt1[r]);
+    } else {
+        int64_t cur = -1;
+        uint32_t n_gt = 0, n_eq = 0;
+        auto flush = [&]() {
+            uint32_t g = n_gt, e = n_eq;
+#pragma unroll
+            for (int d = kWave / 2; d >= 1; d >>= 1) {
+                g += __shfl_xor(g, d, kWave);
+                e += __shfl_xor(e, d, kWave);
+            }
+            if (lane == 0 && cur >= 0) {
+                if (g) atomicAdd(&gt[cur], (unsigned long long)g);
+                if (e) atomicAdd(&eqc[cur], (unsigned long long)e);
+            }
+            n_gt = n_eq = 0;
+        };
+        // flush the previous row's counts when the wave moves on to a new row (all
+        // lanes take part in the reduction)
+        for_each_key<Bits, ALIGNED>(
+            W, ldw, M, N, per_wave,
+            [&](int64_t r) {
+                if (r != cur) {
+                    flush();
+                    cur = r;
+                }
+            },
+            [&](uint32_t key) {
+                n_gt += key > t ? 1u : 0u;
+                n_eq += key == t ? 1u : 0u;
+            });
+        flush();
+    }
+    if (last_workgroup(st, &flag) && !all_ties) take_ties(M, st, gt, eq, wave_tot, &tile_total);
 }
 
 // Zero counts, eq, gt1 and the digit totals, and set the state to (prefix 0,
@@ -445,24 +513,34 @@ __global__ __launch_bounds__(256) void prune_init_kernel(int64_t M, int64_t k, P
         st->k_rem = k;
         st->n_cand = 0;
         st->n_last = 0;
+        st->done = 0;
     }
 }
 
 int64_t align256(int64_t v) { return (v + 255) / 256 * 256; }
 
-template <typename Bits> int64_t segments(int64_t N) {
-    return (N + seg_width<Bits>() - 1) / seg_width<Bits>();
-}
+// Grid of the passes over W and each wave's share of the padded, flattened W:
+// at least one vector per lane (small matrices spread over many CUs: there each
+// wave's latency, not bandwidth, sets the time), at most kMaxHistGroups workgroups
+// (measured: two per CU, each with half the work, run slower), and few enough
+// elements per workgroup (< 2^31) that its 32-bit LDS counters cannot overflow.
+struct PrunePartition {
+    int groups;
+    int64_t per_wave;
+};
 
-template <typename Bits> int hist_groups(int64_t M, int64_t N) {
-    // enough waves for every unit up to kMaxHistGroups workgroups, and few enough
-    // elements per workgroup that its 32-bit LDS counters cannot overflow
-    const int64_t units = M * segments<Bits>(N);
-    int64_t g = (units + kHistWaves - 1) / kHistWaves;
+template <typename Bits> PrunePartition prune_partition(int64_t M, int64_t N) {
+    const int64_t total = M * padded_n<Bits>(N);
+    const int64_t quantum = int64_t(kWave) * PruneTraits<Bits>::VEC;
+    const int64_t per_group_min = quantum * kHistWaves;
+    int64_t g = (total + per_group_min - 1) / per_group_min;
     if (g > kMaxHistGroups) g = kMaxHistGroups;
-    const int64_t per_group_limit = int64_t(1) << 31;
-    while (g * per_group_limit < M * N) g *= 2;
-    return int(g < 1 ? 1 : g);
+    if (g < 1) g = 1;
+    while (g * (int64_t(1) << 30) < total) g *= 2;
+    const int64_t waves = g * kHistWaves;
+    int64_t per_wave = (total + waves - 1) / waves;
+    per_wave = (per_wave + quantum - 1) / quantum * quantum;
+    return {int(g), per_wave};
 }
 
 // Room for candidates: 1/32 of W's elements (typical candidates are ~1 %), at
@@ -519,7 +597,9 @@ hipError_t launch_prune_t(int64_t M, int64_t N, const void *Wv, int64_t ldw, int
     PruneState *st = w.st;
     int64_t *eq = w.eq;
     auto *total_u = reinterpret_cast<unsigned long long *>(w.total);
-    const int groups = hist_groups<Bits>(M, N);
+    const PrunePartition part = prune_partition<Bits>(M, N);
+    const int groups = part.groups;
+    const int64_t per_wave = part.per_wave;
     const int64_t init_n = M > (int64_t(1) << kMaxDigitBits) ? M : (int64_t(1) << kMaxDigitBits);
     const int64_t init_blocks = (init_n + 255) / 256;
     if (init_blocks > 0x7FFFFFFF) return hipErrorInvalidConfiguration;
@@ -530,7 +610,6 @@ hipError_t launch_prune_t(int64_t M, int64_t N, const void *Wv, int64_t ldw, int
                        counts, eq, w.gt1, w.total, split);
     if (k == 0) return hipGetLastError();               // nothing kept: counts stay 0
 
-    const int64_t segs = segments<Bits>(N);
     const bool aligned = (reinterpret_cast<uintptr_t>(W) % 16 == 0) &&
                          ((ldw * int64_t(sizeof(Bits))) % 16 == 0);
     // digit widths from the most significant end
@@ -546,22 +625,20 @@ hipError_t launch_prune_t(int64_t M, int64_t N, const void *Wv, int64_t ldw, int
         const int from_cand = p > 0;
         if (aligned)
             hipLaunchKernelGGL((prune_hist_kernel<Bits, true>), dim3(groups), dim3(kHistThreads),
-                               0, s, W, ldw, M, N, segs, shift, width, st, total_u, w.cand,
+                               0, s, W, ldw, M, N, per_wave, shift, width, st, total_u, w.cand,
                                from_cand);
         else
             hipLaunchKernelGGL((prune_hist_kernel<Bits, false>), dim3(groups), dim3(kHistThreads),
-                               0, s, W, ldw, M, N, segs, shift, width, st, total_u, w.cand,
+                               0, s, W, ldw, M, N, per_wave, shift, width, st, total_u, w.cand,
                                from_cand);
-        hipLaunchKernelGGL(prune_select_kernel, dim3(1), dim3(kHistThreads), 0, s, w.total, width,
-                           st);
         if (p == 0 && split) {                          // first digit chosen: split W once
             if (aligned)
                 hipLaunchKernelGGL((prune_split_kernel<Bits, true>), dim3(groups),
-                                   dim3(kHistThreads), 0, s, W, ldw, M, N, segs, shift, st,
+                                   dim3(kHistThreads), 0, s, W, ldw, M, N, per_wave, shift, st,
                                    gt1_u, w.cand, cap);
             else
                 hipLaunchKernelGGL((prune_split_kernel<Bits, false>), dim3(groups),
-                                   dim3(kHistThreads), 0, s, W, ldw, M, N, segs, shift, st,
+                                   dim3(kHistThreads), 0, s, W, ldw, M, N, per_wave, shift, st,
                                    gt1_u, w.cand, cap);
         }
         hi = shift;
@@ -570,11 +647,10 @@ hipError_t launch_prune_t(int64_t M, int64_t N, const void *Wv, int64_t ldw, int
     auto *eq_u = reinterpret_cast<unsigned long long *>(eq);
     if (aligned)
         hipLaunchKernelGGL((prune_count_kernel<Bits, true>), dim3(groups), dim3(kHistThreads), 0,
-                           s, W, ldw, M, N, segs, st, gt_u, eq_u, w.cand, gt1_u);
+                           s, W, ldw, M, N, per_wave, st, gt_u, eq_u, w.cand, gt1_u);
     else
         hipLaunchKernelGGL((prune_count_kernel<Bits, false>), dim3(groups), dim3(kHistThreads), 0,
-                           s, W, ldw, M, N, segs, st, gt_u, eq_u, w.cand, gt1_u);
-    hipLaunchKernelGGL(prune_finish_kernel, dim3(1), dim3(kHistThreads), 0, s, M, st, counts, eq);
+                           s, W, ldw, M, N, per_wave, st, gt_u, eq_u, w.cand, gt1_u);
     return hipGetLastError();
 }
 
