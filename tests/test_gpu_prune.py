@@ -83,6 +83,21 @@ def test_continuous_values_many_digits(darb, dtype):
         assert np.array_equal(gpu_counts(darb, Wd, k), oracle.prune_counts(W, k)), keep
 
 
+@pytest.mark.parametrize("dtype", [np.float32, np.float16])
+@pytest.mark.parametrize("N", [1, 3, 7, 9, 17])
+def test_narrow_rows_many_rows_per_wave(darb, dtype, N):
+    # W is split evenly over the waves as padded rows; with narrow rows one wave's
+    # range crosses many rows, and rows end inside a 16-byte vector
+    rng = np.random.default_rng(100 + N)
+    M = 20000 // N + 13
+    W = (rng.integers(-40, 41, size=(M, N)) * 0.125).astype(dtype)
+    Wd = dev(W)
+    size = M * N
+    for k in (1, size // 3, size - 5):
+        say(f"  {np.dtype(dtype).name} {M}x{N} k={k}")
+        assert np.array_equal(gpu_counts(darb, Wd, k), oracle.prune_counts(W, k)), k
+
+
 def test_special_values(darb):
     W = np.zeros((6, 40), dtype=np.float32)
     W[0, 3], W[1, 0], W[2, 39], W[3, 7] = np.nan, np.inf, -np.inf, 1e-45
