@@ -409,13 +409,14 @@ def main(argv=None):
     lib.darb_prune_counts(*prune_args[0])              # first launches load the kernels
     prune_us = timed_launches(lib.darb_prune_counts, prune_args, max(K // 4, 8))
     prune_ok = bool(np.array_equal(counts.cpu().numpy(), mi.mask.sum(axis=1)))
-    # from 64 MiB of W the first digit's histogram and the split pass read W and the
-    # later passes only the keys that share the threshold's first digit (about 1 %
-    # of W); below it every pass (3 digits + count for fp32, 2 + count for fp16) reads W
+    # from 64 MiB of W a sample (about 1/32 of W) proposes the first digit's bracket,
+    # one split pass reads W and the later passes only the keys in the bracket
+    # (about 1 % of W); below it every pass (3 digits + count for fp32, 2 + count for
+    # fp16) reads W
     w_stream = cfg.M * cfg.N * s_w
-    w_passes = 2 if w_stream >= (64 << 20) else (4 if cfg.wdtype == "f32" else 3)
-    prune_ctx = {"avg_us": round(prune_us, 3), "k": mi.k, "passes_over_W": w_passes,
-                 "bytes": w_passes * w_stream,
+    w_passes = 1 + 1 / 32 if w_stream >= (64 << 20) else (4 if cfg.wdtype == "f32" else 3)
+    prune_ctx = {"avg_us": round(prune_us, 3), "k": mi.k, "passes_over_W": round(w_passes, 3),
+                 "bytes": int(w_passes * w_stream),
                  "gbps": round(w_passes * w_stream / (prune_us * 1e-6) / 1e9, 1),
                  "counts_equal_generator": prune_ok}
     del prune_ws

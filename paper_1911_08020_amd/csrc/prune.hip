@@ -29,6 +29,8 @@
 // counter in the state tells it), and the count pass's last workgroup takes the
 // keys equal to t, so a call is six launches.
 // All state stays on the device; nothing returns to the host between passes.
+#include <algorithm>
+
 #include "darb_internal.h"
 
 namespace darb {
@@ -48,10 +50,15 @@ struct PruneState {
     unsigned long long n_cand;   // candidates stored
     unsigned long long n_last;   // keys matching the prefix after the latest digit
     uint32_t done;          // workgroups finished in the running pass (0 between passes)
-    uint32_t pad;
+    uint32_t single;        // the split pass also takes the first digit's histogram
+    uint32_t dlo, dhi;      // first digits the split pass keeps as candidates
 };
 
 constexpr int kSplitLds = 8192;                     // candidates a workgroup can hold
+constexpr int64_t kSampleEvery = 32;                // the sample reads about 1/32 of W
+constexpr int64_t kSampleDrift = 37;                // vectors added to the sample stride
+constexpr int64_t kSampleChunk = 4;                 // vectors per lane in one sampled range
+constexpr int kSampleGroups = 256;                  // workgroups of the sample pass
 constexpr int kCandPerThread = 16;                  // candidate passes: keys per thread
 constexpr int64_t kSplitMinBytes = int64_t(64) << 20;   // W size from which the split pays
 
@@ -74,7 +81,9 @@ template <typename Bits, int VEC> struct alignas(16) PVec { Bits e[VEC]; };
 // Work is split evenly over the waves: W is taken as M rows padded to whole
 // VEC-element vectors, flattened, and wave w streams elements [w * per_wave,
 // (w + 1) * per_wave) of that (per_wave a multiple of kWave * VEC, so every piece
-// starts on a vector boundary), in pieces of one row each.
+// starts on a vector boundary), in pieces of one row each.  A sample reads ranges
+// of per_wave elements range_stride apart instead (range_stride = per_wave reads
+// all of W).
 template <typename Bits> constexpr int64_t round_width() {
     return int64_t(PruneTraits<Bits>::UNROLL) * kWave * PruneTraits<Bits>::VEC;
 }
@@ -89,7 +98,7 @@ template <typename Bits> __host__ __device__ constexpr int64_t padded_n(int64_t 
 template <typename Bits, bool ALIGNED, typename U, typename R>
 __device__ __forceinline__ void for_each_round(const Bits *__restrict__ W, int64_t ldw,
                                                int64_t M, int64_t N, int64_t per_wave,
-                                               U &&on_unit, R &&round) {
+                                               int64_t range_stride, U &&on_unit, R &&round) {
     using Tr = PruneTraits<Bits>;
     constexpr int VEC = Tr::VEC;
     constexpr int kUnroll = Tr::UNROLL;
@@ -101,7 +110,7 @@ __device__ __forceinline__ void for_each_round(const Bits *__restrict__ W, int64
     const int64_t tw = int64_t(gridDim.x) * (blockDim.x / kWave);
     const int64_t Np = padded_n<Bits>(N);
     const int64_t total = M * Np;
-    for (int64_t a = gw * per_wave; a < total; a += tw * per_wave) {   // wave-uniform
+    for (int64_t a = gw * range_stride; a < total; a += tw * range_stride) {   // wave-uniform
         const int64_t b = a + per_wave < total ? a + per_wave : total;
         int64_t r = a / Np;
         int64_t c = a - r * Np;
@@ -156,9 +165,10 @@ __device__ __forceinline__ void for_each_round(const Bits *__restrict__ W, int64
 // As for_each_round, with f(key) for every element inside the segment (per lane).
 template <typename Bits, bool ALIGNED, typename U, typename F>
 __device__ __forceinline__ void for_each_key(const Bits *__restrict__ W, int64_t ldw, int64_t M,
-                                             int64_t N, int64_t per_wave, U &&on_unit, F &&f) {
+                                             int64_t N, int64_t per_wave, int64_t range_stride,
+                                             U &&on_unit, F &&f) {
     constexpr int K = PruneTraits<Bits>::UNROLL * PruneTraits<Bits>::VEC;
-    for_each_round<Bits, ALIGNED>(W, ldw, M, N, per_wave, on_unit,
+    for_each_round<Bits, ALIGNED>(W, ldw, M, N, per_wave, range_stride, on_unit,
                                   [&](const uint32_t (&keys)[K], uint32_t mask) {
 #pragma unroll
                                       for (int j = 0; j < K; ++j)
@@ -204,12 +214,18 @@ __device__ __forceinline__ bool last_workgroup(PruneState *st, uint32_t *flag) {
     return *flag != 0;
 }
 
+// What the workgroup that picks the first digit does with it besides.
+enum SelectAfter { kJustSelect = 0, kSetBracket = 1, kCheckBracket = 2 };
+
 // One workgroup, after a histogram pass: find the digit d where the count of
 // matching keys with digit > d is < k_rem <= that count plus total[d], append it
-// to the prefix, and clear `total` for the next pass.
+// to the prefix, and clear `total` for the next pass.  For the first digit, also
+// make d the split pass's bracket (kSetBracket), or, when the split pass took
+// candidates from a sampled bracket, send the later passes back to W if d lies
+// outside it (kCheckBracket).
 __device__ __forceinline__ void select_digit(unsigned long long *__restrict__ total, int width,
                                              PruneState *__restrict__ st, uint64_t *tot,
-                                             uint64_t *wave_tot) {
+                                             uint64_t *wave_tot, int after) {
     const int bins = 1 << width;
     for (int b = int(threadIdx.x); b < bins; b += kHistThreads) tot[b] = atomicExch(&total[b], 0ull);
     __syncthreads();
@@ -235,24 +251,101 @@ __device__ __forceinline__ void select_digit(unsigned long long *__restrict__ to
         st->prefix = (prefix << width) | d;
         st->k_rem = int64_t(k - above);
         st->n_last = d == uint32_t(d0) ? a : b;
+        if (after == kSetBracket) {
+            st->dlo = d;
+            st->dhi = d;
+        } else if (after == kCheckBracket && (d < st->dlo || d > st->dhi)) {
+            atomicExch(&st->overflow, 1u);
+        }
     }
 }
+
+// One workgroup, after the sample's first-digit histogram (n_s keys out of the
+// matrix's total_keys, a fraction f): the split pass's bracket [dlo, dhi] of first
+// digits that holds the k-th largest key's digit, up to six standard deviations
+// of the sample count (a binomial) plus 8 keys: keys above dhi number at most
+// f*k - margin in the sample, keys at or above dlo at least f*k + margin.  One pass
+// over W then suffices (`single`) unless the bracket's predicted candidates exceed
+// cand_limit.  Clears `total`.
+__device__ __forceinline__ void select_bracket(unsigned long long *__restrict__ total, int width,
+                                               PruneState *__restrict__ st, int64_t total_keys,
+                                               uint64_t cand_limit, uint64_t *tot,
+                                               uint64_t *wave_tot, uint32_t *lds_u32) {
+    const int bins = 1 << width;
+    uint32_t &s_dlo = lds_u32[0], &s_dhi = lds_u32[1];
+    for (int b = int(threadIdx.x); b < bins; b += kHistThreads) tot[b] = atomicExch(&total[b], 0ull);
+    if (threadIdx.x == 0) {
+        s_dlo = 0;
+        s_dhi = uint32_t(bins - 1);
+    }
+    __syncthreads();
+    const double k = double(st->k_rem);
+    // thread t owns the digits bins-1-2t and bins-2-2t (descending order)
+    const int d0 = bins - 1 - 2 * int(threadIdx.x), d1 = d0 - 1;
+    const uint64_t a = d0 >= 0 ? tot[d0] : 0, b = d1 >= 0 ? tot[d1] : 0;
+    const uint64_t incl = block_inclusive_scan(a + b, wave_tot);
+    const uint64_t excl = incl - a - b;
+    uint64_t n_s = 0;
+    for (int w = 0; w < kHistWaves; ++w) n_s += wave_tot[w];
+    const double q = k / double(total_keys);
+    const double ks = q * double(n_s);
+    const double margin = 6.0 * sqrt(ks * (1.0 - q)) + 8.0;
+    const double lo = ks - margin, hi = ks + margin;
+    // digit d has `above` keys with a larger digit and `above + tot[d]` at or above
+    // it, both non-increasing in d: dhi is the one digit with above <= lo <
+    // above + tot[d] (or digit 0 with above <= lo), dlo the one with above < hi <=
+    // above + tot[d] (or the top digit with tot >= hi); the defaults stand when no
+    // digit qualifies.  One thread writes each (no contended atomics).
+    auto ends = [&](int d, uint64_t above, uint64_t cnt) {
+        if (d < 0) return;
+        const double ab = double(above), at = double(above + cnt);
+        if (ab <= lo && (d == 0 || at > lo)) s_dhi = uint32_t(d);
+        if (at >= hi && (d == bins - 1 || ab < hi)) s_dlo = uint32_t(d);
+    };
+    ends(d0, excl, a);
+    ends(d1, excl + a, b);
+    __syncthreads();
+    const uint32_t dlo = s_dlo, dhi = s_dhi;
+    uint64_t in = 0;
+    if (d0 >= 0 && uint32_t(d0) >= dlo && uint32_t(d0) <= dhi) in += a;
+    if (d1 >= 0 && uint32_t(d1) >= dlo && uint32_t(d1) <= dhi) in += b;
+    __syncthreads();                                    // wave_tot is reused
+    const uint64_t in_all = block_inclusive_scan(in, wave_tot);
+    if (threadIdx.x == kHistThreads - 1) {
+        // predicted candidates: the bracket's sample keys scaled by 1/f
+        const bool fits = n_s > 0 && double(in_all) * double(total_keys) <=
+                                         double(cand_limit) * double(n_s);
+        st->single = fits ? 1u : 0u;
+        st->dlo = dlo;
+        st->dhi = dhi;
+    }
+}
+
+// What a histogram pass is for.
+enum HistRole {
+    kRoleDigit = 0,     // the next digit (W, or the candidates when they fit)
+    kRoleSample = 1,    // the first digit over a sample of W: the split pass's bracket
+    kRoleFirst = 2,     // the first digit over all of W, unless the bracket suffices
+};
 
 // Histogram of digit (key >> shift) & (2^width - 1) over keys whose higher bits
 // (key >> (shift + width)) equal state.prefix, added into `total` (zero at the
 // start): each workgroup adds its non-zero bins once, and the last workgroup to
-// finish picks the digit.  The keys come from W (all of it) or, when
-// `from_cand` and the candidates fit, from the candidates.
+// finish picks the digit (or, for the sample, the bracket).  The keys come from
+// W (ranges of per_wave elements range_stride apart), or, when `from_cand` and
+// the candidates fit, from the candidates.
 template <typename Bits, bool ALIGNED>
 __global__ __launch_bounds__(kHistThreads) void prune_hist_kernel(
-    const Bits *__restrict__ W, int64_t ldw, int64_t M, int64_t N, int64_t per_wave, int shift,
-    int width, PruneState *__restrict__ st, unsigned long long *__restrict__ total,
-    const uint64_t *__restrict__ cand, int from_cand) {
+    const Bits *__restrict__ W, int64_t ldw, int64_t M, int64_t N, int64_t per_wave,
+    int64_t range_stride, int shift, int width, PruneState *__restrict__ st,
+    unsigned long long *__restrict__ total, const uint64_t *__restrict__ cand, int from_cand,
+    int role, uint64_t cand_limit) {
     constexpr int kStride = (1 << kMaxDigitBits) + 1;   // copies land in different banks
     __shared__ uint32_t hist[kCopies * kStride];
     __shared__ uint64_t tot[1 << kMaxDigitBits];
     __shared__ uint64_t wave_tot[kHistWaves];
-    __shared__ uint32_t flag;
+    __shared__ uint32_t flag[3];                 // last-workgroup flag, bracket ends
+    if (role == kRoleFirst && st->single) return;       // uniform: the split pass does it
     const int bins = 1 << width;
     const bool cands = from_cand && !st->overflow;     // uniform
     const uint64_t n = cands ? uint64_t(st->n_cand) : 0;
@@ -286,7 +379,8 @@ __global__ __launch_bounds__(kHistThreads) void prune_hist_kernel(
                     if (i0 + uint64_t(j) * stride < n) add(kk[j]);
             }
         } else {
-            for_each_key<Bits, ALIGNED>(W, ldw, M, N, per_wave, [](int64_t) {}, add);
+            for_each_key<Bits, ALIGNED>(W, ldw, M, N, per_wave, range_stride, [](int64_t) {},
+                                        add);
         }
         __syncthreads();
         for (int b = int(threadIdx.x); b < bins; b += kHistThreads) {
@@ -296,25 +390,41 @@ __global__ __launch_bounds__(kHistThreads) void prune_hist_kernel(
             if (s) atomicAdd(&total[b], (unsigned long long)s);
         }
     }
-    if (last_workgroup(st, &flag)) select_digit(total, width, st, tot, wave_tot);
+    if (!last_workgroup(st, &flag[0])) return;
+    if (role == kRoleSample)
+        select_bracket(total, width, st, M * N, cand_limit, tot, wave_tot, flag + 1);
+    else
+        select_digit(total, width, st, tot, wave_tot, role == kRoleFirst ? kSetBracket : kJustSelect);
 }
 
-// The split pass, after the first digit d (= state.prefix) is chosen: per row, the
-// keys with first digit > d go to gt1; keys with first digit == d are stored as
-// (row << 32 | key) candidates.  Runs in the same grid as the histogram passes.
-// If any workgroup's candidates overflow its LDS or the workspace's room, the
-// state's overflow flag sends the later passes back to W.
+// The split pass, once the bracket [dlo, dhi] of first digits is known: per row,
+// the keys with first digit > dhi go to gt1; keys with first digit in the bracket
+// are stored as (row << 32 | key) candidates.  Runs in the same grid as the
+// histogram passes.  If any workgroup's candidates overflow its LDS or the
+// workspace's room, the state's overflow flag sends the later passes back to W.
+// With `single` (the bracket came from a sample) it also takes the first digit's
+// histogram of all of W, and its last workgroup picks the digit and checks that
+// it lies in the bracket (if not, the later passes go back to W as well).
 template <typename Bits, bool ALIGNED>
 __global__ __launch_bounds__(kHistThreads) void prune_split_kernel(
     const Bits *__restrict__ W, int64_t ldw, int64_t M, int64_t N, int64_t per_wave, int shift,
-    PruneState *__restrict__ st, unsigned long long *__restrict__ gt1,
-    uint64_t *__restrict__ cand, uint64_t cap) {
+    int width, PruneState *__restrict__ st, unsigned long long *__restrict__ gt1,
+    uint64_t *__restrict__ cand, uint64_t cap, unsigned long long *__restrict__ total) {
+    constexpr int kStride = (1 << kMaxDigitBits) + 1;
     __shared__ uint64_t buf[kSplitLds];
-    __shared__ uint32_t n_buf;
+    __shared__ uint32_t hist[kCopies * kStride];
+    __shared__ uint64_t tot[1 << kMaxDigitBits];
+    __shared__ uint64_t wave_tot[kHistWaves];
+    __shared__ uint32_t n_buf, flag;
     __shared__ uint64_t base;
+    const bool single = st->single != 0;                // uniform
+    const uint32_t dlo = st->dlo, dhi = st->dhi;
+    const int bins = 1 << width;
     if (threadIdx.x == 0) n_buf = 0;
+    if (single)
+        for (int i = int(threadIdx.x); i < kCopies * kStride; i += kHistThreads) hist[i] = 0;
     __syncthreads();
-    const uint32_t d = st->prefix;
+    uint32_t *mine = hist + (int(threadIdx.x) & (kCopies - 1)) * kStride;
     const int lane = int(threadIdx.x) & (kWave - 1);
     int64_t cur = -1;
     uint32_t n_gt = 0;
@@ -327,7 +437,7 @@ __global__ __launch_bounds__(kHistThreads) void prune_split_kernel(
     };
     constexpr int K = PruneTraits<Bits>::UNROLL * PruneTraits<Bits>::VEC;
     for_each_round<Bits, ALIGNED>(
-        W, ldw, M, N, per_wave,
+        W, ldw, M, N, per_wave, per_wave,
         [&](int64_t r) {
             if (r != cur) {
                 flush();
@@ -335,15 +445,21 @@ __global__ __launch_bounds__(kHistThreads) void prune_split_kernel(
             }
         },
         [&](const uint32_t (&keys)[K], uint32_t mask) {
-            // branch-free over the round's keys: the count above d and a mask of the
-            // candidates; then one wave scan and one LDS atomic place them all
+            // branch-free over the round's keys: the count above the bracket and a
+            // mask of the candidates; then one wave scan and one LDS atomic place
+            // them all
             uint32_t cm = 0;
 #pragma unroll
             for (int j = 0; j < K; ++j) {
                 const uint32_t top = keys[j] >> shift;
                 const bool in = (mask >> j) & 1u;
-                n_gt += (in && top > d) ? 1u : 0u;
-                cm |= (in && top == d) ? (1u << j) : 0u;
+                n_gt += (in && top > dhi) ? 1u : 0u;
+                cm |= (in && top >= dlo && top <= dhi) ? (1u << j) : 0u;
+            }
+            if (single) {                               // uniform
+#pragma unroll
+                for (int j = 0; j < K; ++j)
+                    if ((mask >> j) & 1u) atomicAdd(&mine[keys[j] >> shift], 1u);
             }
             const uint32_t c = uint32_t(__popc(cm));
             uint32_t incl = c;
@@ -352,10 +468,10 @@ __global__ __launch_bounds__(kHistThreads) void prune_split_kernel(
                 const uint32_t t = __shfl_up(incl, o, kWave);
                 incl += lane >= o ? t : 0u;
             }
-            const uint32_t total = __shfl(incl, kWave - 1, kWave);
-            if (total) {                                // wave-uniform
+            const uint32_t total_c = __shfl(incl, kWave - 1, kWave);
+            if (total_c) {                              // wave-uniform
                 uint32_t at = 0;
-                if (lane == 0) at = atomicAdd(&n_buf, total);
+                if (lane == 0) at = atomicAdd(&n_buf, total_c);
                 at = __shfl(at, 0, kWave);
                 uint32_t pos = at + incl - c;
                 while (cm) {
@@ -381,6 +497,14 @@ __global__ __launch_bounds__(kHistThreads) void prune_split_kernel(
     __syncthreads();
     if (n <= kSplitLds && base + n <= cap)
         for (uint32_t i = threadIdx.x; i < n; i += kHistThreads) cand[base + i] = buf[i];
+    if (!single) return;                                // uniform
+    for (int b = int(threadIdx.x); b < bins; b += kHistThreads) {
+        uint32_t s = 0;
+#pragma unroll
+        for (int c = 0; c < kCopies; ++c) s += hist[c * kStride + b];
+        if (s) atomicAdd(&total[b], (unsigned long long)s);
+    }
+    if (last_workgroup(st, &flag)) select_digit(total, width, st, tot, wave_tot, kCheckBracket);
 }
 
 // counts[r] (= keys > t) += the keys == t taken in ascending row order, need in
@@ -478,7 +602,7 @@ __global__ __launch_bounds__(kHistThreads) void prune_count_kernel(
         // flush the previous row's counts when the wave moves on to a new row (all
         // lanes take part in the reduction)
         for_each_key<Bits, ALIGNED>(
-            W, ldw, M, N, per_wave,
+            W, ldw, M, N, per_wave, per_wave,
             [&](int64_t r) {
                 if (r != cur) {
                     flush();
@@ -514,6 +638,9 @@ __global__ __launch_bounds__(256) void prune_init_kernel(int64_t M, int64_t k, P
         st->n_cand = 0;
         st->n_last = 0;
         st->done = 0;
+        st->single = 0;
+        st->dlo = 0;
+        st->dhi = 0;
     }
 }
 
@@ -618,28 +745,44 @@ hipError_t launch_prune_t(int64_t M, int64_t N, const void *Wv, int64_t ldw, int
     const int passes = Tr::KEY_BITS == 31 ? 3 : 2;
     const uint64_t cap = uint64_t(cand_capacity(M, N));
     auto *gt1_u = reinterpret_cast<unsigned long long *>(w.gt1);
+    // more predicted candidates than this and the sample's bracket is not used
+    const uint64_t cand_limit =
+        std::min<uint64_t>(cap / 2, uint64_t(groups) * uint64_t(kSplitLds) / 2);
+    auto hist = [&](int grid, int64_t pw, int64_t stride, int shift, int width, int from_cand,
+                    int role) {
+        if (aligned)
+            hipLaunchKernelGGL((prune_hist_kernel<Bits, true>), dim3(grid), dim3(kHistThreads),
+                               0, s, W, ldw, M, N, pw, stride, shift, width, st, total_u, w.cand,
+                               from_cand, role, cand_limit);
+        else
+            hipLaunchKernelGGL((prune_hist_kernel<Bits, false>), dim3(grid), dim3(kHistThreads),
+                               0, s, W, ldw, M, N, pw, stride, shift, width, st, total_u, w.cand,
+                               from_cand, role, cand_limit);
+    };
     int hi = Tr::KEY_BITS;
     for (int p = 0; p < passes; ++p) {
         const int width = widths[p];
         const int shift = hi - width;
-        const int from_cand = p > 0;
-        if (aligned)
-            hipLaunchKernelGGL((prune_hist_kernel<Bits, true>), dim3(groups), dim3(kHistThreads),
-                               0, s, W, ldw, M, N, per_wave, shift, width, st, total_u, w.cand,
-                               from_cand);
-        else
-            hipLaunchKernelGGL((prune_hist_kernel<Bits, false>), dim3(groups), dim3(kHistThreads),
-                               0, s, W, ldw, M, N, per_wave, shift, width, st, total_u, w.cand,
-                               from_cand);
-        if (p == 0 && split) {                          // first digit chosen: split W once
+        if (p == 0 && split) {
+            // the sample (one vector per lane out of about every kSampleEvery, the
+            // stride drifting by an odd number of vectors so that it does not follow
+            // power-of-two rows) proposes the bracket; the full first-digit
+            // histogram runs only when the bracket would hold too many candidates;
+            // the split pass then reads W once
+            const int64_t chunk = kSampleChunk * int64_t(kWave) * Tr::VEC;
+            hist(std::min(groups, kSampleGroups), chunk,
+                 kSampleEvery * chunk + kSampleDrift * Tr::VEC, shift, width, 0, kRoleSample);
+            hist(groups, per_wave, per_wave, shift, width, 0, kRoleFirst);
             if (aligned)
                 hipLaunchKernelGGL((prune_split_kernel<Bits, true>), dim3(groups),
-                                   dim3(kHistThreads), 0, s, W, ldw, M, N, per_wave, shift, st,
-                                   gt1_u, w.cand, cap);
+                                   dim3(kHistThreads), 0, s, W, ldw, M, N, per_wave, shift, width,
+                                   st, gt1_u, w.cand, cap, total_u);
             else
                 hipLaunchKernelGGL((prune_split_kernel<Bits, false>), dim3(groups),
-                                   dim3(kHistThreads), 0, s, W, ldw, M, N, per_wave, shift, st,
-                                   gt1_u, w.cand, cap);
+                                   dim3(kHistThreads), 0, s, W, ldw, M, N, per_wave, shift, width,
+                                   st, gt1_u, w.cand, cap, total_u);
+        } else {
+            hist(groups, per_wave, per_wave, shift, width, p > 0, kRoleDigit);
         }
         hi = shift;
     }

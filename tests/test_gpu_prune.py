@@ -179,6 +179,23 @@ def test_whole_pipeline_on_device(darb, name):
         assert (err <= tol * scale).all()
 
 
+def test_biased_sample_falls_back_to_w(darb):
+    # from 64 MiB the first digit's candidates come from a bracket proposed by a
+    # sample of W (ranges at a fixed stride) and checked against the full
+    # histogram of the split pass.  Rows exactly one sample stride long put every
+    # sampled range at the same columns (the first 1024, with the library's present
+    # sample); values spread over 20 octaves only there make the sample propose a
+    # narrow bracket near the top while the true threshold lies in the rest of W,
+    # so the check must send the later passes back to W, with the oracle's counts.
+    rng = np.random.default_rng(5)
+    M, N = 512, 32 * 1024 + 37 * 4
+    W = rng.uniform(0.0, 0.5, size=(M, N)).astype(np.float32)
+    W[:, :1024] = np.exp2(rng.uniform(0.0, 20.0, size=(M, 1024))).astype(np.float32)
+    k = int(0.05 * M * N)
+    say(f"biased sample: {M}x{N} fp32, k = {k}")
+    assert np.array_equal(gpu_counts(darb, dev(W), k), oracle.prune_counts(W, k))
+
+
 @pytest.mark.parametrize("case", ["candidates_fit", "candidate_room_overflows",
                                   "workgroup_lds_overflows"])
 def test_split_pass_paths(darb, case):
