@@ -179,6 +179,24 @@ def test_whole_pipeline_on_device(darb, name):
         assert (err <= tol * scale).all()
 
 
+@pytest.mark.parametrize("kind", ["normal", "ties"])
+def test_fp16_sampled_bracket(darb, kind):
+    # 64 MiB of fp16 takes the sample and split path (8-bit first digit): normal
+    # values kept at 0.5 % give a one-digit bracket with room for its keys; 61
+    # distinct magnitudes kept at 5 % put 1.6 % of W in the threshold's digit, more
+    # than half the room, so the full first-digit histogram runs before the split
+    rng = np.random.default_rng(8)
+    M, N = 512, 65536
+    if kind == "normal":
+        W = (rng.standard_normal((M, N)) * 0.7).astype(np.float16)
+        k = int(0.005 * M * N)
+    else:
+        W = (rng.integers(-60, 61, size=(M, N)) * 0.015625).astype(np.float16)
+        k = int(0.05 * M * N)
+    say(f"fp16 sampled bracket ({kind}): {M}x{N}, k = {k}")
+    assert np.array_equal(gpu_counts(darb, dev(W), k), oracle.prune_counts(W, k))
+
+
 def test_biased_sample_falls_back_to_w(darb):
     # from 64 MiB the first digit's candidates come from a bracket proposed by a
     # sample of W (ranges at a fixed stride) and checked against the full
