@@ -261,10 +261,10 @@ int darb_spmm_i8(const darb_plan *plan, const int8_t *codes, const float *scales
  *   k          0 <= k <= M * N
  *   counts     device int64 [M], 8-byte aligned, overwritten
  *   workspace  device, 256-byte aligned, >= the size darb_prune_workspace
- *              returns (about M*N/4 bytes: room for the keys that share the
- *              threshold's leading digit, which the later passes read instead
- *              of W when W has 64 MiB or more); its contents on entry do not
- *              matter
+ *              returns (about M*N/4 bytes: room for the keys whose leading digit
+ *              lies in a small bracket around the threshold's, which the later
+ *              passes read instead of W when W has 64 MiB or more); its contents
+ *              on entry do not matter
  * Work is enqueued on `stream` only (several kernels, no host synchronisation);
  * calls sharing a workspace must not overlap.
  * Errors: DARB_E_INVALID, DARB_E_DTYPE, DARB_E_WORKSPACE, DARB_E_HIP.

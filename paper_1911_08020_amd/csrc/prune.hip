@@ -11,23 +11,27 @@
 // counts the current digit of the keys that match the digits chosen so far (one
 // LDS histogram per workgroup, four interleaved copies so lanes with equal digits
 // rarely hit the same address; each workgroup then adds its non-zero bins into the
-// global totals), and a one-workgroup kernel picks the digit where the count from
-// the top reaches the remaining K.  Finally, per row, the keys > t are counted and
-// the keys == t taken in flat order, which for row counts means rows in ascending
-// order.
+// global totals), and the workgroup that finishes the pass last (a counter in the
+// state tells it) picks the digit where the count from the top reaches the
+// remaining K.  Finally, per row, the keys > t are counted and the keys == t taken
+// in flat order, which for row counts means rows in ascending order (by the count
+// pass's last workgroup).
 //
-// Only the first pass streams all of W.  The second one (split) counts, per row,
-// the keys whose first digit is above the chosen one and copies the keys whose
-// first digit equals it -- the candidates, typically about 1 % of W -- with their
-// rows into the workspace; the remaining digits and the final counts then read the
-// candidates only.  Each workgroup gathers its candidates in LDS and reserves room
-// for them with one atomic; if a workgroup's LDS or the workspace's candidate
-// room overflows, every later pass streams W instead (the result is the same).
-// Below 64 MiB of W the split pass is skipped: there a pass over W costs less than
-// the extra launches.
-// Each histogram pass picks its digit in the workgroup that finishes last (a
-// counter in the state tells it), and the count pass's last workgroup takes the
-// keys equal to t, so a call is six launches.
+// From 64 MiB of W one pass streams all of W.  A sample of W (about 1/32) first
+// proposes a bracket of first digits that holds the K-th key's, with a margin of
+// six binomial standard deviations.  The split pass then counts, per row, the keys
+// whose first digit is above the bracket and copies the keys inside it -- the
+// candidates, typically about 1 % of W -- with their rows into the workspace; it
+// also takes the exact first-digit histogram, and its last workgroup picks the
+// first digit and checks it against the bracket.  The remaining digits and the
+// final counts read the candidates only.  Each workgroup gathers its candidates in
+// LDS and reserves room for them with one atomic; if a workgroup's LDS or the
+// workspace's candidate room overflows, or the first digit lies outside the
+// bracket, every later pass streams W instead (the result is the same).  When the
+// sample predicts more candidates than half the room, the exact first-digit
+// histogram runs over W before the split, which then keeps that digit only.
+// Below 64 MiB of W there is no sample and no split: every pass streams W, which
+// there costs less than the extra launches.
 // All state stays on the device; nothing returns to the host between passes.
 #include <algorithm>
 
@@ -162,7 +166,7 @@ __device__ __forceinline__ void for_each_round(const Bits *__restrict__ W, int64
     }
 }
 
-// As for_each_round, with f(key) for every element inside the segment (per lane).
+// As for_each_round, with f(key) for every element inside the row (per lane).
 template <typename Bits, bool ALIGNED, typename U, typename F>
 __device__ __forceinline__ void for_each_key(const Bits *__restrict__ W, int64_t ldw, int64_t M,
                                              int64_t N, int64_t per_wave, int64_t range_stride,
