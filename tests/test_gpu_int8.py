@@ -15,6 +15,7 @@ import pytest
 
 import oracle
 import workloads
+from tests._parity import compare
 
 pytestmark = pytest.mark.gpu
 
@@ -54,15 +55,8 @@ def quantize_both(darb, plan, lay, vals):
 
 
 def check_i8_product(Y, q, s, offs, lay, X, label):
-    ref = oracle.spmm_i8(q, s, offs, lay, X)
-    scale = oracle.spmm_i8_absdot(q, s, offs, lay, X)
-    Y = np.asarray(Y, dtype=np.float64).reshape(ref.shape)
-    zero = scale == 0
-    assert np.all(Y[zero] == 0.0), label
-    rel = np.abs(Y - ref)[~zero] / scale[~zero]
-    worst = float(rel.max()) if rel.size else 0.0
-    say(f"  {label}: max rel err {worst:.3e}")
-    assert worst <= TOL, label
+    compare(Y, oracle.spmm_i8(q, s, offs, lay, X), oracle.spmm_i8_absdot(q, s, offs, lay, X),
+            TOL, label)
 
 
 def plan_for(darb, W, d, D, bmin, bmax):

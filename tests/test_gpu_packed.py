@@ -13,6 +13,7 @@ import pytest
 
 import oracle
 import workloads
+from tests._parity import compare
 
 pytestmark = pytest.mark.gpu
 
@@ -42,15 +43,8 @@ def host(t) -> np.ndarray:
 
 
 def check_product(Y, vals, offs, lay, X, wdtype, label):
-    ref = oracle.spmm(vals, offs, lay, X)
-    scale = oracle.spmm_absdot(vals, offs, lay, X)
-    Y = np.asarray(Y, dtype=np.float64).reshape(ref.shape)
-    zero = scale == 0
-    assert np.all(Y[zero] == 0.0), label
-    rel = np.abs(Y - ref)[~zero] / scale[~zero]
-    worst = float(rel.max()) if rel.size else 0.0
-    say(f"  {label}: max rel err {worst:.3e}")
-    assert worst <= TOL[np.dtype(wdtype)], label
+    compare(Y, oracle.spmm(vals, offs, lay, X), oracle.spmm_absdot(vals, offs, lay, X),
+            TOL[np.dtype(wdtype)], label)
 
 
 def setup(darb, W, d, D, bmin, bmax):

@@ -13,6 +13,7 @@ import pytest
 
 import oracle
 import workloads
+from tests._parity import compare
 
 pytestmark = pytest.mark.gpu
 
@@ -44,16 +45,8 @@ def host(t) -> np.ndarray:
 
 
 def check_product(Y, vals, offs, lay, X, wdtype, label=""):
-    ref = oracle.spmm(vals, offs, lay, X)
-    scale = oracle.spmm_absdot(vals, offs, lay, X)
-    Y = np.asarray(Y, dtype=np.float64).reshape(ref.shape)
-    err = np.abs(Y - ref)
-    zero = scale == 0
-    assert np.all(Y[zero] == 0.0), f"{label}: nonzero output where every term is 0"
-    rel = err[~zero] / scale[~zero]
-    worst = float(rel.max()) if rel.size else 0.0
-    say(f"  {label}: max rel err {worst:.3e} (tol {TOL[np.dtype(wdtype)]:.0e})")
-    assert worst <= TOL[np.dtype(wdtype)], label
+    compare(Y, oracle.spmm(vals, offs, lay, X), oracle.spmm_absdot(vals, offs, lay, X),
+            TOL[np.dtype(wdtype)], label)
 
 
 def encode_both(darb, W, d, D, mode, bmin, bmax, W_dev=None):
@@ -429,6 +422,5 @@ def test_spmv_workgroups_take_several_blocks(darb):
     assert np.array_equal(y.view(np.uint32), yp.view(np.uint32))
     q, s = oracle.quantize_i8(vals, lay)
     y8 = host(plan.spmv_i8(dev(q), dev(s), dev(x), packed=packed))
-    ref = oracle.spmm_i8(q, s, offs, lay, x)
-    scale = oracle.spmm_i8_absdot(q, s, offs, lay, x)
-    assert (np.abs(y8.astype(np.float64) - ref) <= 1e-5 * scale).all()
+    compare(y8, oracle.spmm_i8(q, s, offs, lay, x), oracle.spmm_i8_absdot(q, s, offs, lay, x),
+            1e-5, "looping spmv INT8")

@@ -12,6 +12,7 @@ import pytest
 
 import oracle
 import workloads
+from tests._parity import compare
 
 pytestmark = pytest.mark.gpu
 
@@ -172,11 +173,9 @@ def test_whole_pipeline_on_device(darb, name):
     assert np.array_equal(packed.cpu().numpy()[:plan.packed_words].view(np.uint32),
                           oracle.pack_offsets(orf, lay))
     tol = 1e-5 if mi.W.dtype == np.float32 else 2e-3
-    for got, act in ((y.cpu().numpy(), x), (Y.cpu().numpy(), X)):
-        ref = oracle.spmm(vr, orf, lay, act)
-        scale = oracle.spmm_absdot(vr, orf, lay, act)
-        err = np.abs(np.asarray(got, dtype=np.float64).reshape(ref.shape) - ref)
-        assert (err <= tol * scale).all()
+    for got, act, what in ((y.cpu().numpy(), x, "spmv"), (Y.cpu().numpy(), X, "spmm")):
+        compare(got, oracle.spmm(vr, orf, lay, act), oracle.spmm_absdot(vr, orf, lay, act), tol,
+                f"pruned {what}")
 
 
 @pytest.mark.parametrize("kind", ["normal", "ties"])

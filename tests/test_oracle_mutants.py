@@ -40,6 +40,23 @@ MUTANTS = {
                          "key = ((const uint32_t *)W)[r * ldw + c];")],
     "prune_keeps_one_less": [("for (int64_t i = 0; i < k; ++i) counts",
                               "for (int64_t i = 1; i < k; ++i) counts")],
+    # the error scale of the product checks, sum_k |v_k * x_k|
+    "absdot_fabs_dropped": [("a[j] += fabs(v * load_elem(xdtype, X, c * ldx + j));",
+                             "a[j] += v * load_elem(xdtype, X, c * ldx + j);")],
+    "absdot_term_doubled": [("a[j] += fabs(v * load_elem(xdtype, X, c * ldx + j));",
+                             "a[j] += 2.0 * fabs(v * load_elem(xdtype, X, c * ldx + j));")],
+    "absdot_offset_dropped": [("a[j] += fabs(v * load_elem(xdtype, X, c * ldx + j));",
+                               "a[j] += fabs(v * load_elem(xdtype, X, (k * b) * ldx + j));")],
+    "absdot_batch_column_fixed": [("a[j] += fabs(v * load_elem(xdtype, X, c * ldx + j));",
+                                   "a[j] += fabs(v * load_elem(xdtype, X, c * ldx));")],
+    "absdot_sums_all_columns": [
+        ("for (int64_t j = 0; j < B; ++j) a[j] += fabs(v * load_elem(xdtype, X, c * ldx + j));",
+         "for (int64_t j = 0; j < B; ++j) for (int64_t i = 0; i < B; ++i) "
+         "a[j] += fabs(v * load_elem(xdtype, X, c * ldx + i));")],
+    "i8_absdot_scale_dropped": [("py", "return A * (s if A.ndim == 1 else s[:, None])",
+                                 "return A")],
+    "i8_absdot_scale_signed": [("py", "s = np.abs(np.asarray(scales, dtype=np.float64))",
+                                "s = np.asarray(scales, dtype=np.float64)")],
     # INT8 values (edits of the Python wrapper, where that arithmetic lives)
     "i8_round_half_up": [("py", "q = np.rint(row * inv)",
                           "q = np.floor(row * inv + np.float32(0.5))")],
@@ -129,6 +146,23 @@ def pin_suite(orc):
     assert [q[int(lay.row_start[r]):int(lay.row_start[r]) + int(lay.nblk[r])].tolist()
             for r in range(3)] == [[127, 2, -4, 0], [-127, 64], [0]]
     assert s.tolist() == [1.0, float(np.float32(2.0) / np.float32(127.0)), 0.0]
+    # the products' error scale against a library matmul of the magnitudes, and its
+    # INT8 form with scales of either sign
+    lay = orc.layout(37, np.array([0, 2, 5, 3, 7], dtype=np.uint8))
+    W = rng.standard_normal((5, 37)).astype(np.float32)
+    v, o = orc.encode(W, lay)
+    Wa = np.abs(orc.decode(v, o, lay).astype(np.float64))
+    for B in (1, 3):
+        X = rng.standard_normal((37, B)).astype(np.float32)
+        act = X[:, 0].copy() if B == 1 else X
+        assert np.allclose(orc.spmm_absdot(v, o, lay, act), Wa @ np.abs(act.astype(np.float64)),
+                           rtol=1e-14, atol=0)
+        q = rng.integers(-127, 128, size=lay.nnz).astype(np.int8)
+        sc = np.array([0.5, -2.0, 0.0, 1.5, -0.25], dtype=np.float32)
+        ref = np.abs(orc.decode(q.astype(np.float32), o, lay).astype(np.float64)) @ \
+            np.abs(act.astype(np.float64))
+        ref = ref * (np.abs(sc) if B == 1 else np.abs(sc)[:, None])
+        assert np.allclose(orc.spmm_i8_absdot(q, sc, o, lay, act), ref, rtol=1e-14, atol=0)
     # fp16 decoding of a few bit patterns against numpy
     for bits in [0x3C00, 0x0001, 0x7BFF, 0xC000, 0x0400]:
         assert orc.half_to_double(bits) == float(np.array([bits], np.uint16).view(np.float16)[0])

@@ -294,6 +294,72 @@ def test_product_equals_dense_masked_matmul(wdt, xdt):
     assert np.array_equal(y, Y[:, 0])
 
 
+# The error scale every product parity check divides by, sum_k |v_k * x_k| per
+# output, is pinned against a library matmul of the magnitudes: |decode(W)| @ |X|
+# has exactly the same terms (the masked matrix is zero off the kept columns).
+
+def _random_format(rng, wdt, M, N):
+    """A format over every block size 1..128 (rows cycle through them, N ragged)."""
+    W = rng.standard_normal((M, N)).astype(wdt)
+    W[rng.random((M, N)) < 0.05] = 0                    # exact zeros, both signs kept
+    log2b = (np.arange(M) % 8).astype(np.uint8)
+    rng.shuffle(log2b)
+    lay = oracle.layout(N, log2b)
+    v, o = oracle.encode(W, lay)
+    return lay, v, o
+
+
+@pytest.mark.parametrize("wdt,xdt", [(np.float32, np.float32), (np.float16, np.float16),
+                                     (np.float16, np.float32), (np.float32, np.float16)])
+@pytest.mark.parametrize("B", [1, 6])
+def test_error_scale_equals_abs_matmul(wdt, xdt, B):
+    rng = np.random.default_rng(21 + B)
+    for M, N in [(16, 300), (11, 1), (24, 129), (9, 1000)]:
+        lay, v, o = _random_format(rng, wdt, M, N)
+        X = rng.standard_normal((N, B)).astype(xdt)
+        X[rng.random((N, B)) < 0.05] = 0
+        act = X[:, 0].copy() if B == 1 else X
+        A = oracle.spmm_absdot(v, o, lay, act)
+        ref = np.abs(oracle.decode(v, o, lay).astype(np.float64)) @ \
+            np.abs(act.astype(np.float64))
+        assert A.shape == ref.shape == ((M,) if B == 1 else (M, B))
+        assert np.array_equal(A == 0, ref == 0)
+        assert np.all(np.abs(A - ref) <= 1e-14 * ref), (M, N)
+
+
+def test_error_scale_is_abs_of_product_when_terms_share_sign():
+    """With W >= 0 and X >= 0 no term cancels: the scale equals the product itself,
+    and with mixed signs it bounds the product's magnitude."""
+    rng = np.random.default_rng(23)
+    lay, v, o = _random_format(rng, np.float32, 20, 257)
+    X = rng.standard_normal((257, 4)).astype(np.float32)
+    A = oracle.spmm_absdot(v, o, lay, X)
+    assert np.all(np.abs(oracle.spmm(v, o, lay, X)) <= A * (1 + 1e-14))
+    vp, Xp = np.abs(v), np.abs(X)
+    assert np.allclose(oracle.spmm_absdot(vp, o, lay, Xp), oracle.spmm(vp, o, lay, Xp),
+                       rtol=1e-14, atol=0)
+
+
+def test_int8_error_scale_equals_abs_matmul():
+    """|s_r| * (|Dq| @ |X|), Dq the decoded matrix of the codes; scales of either sign."""
+    rng = np.random.default_rng(25)
+    for B in (1, 5):
+        lay, v, o = _random_format(rng, np.float32, 18, 333)
+        q = rng.integers(-127, 128, size=lay.nnz).astype(np.int8)
+        s = rng.standard_normal(lay.M).astype(np.float32)
+        s[::5] = 0
+        X = rng.standard_normal((lay.N, B)).astype(np.float32)
+        act = X[:, 0].copy() if B == 1 else X
+        A = oracle.spmm_i8_absdot(q, s, o, lay, act)
+        Dq = oracle.decode(q.astype(np.float32), o, lay).astype(np.float64)
+        ref = np.abs(Dq) @ np.abs(act.astype(np.float64))
+        ref = ref * (np.abs(s.astype(np.float64)) if B == 1 else
+                     np.abs(s.astype(np.float64))[:, None])
+        assert A.shape == ref.shape
+        assert np.all(np.abs(A - ref) <= 1e-14 * ref)
+        assert np.all(A[s == 0] == 0)
+
+
 def test_product_with_unit_vector_returns_masked_column():
     rng = np.random.default_rng(6)
     M, N = 30, 90
