@@ -1,20 +1,28 @@
 #!/usr/bin/env python3
-"""DARB benchmark on one MI355X: BMWM encode + SpMV (batch 1) + SpMM (batch 64).
+"""DARB benchmark on one MI355X: SpMV (batch 1) and SpMM (batch 64) over the DARB format.
 
-One step is one pass of the DARB hot path over the FC-head workload
-(W fp32 [4096 x 9216], Laplace weights, 4 % irregular keep, block sizes 8..128):
+Workload: the FC-head matrix (W fp32 [4096 x 9216], Laplace weights, 4 % irregular
+keep, block sizes 8..128), encoded on the device with BMWM.  The metric is the
+products' effective bandwidth and rate: ``value`` is the SpMV's algorithmic bytes
+divided by its average kernel time, in GB/s; the SpMM (B = 64) figures and the
+whole step's are extra keys.
+
+One step (the timed loop, ``ms_per_step``) is one pass of the whole hot path:
     darb_encode(W)  ->  darb_spmv(x)  ->  darb_spmm(X, B = 64)
-The plan (block sizes and layout from the row densities) is host work done once
-per matrix and is timed separately.  All inputs are resident in HBM before the
-timed region.  To measure HBM rather than the 256 MB Infinity Cache, every
-kernel of a step reads buffers not touched for the previous several steps:
-W rotates over ``--rotate-w`` copies (151 MB each) and the encoded matrix /
-activations over ``--rotate-fmt`` copies; the products of step i read the copy
-encoded ``--rotate-fmt - 1`` steps earlier (identical contents).
+Inputs are resident in HBM before any timed region.  To measure HBM rather than
+the 256 MB Infinity Cache, every launch reads buffers not touched recently: W
+rotates over ``--rotate-w`` copies (151 MB each) and the format and activations
+over ``--rotate-fmt`` copies (>= 64, over 540 MB); the products of step i read
+the copy encoded several steps earlier (identical contents).
 
-Prints one JSON line.  ``value`` is the step's algorithmic bytes divided by the
-wall time per step (GB/s).  Per-kernel durations come from HIP events on the
-launch stream around K back-to-back launches of each kernel (same rotation).
+Per-kernel times: for each kernel, at least 256 launches (whatever ``--steps``
+says) rotating over the same copies are enqueued behind a sleep kernel, so the
+host's enqueue cost cannot starve the GPU, and timed with HIP events on the
+launch stream; the average per launch is what the rocprofv3 kernel trace shows
+for the same kernel.  The same-size read floor is the fastest of several launch
+shapes of a plain read over buffers of the SpMV's size, same rotation.
+
+Prints one JSON line.
 """
 import argparse
 import json
@@ -28,9 +36,16 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0          # MI355X published HBM3E bandwidth
-FP32_PEAK_GFLOPS = 157300.0     # MI355X published fp32 vector rate
+# X-row gathers of the SpMM go through each CU's load path at 128 bytes per clock:
+# 256 CUs x 128 B x 2.4 GHz
+GATHER_PEAK_GBPS = 256 * 128 * 2.4
+MIN_LAUNCHES = 256
+MIN_ROTATION_BYTES = 512 << 20  # > 2x the 256 MB Infinity Cache
 
 METRIC = "DARB SpMV/SpMM effective GB/s (% of HBM peak) and GFLOP/s, batch 1 & 64"
+
+READ_SHAPES = [(256, 1), (256, 2), (256, 4), (256, 8), (512, 1), (512, 2), (512, 4),
+               (1024, 1), (1024, 2), (64, 4), (128, 4)]
 
 
 def parse_args(argv=None):
@@ -42,9 +57,11 @@ def parse_args(argv=None):
     ap.add_argument("--batch", type=int, default=None,
                     help="SpMM batch (default: the workload's own; 64 for fc_9216)")
     ap.add_argument("--rotate-w", type=int, default=4)
-    ap.add_argument("--rotate-fmt", type=int, default=8)
-    ap.add_argument("--cpu-seconds", type=float, default=10.0,
+    ap.add_argument("--rotate-fmt", type=int, default=64)
+    ap.add_argument("--cpu-seconds", type=float, default=20.0,
                     help="budget of the oracle timing on the host (0 disables)")
+    ap.add_argument("--no-recurrent", action="store_true",
+                    help="skip the recurrent-workload figures in the default line")
     ap.add_argument("--seed", type=int, default=0)
     return ap.parse_args(argv)
 
@@ -111,42 +128,121 @@ def stored_traffic(workload, batch):
     return out
 
 
-def cpu_baseline(cfg, mi, x, X, seconds, bytes_per_step):
-    """The oracle as it stands (plain C, fp64 sums, one thread) on the same step."""
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for ln in f:
+                if ln.startswith("model name"):
+                    return ln.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor() or platform.machine()
+
+
+def cpu_baseline(cfg, mi, x, X, seconds, nbytes):
+    """The oracle as it stands (plain C, fp64 sums) on the same workload: encode, SpMV
+    and SpMM (B = X's columns), each the median of >= 5 runs, on one thread and with
+    the rows split over every core this process may use (threads calling the oracle
+    on disjoint row ranges; the oracle's arithmetic is unchanged).  A reported
+    baseline, not a target."""
+    import statistics
+    from concurrent.futures import ThreadPoolExecutor
+
+    import numpy as np
+
     import oracle
     lay = oracle.plan(cfg.N, mi.row_density, mi.matrix_density, oracle.ROUND_FLOOR,
                       cfg.b_min, cfg.b_max)
-    reps = 0
-    t0 = time.perf_counter()
-    while True:
-        v, o = oracle.encode(mi.W, lay)
-        oracle.spmm(v, o, lay, x)
-        oracle.spmm(v, o, lay, X)
-        reps += 1
-        el = time.perf_counter() - t0
-        if el >= seconds:
-            break
-    return {"value": round(bytes_per_step * reps / el / 1e9, 3), "unit": "GB/s", "cores": 1,
-            "kind": "oracle",
-            "sample": f"the full {cfg.name} step (encode + SpMV + SpMM B={X.shape[1]}) "
-                      f"repeated {reps} times in {el:.1f} s, single thread, "
-                      f"{platform.processor() or platform.machine()}"}
+    affinity = len(os.sched_getaffinity(0))
+    cores = min(affinity, 16)       # the host share of one GPU on the test boxes
+    W = np.ascontiguousarray(mi.W)
+    v, o = oracle.encode(W, lay)
+    ranges = {1: [(0, cfg.M)]}
+    step = -(-cfg.M // cores)
+    ranges[cores] = [(r, min(cfg.M, r + step)) for r in range(0, cfg.M, step)]
+    budget = seconds / 6.0      # per op and thread count
+
+    def run(threads, op):
+        rs = ranges[threads]
+        pool = ThreadPoolExecutor(max_workers=threads)
+        try:
+            if op == "encode":
+                vv, oo = np.zeros_like(v), np.zeros_like(o)
+                fn = lambda r: oracle.encode_rows(W, lay, r[0], r[1], vv, oo)   # noqa: E731
+            else:
+                act = x if op == "spmv" else X
+                Y = np.zeros((cfg.M, 1 if act.ndim == 1 else act.shape[1]), dtype=np.float64)
+                fn = lambda r: oracle.spmm_rows(v, o, lay, act, r[0], r[1], Y)   # noqa: E731
+            times = []
+            t_end = time.perf_counter() + budget
+            while len(times) < 5 or (time.perf_counter() < t_end and len(times) < 50):
+                t0 = time.perf_counter()
+                list(pool.map(fn, rs))
+                times.append(time.perf_counter() - t0)
+            return statistics.median(times), len(times)
+        finally:
+            pool.shutdown()
+
+    per_op = {}
+    for threads in sorted(ranges):
+        for op in ("encode", "spmv", "spmm"):
+            t, n = run(threads, op)
+            per_op[f"{op}_{threads}t"] = {"median_ms": round(t * 1e3, 3), "runs": n,
+                                          "gbps": round(nbytes[op] / t / 1e9, 3)}
+    best = per_op[f"spmv_{cores}t"]
+    return {"value": best["gbps"], "unit": "GB/s", "cores": cores, "kind": "oracle",
+            "sample": f"{cfg.name} SpMV (B=1) over the full matrix, rows split over {cores} "
+                      f"threads, median of {best['runs']} runs; the oracle's fp64 loops as "
+                      f"they stand; CPU: {cpu_model()}",
+            "cpu_model": cpu_model(), "affinity_cores": affinity, "per_op": per_op}
 
 
-def bench_lstm(args):
+class Timer:
+    """Average per-launch GPU time of back-to-back launches, HIP events on the launch
+    stream.  The launches are enqueued behind a sleep kernel long enough to cover the
+    host's enqueue time, so the GPU runs them back to back."""
+
+    def __init__(self, torch, stream):
+        self.torch, self.stream = torch, stream
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        torch.cuda._sleep(1 << 20)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        self.cycles_per_us = (1 << 20) / (e0.elapsed_time(e1) * 1e3)
+
+    def __call__(self, fn, args_list, count, host_us_per_call=30.0):
+        torch = self.torch
+        rc = fn(*args_list[0])                       # first launch loads the code object
+        if rc:
+            raise RuntimeError(f"launch failed ({rc})")
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        torch.cuda._sleep(int(self.cycles_per_us * host_us_per_call * count))
+        e0.record(self.stream)
+        for i in range(count):
+            rc |= fn(*args_list[i % len(args_list)])
+        e1.record(self.stream)
+        torch.cuda.synchronize()
+        if rc:
+            raise RuntimeError(f"launch failed ({rc})")
+        return e0.elapsed_time(e1) * 1e3 / count
+
+
+def recurrent_figures(args, with_cpu):
     """The recurrent workload: 2-layer LSTM, hidden 1024, T = 200, batch 32, fp16 DARB
-    weights, fp32 state.  A step is one forward pass over the whole sequence (both
-    layers, darb_lstm_layer each).  The DARB weights are encoded once before timing
-    (model load); they stay cache-resident, as they would in a serving loop."""
+    weights, fp32 state.  One sequence = both layers (darb_lstm_layer each).  The
+    weights are encoded once before timing (model load) and stay cache-resident, as
+    in a serving loop.  Returns tokens/s, the per-step time of the fused step kernel
+    and the two products' times."""
     import ctypes
 
-    import numpy as np
     import torch
 
     import paper_1911_08020_amd as darb
     import workloads
 
-    torch.cuda.set_device(0)
     dev = torch.device("cuda", 0)
     cfg, mats, xs, shp = workloads.make_lstm_inputs(seed=args.seed)
     H, T, Bt = shp["hidden"], shp["seq_len"], shp["batch"]
@@ -174,11 +270,10 @@ def bench_lstm(args):
             darb.lstm_layer(wih, whh, inp, H, T, Bt, h=hh[l], c=cc[l], h_seq=hs[l], workspace=ws)
             inp = hs[l]
 
-    for _ in range(max(1, args.warmup // 10)):
-        sequence()
+    sequence()
     torch.cuda.synchronize()
     ref = hs[-1].clone()
-    K = max(1, args.steps // 20)
+    K = max(3, args.steps // 20)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(K):
@@ -187,71 +282,39 @@ def bench_lstm(args):
     ms = (time.perf_counter() - t0) * 1e3 / K
     assert torch.equal(hs[-1], ref), "sequence output changed across runs"
 
-    # per-kernel averages of the two product shapes, back-to-back between events
     stream = torch.cuda.current_stream()
+    timer = Timer(torch, stream)
     lib = darb.lib()
     P = ctypes.c_void_p
-    plan, v, o = layers[0][0]
     Uo = torch.empty((4 * H, T * Bt), dtype=torch.float32, device=dev)
     Go = torch.empty((4 * H, Bt), dtype=torch.float32, device=dev)
-    reps = 50
     res = {}
-    for name, (pl, vv, oo), X, Y, B in (("input_product", layers[0][0], x_seq, Uo, T * Bt),
-                                        ("recurrent_product", layers[0][1], hh[0], Go, Bt)):
-        a = (pl.handle, darb.F16, P(vv.data_ptr()), P(oo.data_ptr()), darb.F32, B,
-             P(X.data_ptr()), B, P(Y.data_ptr()), B, P(stream.cuda_stream))
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        torch.cuda.synchronize()
-        e0.record(stream)
-        for _ in range(reps):
-            lib.darb_spmm(*a)
-        e1.record(stream)
-        torch.cuda.synchronize()
-        us = e0.elapsed_time(e1) * 1e3 / reps
+    for name, (pl, vv, oo), X, Y, B, reps in (("input_product", layers[0][0], x_seq, Uo, T * Bt, 20),
+                                              ("recurrent_product", layers[0][1], hh[0], Go, Bt,
+                                               MIN_LAUNCHES)):
+        a = [(pl.handle, darb.F16, P(vv.data_ptr()), P(oo.data_ptr()), darb.F32, B,
+              P(X.data_ptr()), B, P(Y.data_ptr()), B, P(stream.cuda_stream))]
+        us = timer(lib.darb_spmm, a, reps)
         res[name] = {"avg_us": round(us, 3), "batch": B,
                      "gflops": round(2 * pl.nnz * B / (us * 1e-6) / 1e9, 1)}
-    flops = sum(2 * n * T * Bt for n in nnz)
-    # the dominant kernel by total time is the time step (T launches per layer): its
-    # average from the layer's time minus its input product, between events
+    # the fused time step: the layer's time minus its input product, over T steps
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     wih, whh = layers[0]
     torch.cuda.synchronize()
     e0.record(stream)
     for _ in range(3):
-        hh[0].zero_()
-        cc[0].zero_()
         darb.lstm_layer(wih, whh, x_seq, H, T, Bt, h=hh[0], c=cc[0], h_seq=hs[0], workspace=ws)
     e1.record(stream)
     torch.cuda.synchronize()
     layer_us = e0.elapsed_time(e1) * 1e3 / 3
     step_us = (layer_us - res["input_product"]["avg_us"]) / T
-    rp = whh[0]
-    # per step: the recurrent format, h_{t-1} once, the step's input products, c read
-    # and written, h_t written twice (state and sequence), the per-row table of 4H rows
-    step_bytes = rp.nnz * (2 + 1) + H * Bt * 4 + 4 * H * Bt * 4 + 2 * H * Bt * 4 + \
-        2 * H * Bt * 4 + 8 * rp.M
-    res["step"] = {"avg_us": round(step_us, 3), "derived_from_layer_us": round(layer_us, 1)}
-    step_gbps = step_bytes / (step_us * 1e-6) / 1e9
-    roofline = {"kernel": "lstm_step", "bound": "hbm", "achieved": round(step_gbps, 1),
-                "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(step_gbps / HBM_PEAK_GBPS, 4),
-                "traffic": None,
-                "note": "latency-bound: about 2 MB per launch, W_hh cache-resident"}
-    out = {
-        "metric": "DARB 2-layer LSTM forward tokens/s (hidden 1024, T=200, batch 32)",
-        "value": round(T * Bt / (ms * 1e-3), 1), "unit": "tokens/s", "n_gpus": 1,
-        "steps": K, "warmup": max(1, args.warmup // 10), "ms_per_step": round(ms, 4),
-        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f16",
-        "data": "synthetic: seeded fp16 weights, exact-k irregular densities, N(0,1) inputs",
-        "config": {"workload": "lstm2_seq: 2-layer LSTM, hidden 1024, T=200, batch 32, "
-                               "W_ih and W_hh [4096 x 1024] fp16 DARB (keep 5 %, b 4..64); "
-                               "step = one forward pass over the sequence",
-                   "nnz_per_matrix": nnz},
-        "gflops_step": round(flops / (ms * 1e-3) / 1e9, 1),
-        "kernels": res,
-        "roofline": roofline,
-        "cpu_baseline": None,
-    }
-    if args.cpu_seconds > 0:
+    out = {"workload": "lstm2_seq: 2-layer LSTM, hidden 1024, T=200, batch 32, W_ih and W_hh "
+                       "[4096 x 1024] fp16 DARB (keep 5 %, b 4..64), fp32 state",
+           "tokens_per_s": round(T * Bt / (ms * 1e-3), 1), "ms_per_sequence": round(ms, 4),
+           "sequences": K, "us_per_step": round(step_us, 3),
+           "gflops": round(sum(2 * n * T * Bt for n in nnz) / (ms * 1e-3) / 1e9, 1),
+           "nnz_per_matrix": nnz, "kernels": res}
+    if with_cpu:
         import oracle
         masked = []
         for (wih, whh) in layers:
@@ -262,14 +325,34 @@ def bench_lstm(args):
                 pair.append(oracle.decode(vv.cpu().numpy(), oo.cpu().numpy(), lay))
             masked.append(tuple(pair))
         from threadpoolctl import threadpool_limits
-        with threadpool_limits(limits=1):
+        cores = len(os.sched_getaffinity(0))
+        with threadpool_limits(limits=cores):
             t0 = time.perf_counter()
             oracle.lstm_forward(masked, xs, H, T, Bt)
             el = time.perf_counter() - t0
-        out["cpu_baseline"] = {"value": round(T * Bt / el, 1), "unit": "tokens/s", "cores": 1,
-                               "kind": "oracle",
+        out["cpu_baseline"] = {"value": round(T * Bt / el, 1), "unit": "tokens/s",
+                               "cores": cores, "kind": "oracle",
                                "sample": f"one full sequence in {el:.1f} s (numpy fp64 dense "
-                                         "masked products, one BLAS thread)"}
+                                         f"masked products, {cores} BLAS threads)"}
+    return out
+
+
+def bench_lstm(args):
+    """``--workload lstm2_seq``: the recurrent workload as the headline."""
+    import torch
+    torch.cuda.set_device(0)
+    r = recurrent_figures(args, with_cpu=args.cpu_seconds > 0)
+    out = {
+        "metric": "DARB 2-layer LSTM forward tokens/s (hidden 1024, T=200, batch 32)",
+        "value": r["tokens_per_s"], "unit": "tokens/s", "n_gpus": 1, "steps": r["sequences"],
+        "warmup": 1, "ms_per_step": r["ms_per_sequence"], "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f16",
+        "data": "synthetic: seeded fp16 weights, exact-k irregular densities, N(0,1) inputs",
+        "config": {"workload": r["workload"] + "; step = one forward pass over the sequence",
+                   "nnz_per_matrix": r["nnz_per_matrix"]},
+        "gflops_step": r["gflops"], "us_per_time_step": r["us_per_step"], "kernels": r["kernels"],
+        "roofline": None, "cpu_baseline": r.get("cpu_baseline"),
+    }
     print(json.dumps(out), flush=True)
 
 
@@ -284,6 +367,8 @@ def main(argv=None):
 
     if args.workload == "lstm2_seq":
         return bench_lstm(args)
+
+    import ctypes
 
     import numpy as np
     import torch
@@ -306,20 +391,20 @@ def main(argv=None):
     s_w = 4 if cfg.wdtype == "f32" else 2
     s_x = 4 if cfg.xdtype == "f32" else 2
     RW, RE = args.rotate_w, args.rotate_fmt
+    with_spmm = B > 1
 
     Wd = [torch.from_numpy(mi.W).to(dev) for _ in range(RW)]
     fmt = [plan.empty_format(wdt, dev) for _ in range(RE)]
     xd = [torch.from_numpy(x).to(dev) for _ in range(RE)]
-    Xd = [torch.from_numpy(X).to(dev) for _ in range(RE)]
+    Xd = [torch.from_numpy(X).to(dev) for _ in range(RE)] if with_spmm else []
     y = torch.empty(cfg.M, dtype=torch.float32, device=dev)
     Y = torch.empty((cfg.M, B), dtype=torch.float32, device=dev)
     for v, o in fmt:
         plan.encode(Wd[0], v, o)
     torch.cuda.synchronize()
 
-    # Pre-bound C-ABI calls: the timed loop only enqueues (argument checks done once
+    # Pre-bound C-ABI calls: the timed loops only enqueue (argument checks done once
     # by the binding above; the library checks again on every call).
-    import ctypes
     lib = darb.lib()
     h = plan.handle
     wcode = darb.F32 if cfg.wdtype == "f32" else darb.F16
@@ -332,15 +417,14 @@ def main(argv=None):
     spmv_args = [(h, wcode, P(fmt[j][0].data_ptr()), P(fmt[j][1].data_ptr()), xcode,
                   P(xd[j].data_ptr()), P(y.data_ptr()), sp) for j in range(RE)]
     spmm_args = [(h, wcode, P(fmt[j][0].data_ptr()), P(fmt[j][1].data_ptr()), xcode, B,
-                  P(Xd[j].data_ptr()), B, P(Y.data_ptr()), B, sp) for j in range(RE)]
-
-    with_spmm = B > 1
+                  P(Xd[j].data_ptr()), B, P(Y.data_ptr()), B, sp) for j in range(RE)] \
+        if with_spmm else []
 
     def step(i):
         rc = lib.darb_encode(*enc_args[i % (RW * RE)])
-        rc |= lib.darb_spmv(*spmv_args[(i + 1) % RE])
+        rc |= lib.darb_spmv(*spmv_args[(i + 7) % RE])
         if with_spmm:
-            rc |= lib.darb_spmm(*spmm_args[(i + 2) % RE])
+            rc |= lib.darb_spmm(*spmm_args[(i + 13) % RE])
         if rc:
             raise RuntimeError(f"DARB call failed: {lib.darb_last_error().decode()}")
 
@@ -361,42 +445,51 @@ def main(argv=None):
     ms_per_step = (t_end - t_start) * 1e3 / K
     host_us = (t_enq - t_start) * 1e6 / K
 
-    # per-kernel durations: for each kernel, K back-to-back launches (same rotation
-    # as the steps) between two HIP events on the launch stream; average = elapsed / K
-    def timed_launches(fn, args_list, count):
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        torch.cuda.synchronize()
-        e0.record(stream)
-        rc = 0
-        for i in range(count):
-            rc |= fn(*args_list[i % len(args_list)])
-        e1.record(stream)
-        torch.cuda.synchronize()
-        if rc:
-            raise RuntimeError(f"DARB call failed: {lib.darb_last_error().decode()}")
-        return e0.elapsed_time(e1) * 1e3 / count
-
-    spmv_rot = [spmv_args[(i + 1) % RE] for i in range(RE)]
-    spmm_rot = [spmm_args[(i + 2) % RE] for i in range(RE)]
-    avg_us = {"encode": timed_launches(lib.darb_encode, enc_args, K),
-              "spmv": timed_launches(lib.darb_spmv, spmv_rot, K)}
+    timer = Timer(torch, stream)
+    NL = max(K, MIN_LAUNCHES)
+    spmv_rot = [spmv_args[(i + 7) % RE] for i in range(RE)]
+    avg_us = {"encode": timer(lib.darb_encode, enc_args, NL),
+              "spmv": timer(lib.darb_spmv, spmv_rot, NL)}
     if with_spmm:
-        avg_us["spmm"] = timed_launches(lib.darb_spmm, spmm_rot, K)
+        avg_us["spmm"] = timer(lib.darb_spmm, [spmm_args[(i + 13) % RE] for i in range(RE)], NL)
     names = ["encode", "spmv", "spmm"] if with_spmm else ["encode", "spmv"]
     nbytes = step_bytes(cfg.M, cfg.N, plan.nnz, s_w, s_x, B)
-    if not with_spmm:
-        nbytes.pop("spmm")
     flops = {"encode": 0, "spmv": 2 * plan.nnz, "spmm": 2 * plan.nnz * B}
     kernels = {}
     for n in names:
         us = avg_us[n]
         gbps = nbytes[n] / (us * 1e-6) / 1e9
         kernels[n] = {
-            "avg_us": round(us, 3), "bytes": int(nbytes[n]), "flops": int(flops[n]),
-            "gbps": round(gbps, 1), "frac_hbm_peak": round(gbps / HBM_PEAK_GBPS, 4),
+            "avg_us": round(us, 3), "launches": NL, "bytes": int(nbytes[n]),
+            "flops": int(flops[n]), "gbps": round(gbps, 1),
+            "frac_hbm_peak": round(gbps / HBM_PEAK_GBPS, 4),
             "gflops": round(flops[n] / (us * 1e-6) / 1e9, 1),
         }
-    dominant = max(names, key=lambda n: kernels[n]["avg_us"])
+    assert torch.equal(y.view(torch.int32), y_ref.view(torch.int32)), "SpMV not deterministic"
+
+    # HBM reference reads in the same process: the 4 GiB rate (measured peak) and the
+    # fastest of several launch shapes over buffers of the SpMV's size, rotated like
+    # the format (same-size floor: launch, ramp and one memory latency included)
+    sink = torch.empty(8192, dtype=torch.float32, device=dev)
+    big = torch.empty(1 << 30, dtype=torch.float32, device=dev)
+    read_peak_us = timer(lib.darb_stream_read, [(P(big.data_ptr()), big.numel() * 4,
+                                                 P(sink.data_ptr()), sp)], 5)
+    read_peak = big.numel() * 4 / (read_peak_us * 1e-6) / 1e9
+    del big
+    small_b = nbytes["spmv"] // 16 * 16
+    n_small = max(RE, -(-MIN_ROTATION_BYTES // small_b))
+    smalls = [torch.empty(small_b // 4, dtype=torch.float32, device=dev) for _ in range(n_small)]
+    shapes = {}
+    for (th, vp) in READ_SHAPES:
+        a = [(P(t.data_ptr()), small_b, th, vp, P(sink.data_ptr()), sp) for t in smalls]
+        shapes[f"{th}x{vp}"] = round(timer(lib.darb_stream_read_shape, a, NL), 3)
+    del smalls
+    best_shape = min(shapes, key=shapes.get)
+    floor_us = shapes[best_shape]
+    # the same read over the encode's input: the rotated W copies themselves
+    w_bytes = (Wd[0].numel() * Wd[0].element_size()) // 16 * 16
+    w_read_us = timer(lib.darb_stream_read, [(P(t.data_ptr()), w_bytes, P(sink.data_ptr()), sp)
+                                             for t in Wd], max(K // 4, 32))
 
     # the step DARB starts from, on the device: per-row counts of the k largest
     # magnitudes (radix select over W, several kernels)
@@ -406,24 +499,20 @@ def main(argv=None):
     counts = torch.empty(cfg.M, dtype=torch.int64, device=dev)
     prune_args = [(cfg.M, cfg.N, wcode, P(Wd[i].data_ptr()), cfg.N, mi.k, P(counts.data_ptr()),
                    P(prune_ws.data_ptr()), nb_ws.value, sp) for i in range(RW)]
-    lib.darb_prune_counts(*prune_args[0])              # first launches load the kernels
-    prune_us = timed_launches(lib.darb_prune_counts, prune_args, max(K // 4, 8))
+    prune_us = timer(lib.darb_prune_counts, prune_args, max(K // 4, 32), host_us_per_call=60.0)
     prune_ok = bool(np.array_equal(counts.cpu().numpy(), mi.mask.sum(axis=1)))
-    # from 64 MiB of W a sample (about 1/32 of W) proposes the first digit's bracket,
-    # one split pass reads W and the later passes only the keys in the bracket
-    # (about 1 % of W); below it every pass (3 digits + count for fp32, 2 + count for
-    # fp16) reads W
     w_stream = cfg.M * cfg.N * s_w
     w_passes = 1 + 1 / 32 if w_stream >= (64 << 20) else (4 if cfg.wdtype == "f32" else 3)
     prune_ctx = {"avg_us": round(prune_us, 3), "k": mi.k, "passes_over_W": round(w_passes, 3),
                  "bytes": int(w_passes * w_stream),
                  "gbps": round(w_passes * w_stream / (prune_us * 1e-6) / 1e9, 1),
+                 "x_of_W_read": round(prune_us / w_read_us, 3),
                  "counts_equal_generator": prune_ok}
     del prune_ws
 
-    # the paper's storage form: offsets bit-packed to log2 b bits (section 4.2).  The
-    # conversion from the encode's bytes and both products on the packed form, same
-    # rotation; outputs must equal the byte-offset products bit for bit.
+    # the paper's storage form: offsets bit-packed to log2 b bits (section 4.2), the
+    # conversion and both products on it; outputs equal the byte-offset products bit
+    # for bit
     packed = [plan.empty_packed(dev) for _ in range(RE)]
     for j in range(RE):
         plan.pack_offsets(fmt[j][1], packed[j])
@@ -432,16 +521,21 @@ def main(argv=None):
     pk_spmv = [(h, wcode, P(fmt[j][0].data_ptr()), P(packed[j].data_ptr()), xcode,
                 P(xd[j].data_ptr()), P(y.data_ptr()), sp) for j in range(RE)]
     pk_spmm = [(h, wcode, P(fmt[j][0].data_ptr()), P(packed[j].data_ptr()), xcode, B,
-                P(Xd[j].data_ptr()), B, P(Y.data_ptr()), B, sp) for j in range(RE)]
+                P(Xd[j].data_ptr()), B, P(Y.data_ptr()), B, sp) for j in range(RE)] \
+        if with_spmm else []
     pw = plan.packed_words
     pk_bytes = {"pack": plan.nnz + 4 * pw,
                 "spmv": plan.nnz * s_w + 4 * pw + cfg.N * s_x + 8 * cfg.M,
                 "spmm": plan.nnz * s_w + 4 * pw + cfg.N * B * s_x + 4 * cfg.M * B + 4 * cfg.M}
-    pk_us = {"pack": timed_launches(lib.darb_pack_offsets, pack_args, K),
-             "spmv": timed_launches(lib.darb_spmv_packed, pk_spmv, K)}
+    pk_us = {"pack": timer(lib.darb_pack_offsets, pack_args, NL)}
+    lib.darb_spmv_packed(*pk_spmv[(K + args.warmup + 6) % RE])
+    torch.cuda.synchronize()
     pk_same = bool(torch.equal(y.view(torch.int32), y_ref.view(torch.int32)))
+    pk_us["spmv"] = timer(lib.darb_spmv_packed, pk_spmv, NL)
     if with_spmm:
-        pk_us["spmm"] = timed_launches(lib.darb_spmm_packed, pk_spmm, K)
+        pk_us["spmm"] = timer(lib.darb_spmm_packed, pk_spmm, NL)
+        lib.darb_spmm_packed(*pk_spmm[0])
+        torch.cuda.synchronize()
         pk_same = pk_same and bool(torch.equal(Y.view(torch.int32), Y_ref.view(torch.int32)))
     packed_ctx = {"words": pw, "bits_per_index": round(32.0 * pw / plan.nnz, 3),
                   "format_bytes": plan.nnz * s_w + 4 * pw,
@@ -454,9 +548,8 @@ def main(argv=None):
                          "traffic_bytes": traffic.get(n if n == "pack" else n + "_packed")}
 
     # INT8 retained values (section 4.2's storage accounting assumes INT8 weights): the
-    # per-row quantisation of the format's values and both products on INT8 codes
-    # with the packed offsets -- the paper's full storage form, 8 + log2 b bits per
-    # weight -- and with byte offsets; same rotation
+    # per-row quantisation and both products on INT8 codes, with the packed offsets
+    # (the paper's full storage form, 8 + log2 b bits per weight) and with byte offsets
     codes = [torch.empty(plan.nnz, dtype=torch.int8, device=dev) for _ in range(RE)]
     scales = [torch.empty(cfg.M, dtype=torch.float32, device=dev) for _ in range(RE)]
     for j in range(RE):
@@ -471,13 +564,17 @@ def main(argv=None):
                   None, xcode, P(xd[j].data_ptr()), P(y.data_ptr()), sp) for j in range(RE)]
     i8_spmm = [(h, P(codes[j].data_ptr()), P(scales[j].data_ptr()), None,
                 P(packed[j].data_ptr()), xcode, B, P(Xd[j].data_ptr()), B, P(Y.data_ptr()), B,
-                sp) for j in range(RE)]
-    i8_us = {"quantize": timed_launches(lib.darb_quantize_i8, q_args, K),
-             "spmv_byte_offsets": timed_launches(lib.darb_spmv_i8, i8_spmv_b, K),
-             "spmv": timed_launches(lib.darb_spmv_i8, i8_spmv, K)}
+                sp) for j in range(RE)] if with_spmm else []
+    i8_us = {"quantize": timer(lib.darb_quantize_i8, q_args, NL),
+             "spmv_byte_offsets": timer(lib.darb_spmv_i8, i8_spmv_b, NL),
+             "spmv": timer(lib.darb_spmv_i8, i8_spmv, NL)}
+    lib.darb_spmv_i8(*i8_spmv[(K + args.warmup + 6) % RE])
+    torch.cuda.synchronize()
     i8_err = {"spmv": float((y - y_ref).norm() / y_ref.norm())}
     if with_spmm:
-        i8_us["spmm"] = timed_launches(lib.darb_spmm_i8, i8_spmm, K)
+        i8_us["spmm"] = timer(lib.darb_spmm_i8, i8_spmm, NL)
+        lib.darb_spmm_i8(*i8_spmm[0])
+        torch.cuda.synchronize()
         i8_err["spmm"] = float((Y - Y_ref).norm() / Y_ref.norm())
     i8_fmt = plan.nnz + 4 * pw + 4 * cfg.M
     i8_bytes = {"quantize": plan.nnz * (s_w + 1) + 8 * cfg.M,
@@ -495,8 +592,6 @@ def main(argv=None):
                        "traffic_bytes": traffic.get(tkey)}
     del packed, codes, scales
 
-    # HBM reference rates measured in the same process: a plain stream read over
-    # 4 GiB, and over buffers the size of the SpMV's bytes rotated past the cache
     # a plain copy of known size: its FETCH_SIZE / WRITE_SIZE counters calibrate the
     # HBM-traffic counters of the DARB kernels (same process, same command)
     cp_src = torch.ones(16 << 20, dtype=torch.float32, device=dev)      # 64 MiB
@@ -505,40 +600,18 @@ def main(argv=None):
         darb.stream_copy(cp_dst, cp_src)
     torch.cuda.synchronize()
     del cp_src, cp_dst
-    sink = torch.empty(8192, dtype=torch.float32, device=dev)
-    big = torch.empty(1 << 30, dtype=torch.float32, device=dev)
-    darb.stream_read(big, sink)
-    torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record(stream)
-    for _ in range(5):
-        darb.stream_read(big, sink)
-    e1.record(stream)
-    torch.cuda.synchronize()
-    read_peak = 5 * big.numel() * 4 / (e0.elapsed_time(e1) * 1e-3) / 1e9
-    del big
-    small_n = (nbytes["spmv"] // 16) * 4
-    smalls = [torch.empty(small_n, dtype=torch.float32, device=dev) for _ in range(40)]
-    small_args = [(P(t.data_ptr()), small_n * 4, P(sink.data_ptr()), sp) for t in smalls]
-    small_us = timed_launches(lib.darb_stream_read, small_args, K)
-    small_gbps = small_n * 4 / (small_us * 1e-6) / 1e9
-    del smalls
-    # the same kernel reading the encode's input: the rotated W copies themselves
-    w_bytes = (Wd[0].numel() * Wd[0].element_size()) // 16 * 16
-    w_args = [(P(t.data_ptr()), w_bytes, P(sink.data_ptr()), sp) for t in Wd]
-    w_read_us = timed_launches(lib.darb_stream_read, w_args, K)
 
     # the SpMV at larger sizes: the same rows tiled t times (t*M rows with the same
-    # densities, W tiled on the device), format copies rotated past the 256 MB cache.
-    # A single launch pays a fixed start-up and memory latency; these sizes show how
-    # far the kernel's own rate rises once that is amortised.
+    # densities), format copies rotated past the cache.  A single launch pays a fixed
+    # start-up and memory latency; these sizes show the rate once that is amortised,
+    # for the fp32 byte-offset form and for INT8 codes with packed offsets.
     size_sweep = []
     for t in (1, 4, 16):
         Mt = cfg.M * t
         plan_t = darb.Plan(Mt, cfg.N, np.tile(mi.row_density, t), mi.matrix_density,
                            darb.ROUND_FLOOR, cfg.b_min, cfg.b_max).upload()
         fbytes = plan_t.nnz * (s_w + 1)
-        reps = int(min(8, max(2, -(-(512 << 20) // fbytes))))
+        reps = int(max(2, -(-MIN_ROTATION_BYTES // fbytes)))
         Wt = Wd[0].repeat(t, 1)
         fmts = [plan_t.empty_format(wdt, dev) for _ in range(reps)]
         for v_t, o_t in fmts:
@@ -547,35 +620,36 @@ def main(argv=None):
         y_t = torch.empty(Mt, dtype=torch.float32, device=dev)
         sw_args = [(plan_t.handle, wcode, P(v_t.data_ptr()), P(o_t.data_ptr()), xcode,
                     P(xd[0].data_ptr()), P(y_t.data_ptr()), sp) for v_t, o_t in fmts]
-        lib.darb_spmv(*sw_args[0])
-        us = timed_launches(lib.darb_spmv, sw_args, max(K // 2, 20))
+        us = timer(lib.darb_spmv, sw_args, max(NL // 4, 64))
         sb = fbytes + cfg.N * s_x + 8 * Mt
         gbps = sb / (us * 1e-6) / 1e9
-        entry = {"rows": Mt, "bytes": int(sb), "avg_us": round(us, 3), "gbps": round(gbps, 1),
-                 "frac_of_4GiB_read": round(gbps / read_peak, 4)}
-        # the same rows in the paper's storage form: INT8 codes + log2 b-bit offsets
+        entry = {"rows": Mt, "bytes": int(sb), "copies": reps, "avg_us": round(us, 3),
+                 "gbps": round(gbps, 1), "frac_of_4GiB_read": round(gbps / read_peak, 4)}
         i8 = []
         for v_t, o_t in fmts:
             q_t, sc_t = plan_t.quantize_i8(v_t)
             i8.append((q_t, sc_t, plan_t.pack_offsets(o_t)))
         del fmts
+        sb8 = plan_t.nnz + 4 * plan_t.packed_words + 4 * Mt + cfg.N * s_x + 8 * Mt
+        reps8 = int(max(2, -(-MIN_ROTATION_BYTES // sb8)))
+        while len(i8) < reps8:
+            q_t, sc_t, pk_t = i8[len(i8) % reps]
+            i8.append((q_t.clone(), sc_t.clone(), pk_t.clone()))
         i8_args = [(plan_t.handle, P(q_t.data_ptr()), P(sc_t.data_ptr()), None,
                     P(pk_t.data_ptr()), xcode, P(xd[0].data_ptr()), P(y_t.data_ptr()), sp)
                    for q_t, sc_t, pk_t in i8]
-        lib.darb_spmv_i8(*i8_args[0])
-        us8 = timed_launches(lib.darb_spmv_i8, i8_args, max(K // 2, 20))
-        sb8 = plan_t.nnz + 4 * plan_t.packed_words + 4 * Mt + cfg.N * s_x + 8 * Mt
-        entry["int8_packed"] = {"bytes": int(sb8), "avg_us": round(us8, 3),
+        us8 = timer(lib.darb_spmv_i8, i8_args, max(NL // 4, 64))
+        entry["int8_packed"] = {"bytes": int(sb8), "copies": len(i8), "avg_us": round(us8, 3),
                                 "gbps": round(sb8 / (us8 * 1e-6) / 1e9, 1)}
         size_sweep.append(entry)
         del i8, y_t, plan_t
 
-    # context, not a target: the same masked matrix as a dense fp32/fp16 matrix through
-    # torch (hipBLASLt / rocBLAS), rotated like the DARB format
+    # context, not a target: the same masked matrix as a dense matrix through torch
+    # (hipBLASLt / rocBLAS) and in CSR (hipSPARSE), rotated like the DARB format
     Wm = plan.decode(*fmt[0])
     dense = [Wm.clone() for _ in range(RW)]
-    xs_t = [t.to(Wm.dtype) for t in xd]
-    Xs_t = [t.to(Wm.dtype) for t in Xd]
+    xs_t = [t.to(Wm.dtype) for t in xd[:16]]
+    Xs_t = [t.to(Wm.dtype) for t in Xd[:16]]
     del Wm
 
     def timed_torch(fn, count):
@@ -591,23 +665,21 @@ def main(argv=None):
         return e0.elapsed_time(e1) * 1e3 / count
 
     dense_ctx = {"gemv_us": round(timed_torch(
-        lambda i: torch.mv(dense[i % RW], xs_t[i % RE]), K), 3)}
+        lambda i: torch.mv(dense[i % RW], xs_t[i % 16]), 64), 3)}
     if with_spmm:
         dense_ctx["gemm_us"] = round(timed_torch(
-            lambda i: torch.mm(dense[i % RW], Xs_t[i % RE]), K), 3)
-    # the same masked matrix in CSR (hipSPARSE through torch); CSR keeps every retained
-    # weight's column index (4-8 bytes) instead of DARB's one offset byte
+            lambda i: torch.mm(dense[i % RW], Xs_t[i % 16]), 64), 3)
     if cfg.wdtype == "f32":
         try:
             import warnings
             with warnings.catch_warnings():
                 warnings.simplefilter("ignore")      # torch flags sparse CSR as beta
-                csr = [dense[0].to_sparse_csr() for _ in range(RE)]
+                csr = [dense[0].to_sparse_csr() for _ in range(8)]
             dense_ctx["csr_spmv_us"] = round(timed_torch(
-                lambda i: torch.mv(csr[i % RE], xs_t[i % RE]), K), 3)
+                lambda i: torch.mv(csr[i % 8], xs_t[i % 16]), 64), 3)
             if with_spmm:
                 dense_ctx["csr_spmm_us"] = round(timed_torch(
-                    lambda i: torch.mm(csr[i % RE], Xs_t[i % RE]), K), 3)
+                    lambda i: torch.mm(csr[i % 8], Xs_t[i % 16]), 64), 3)
             del csr
         except RuntimeError as e:          # sparse kernels unavailable in this torch build
             dense_ctx["csr_error"] = str(e)[:120]
@@ -615,12 +687,16 @@ def main(argv=None):
 
     for n in names:
         kernels[n]["traffic_bytes"] = traffic.get(n)
-    step_total = sum(nbytes.values())
-    value = step_total / (ms_per_step * 1e-3) / 1e9
-    k = kernels[dominant]
+    ks = kernels["spmv"]
+    step_total = sum(nbytes[n] for n in names)
+    roofline = {"kernel": "spmv", "bound": "hbm", "achieved": ks["gbps"], "peak": HBM_PEAK_GBPS,
+                "unit": "GB/s", "frac": round(ks["gbps"] / HBM_PEAK_GBPS, 4),
+                "traffic": traffic.get("spmv"),
+                "frac_of_measured_read_peak": round(ks["gbps"] / read_peak, 4),
+                "x_of_same_size_read_floor": round(ks["avg_us"] / floor_us, 3)}
     out = {
         "metric": METRIC,
-        "value": round(value, 1),
+        "value": ks["gbps"],
         "unit": "GB/s",
         "n_gpus": 1,
         "steps": K,
@@ -635,25 +711,27 @@ def main(argv=None):
         "config": {
             "workload": f"{cfg.name}: W {cfg.wdtype} [{cfg.M} x {cfg.N}] {cfg.dist}, "
                         f"keep {cfg.keep}, block sizes {cfg.b_min}..{cfg.b_max} (floor rule); "
-                        f"step = encode + SpMV (B=1)" + (f" + SpMM (B={B})" if with_spmm else ""),
+                        f"value = SpMV (B=1) over the encoded matrix; step = encode + SpMV"
+                        + (f" + SpMM (B={B})" if with_spmm else ""),
             "M": cfg.M, "N": cfg.N, "nnz": plan.nnz, "spmm_batch": B,
             "bins": {str(1 << b["log2b"]): b["rows"] for b in plan.bins},
-            "rotation": {"W_copies": RW, "format_copies": RE},
+            "rotation": {"W_copies": RW, "format_copies": RE,
+                         "format_rotation_MB": round(RE * plan.nnz * (s_w + 1) / 1e6, 1)},
         },
-        "roofline": {
-            "kernel": dominant, "bound": "hbm", "achieved": k["gbps"], "peak": HBM_PEAK_GBPS,
-            "unit": "GB/s", "frac": round(k["gbps"] / HBM_PEAK_GBPS, 4),
-            "traffic": traffic.get(dominant),
-        },
+        "roofline": roofline,
+        "spmv_gflops": ks["gflops"],
         "kernels": kernels,
+        "step_gbps": round(step_total / (ms_per_step * 1e-3) / 1e9, 1),
         "gflops_step": round(sum(flops[n] for n in names) / (ms_per_step * 1e-3) / 1e9, 1),
         "hbm_measured": {"stream_read_4GiB_gbps": round(read_peak, 1),
-                         "stream_read_spmv_size_gbps": round(small_gbps, 1),
-                         "stream_read_spmv_size_us": round(small_us, 3),
+                         "same_size_read_us_by_shape": shapes,
+                         "same_size_read_floor_us": floor_us,
+                         "same_size_read_floor_shape": best_shape,
+                         "same_size_read_floor_gbps": round(small_b / (floor_us * 1e-6) / 1e9, 1),
+                         "same_size_rotation": n_small,
                          "stream_read_W_us": round(w_read_us, 3),
                          "stream_read_W_gbps": round(w_bytes / (w_read_us * 1e-6) / 1e9, 1)},
         "encode_frac_of_W_read": round(w_read_us / kernels["encode"]["avg_us"], 4),
-        "spmv_frac_of_measured_read_peak": round(kernels["spmv"]["gbps"] / read_peak, 4),
         "spmv_size_sweep": size_sweep,
         "packed_offsets": packed_ctx,
         "int8_values": int8_ctx,
@@ -661,10 +739,23 @@ def main(argv=None):
         "dense_masked_context": dense_ctx,
         "host": {"plan_ms": round(plan_ms, 3), "enqueue_us_per_step": round(host_us, 2)},
     }
-    if args.cpu_seconds > 0:
-        out["cpu_baseline"] = cpu_baseline(cfg, mi, x, X, args.cpu_seconds, step_total)
-    else:
-        out["cpu_baseline"] = None
+    if with_spmm:
+        km = kernels["spmm"]
+        gather = plan.nnz * B * s_x       # every retained weight reads its X row on chip
+        g_gbps = gather / (km["avg_us"] * 1e-6) / 1e9
+        out["spmm_b64_gbps"] = km["gbps"]
+        out["spmm_b64_gflops"] = km["gflops"]
+        out["roofline_spmm"] = {"kernel": "spmm", "bound": "gather", "achieved": round(g_gbps, 1),
+                                "peak": round(GATHER_PEAK_GBPS, 1), "unit": "GB/s",
+                                "frac": round(g_gbps / GATHER_PEAK_GBPS, 4),
+                                "gather_bytes": int(gather),
+                                "hbm_gbps": km["gbps"],
+                                "hbm_frac": km["frac_hbm_peak"],
+                                "traffic": traffic.get("spmm")}
+    if not args.no_recurrent:
+        out["recurrent"] = recurrent_figures(args, with_cpu=False)
+    out["cpu_baseline"] = (cpu_baseline(cfg, mi, x, X, args.cpu_seconds, nbytes)
+                           if args.cpu_seconds > 0 else None)
     print(json.dumps(out), flush=True)
 
 

@@ -313,6 +313,17 @@ int darb_lstm_workspace(int64_t H, int64_t T, int64_t batch, int64_t *floats);
  * rates the DARB kernels are compared with.
  */
 int darb_stream_read(const void *buf, int64_t bytes, float *sink, void *stream);
+/*
+ * The same read in other launch shapes, to find the fastest plain read of a given
+ * size: `threads` per workgroup (64, 128, 256, 512 or 1024) each issuing `vectors`
+ * 16-byte loads (1, 2, 4 or 8; the pairs 64/1, 64/2, 128/1, 128/2, 128/8, 512/8
+ * and 1024/8 are not built) before using any of them.  The loaded data decides
+ * whether anything is written to `sink` (device, >= 8192 floats); real data never
+ * produces the value that would, so the launch is the read alone.
+ * Errors: DARB_E_INVALID (also for a shape that is not built), DARB_E_HIP.
+ */
+int darb_stream_read_shape(const void *buf, int64_t bytes, int threads, int vectors, float *sink,
+                           void *stream);
 int darb_stream_copy(void *dst, const void *src, int64_t bytes, void *stream);
 
 /* Text for a DARB_E_* code (static storage). */

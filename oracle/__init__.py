@@ -161,6 +161,36 @@ def encode(W: np.ndarray, lay: Layout):
     return values, offsets
 
 
+def _at(a: np.ndarray, first: int):
+    """Pointer to element `first` along a's first axis (C-contiguous arrays)."""
+    return ctypes.c_void_p(a.ctypes.data + int(first) * a.strides[0])
+
+
+def encode_rows(W: np.ndarray, lay: Layout, r0: int, r1: int, values: np.ndarray,
+                offsets: np.ndarray) -> None:
+    """encode() restricted to the original rows [r0, r1), writing their slots of the
+    caller's values / offsets (the same arithmetic; only the row range is narrowed,
+    so several calls on disjoint ranges can run on separate threads)."""
+    W = np.ascontiguousarray(W)
+    bits = W.view(_BITS[W.dtype])
+    fn = _load().oracle_encode_f32 if W.dtype == np.float32 else _load().oracle_encode_f16
+    fn(r1 - r0, lay.N, _at(bits, r0), bits.shape[1], _at(lay.log2b, r0), _at(lay.row_start, r0),
+       _ptr(values), _ptr(offsets))
+
+
+def spmm_rows(values: np.ndarray, offsets: np.ndarray, lay: Layout, X: np.ndarray, r0: int,
+              r1: int, Y: np.ndarray) -> None:
+    """spmm() restricted to the original rows [r0, r1), written to those rows of the
+    caller's fp64 Y [M, B] (same arithmetic; for running row ranges on threads)."""
+    X2 = _as_2d(X)
+    B = X2.shape[1]
+    rc = _load().oracle_spmm_f64(r1 - r0, lay.N, _DT[values.dtype], _ptr(values), _ptr(offsets),
+                                 _at(lay.log2b, r0), _at(lay.row_start, r0), _DT[X2.dtype],
+                                 _ptr(X2), B, B, _at(Y, r0), B)
+    if rc != 0:
+        raise ValueError("malformed DARB format (offset outside its block or row)")
+
+
 def decode(values: np.ndarray, offsets: np.ndarray, lay: Layout) -> np.ndarray:
     values = np.ascontiguousarray(values)
     offsets = np.ascontiguousarray(offsets, dtype=np.uint8)

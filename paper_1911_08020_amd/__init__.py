@@ -99,6 +99,7 @@ def _load_library():
         "darb_lstm_layer": ([P, P, P, P, P, P, I, I64, I64, I64, P, P, P, P, P, I64, P], I),
         "darb_lstm_workspace": ([I64, I64, I64, ctypes.POINTER(I64)], I),
         "darb_stream_read": ([P, I64, P, P], I),
+        "darb_stream_read_shape": ([P, I64, I, I, P, P], I),
         "darb_stream_copy": ([P, P, I64, P], I),
     }
     for name, (args, res) in sig.items():
@@ -116,7 +117,7 @@ EXPORTED = ("darb_plan_create", "darb_plan_create_counts", "darb_prune_workspace
             "darb_plan_destroy", "darb_encode", "darb_decode", "darb_spmv", "darb_spmm",
             "darb_pack_offsets", "darb_unpack_offsets", "darb_spmv_packed", "darb_spmm_packed",
             "darb_quantize_i8", "darb_spmv_i8", "darb_spmm_i8", "darb_lstm_layer",
-            "darb_lstm_workspace", "darb_stream_read", "darb_stream_copy", "darb_strerror",
+            "darb_lstm_workspace", "darb_stream_read", "darb_stream_read_shape", "darb_stream_copy", "darb_strerror",
             "darb_last_error", "darb_version")
 
 

@@ -592,6 +592,17 @@ int darb_stream_read(const void *buf, int64_t bytes, float *sink, void *stream) 
                     "stream read launch");
 }
 
+int darb_stream_read_shape(const void *buf, int64_t bytes, int threads, int vectors, float *sink,
+                           void *stream) {
+    clear_error();
+    if (!buf || !sink || bytes <= 0 || (bytes & 15) || (reinterpret_cast<uintptr_t>(buf) & 15))
+        return fail(DARB_E_INVALID, "buf/sink NULL or bytes/alignment not a multiple of 16");
+    const hipError_t e = launch_stream_read_shape(buf, bytes, threads, vectors, sink,
+                                                  static_cast<hipStream_t>(stream));
+    if (e == hipErrorInvalidValue) return fail(DARB_E_INVALID, "no stream read of that shape");
+    return launched(e, "stream read launch");
+}
+
 int darb_stream_copy(void *dst, const void *src, int64_t bytes, void *stream) {
     clear_error();
     if (!dst || !src || bytes <= 0 || (bytes & 15) || (reinterpret_cast<uintptr_t>(dst) & 15) ||

@@ -104,6 +104,8 @@ hipError_t launch_lstm_cell(int64_t H, int64_t batch, const float *G, const floa
                             int64_t ldu, float *h, float *c, float *h_seq, int64_t ld_seq,
                             hipStream_t s);
 hipError_t launch_stream_read(const void *buf, int64_t bytes, float *sink, hipStream_t s);
+hipError_t launch_stream_read_shape(const void *buf, int64_t bytes, int threads, int vectors,
+                                   float *sink, hipStream_t s);
 hipError_t launch_stream_copy(void *dst, const void *src, int64_t bytes, hipStream_t s);
 
 }  // namespace darb

@@ -73,6 +73,27 @@ __global__ __launch_bounds__(kThreads) void stream_read_kernel(const f32x4 *__re
         sink[blockIdx.x % kStreamBlocks] = (part[0] + part[1]) + (part[2] + part[3]);
 }
 
+// The same read in other launch shapes: THREADS threads per workgroup, each issuing
+// VPL 16-byte non-temporal loads (lanes interleaved, so every load instruction of a
+// wave covers 1 KiB) before summing them.  The sum goes to memory only when it
+// equals a value no real data produces, so the loads cannot be elided and nothing is
+// normally written: the launch measures the read alone.
+template <int THREADS, int VPL>
+__global__ __launch_bounds__(THREADS) void stream_read_shape_kernel(
+    const f32x4 *__restrict__ buf, int64_t n16, float *sink) {
+    const int64_t base = int64_t(blockIdx.x) * (VPL * THREADS) + threadIdx.x;
+    f32x4 v[VPL];
+#pragma unroll
+    for (int u = 0; u < VPL; ++u) {
+        const int64_t i = base + int64_t(u) * THREADS;
+        v[u] = __builtin_nontemporal_load(buf + (i < n16 ? i : n16 - 1));
+    }
+    float s = 0.0f;
+#pragma unroll
+    for (int u = 0; u < VPL; ++u) s += (v[u][0] + v[u][1]) + (v[u][2] + v[u][3]);
+    if (s == -0x1.5p-126f) sink[blockIdx.x % kStreamBlocks] = s;
+}
+
 __global__ __launch_bounds__(kThreads) void stream_copy_kernel(float4 *__restrict__ dst,
                                                                const float4 *__restrict__ src,
                                                                int64_t n16) {
@@ -119,6 +140,27 @@ hipError_t launch_stream_read(const void *buf, int64_t bytes, float *sink, hipSt
     hipLaunchKernelGGL(stream_read_kernel, dim3(unsigned(blocks)), dim3(kThreads), 0, s,
                        static_cast<const f32x4 *>(buf), n16, sink);
     return hipGetLastError();
+}
+
+hipError_t launch_stream_read_shape(const void *buf, int64_t bytes, int threads, int vectors,
+                                   float *sink, hipStream_t s) {
+    const int64_t n16 = bytes / 16;
+    const int64_t per_block = int64_t(threads) * vectors;
+    const int64_t blocks = (n16 + per_block - 1) / per_block;
+    if (blocks > 0x7FFFFFFF) return hipErrorInvalidConfiguration;
+    const f32x4 *b = static_cast<const f32x4 *>(buf);
+#define DARB_READ_SHAPE(T, V)                                                               \
+    if (threads == T && vectors == V) {                                                     \
+        hipLaunchKernelGGL((stream_read_shape_kernel<T, V>), dim3(unsigned(blocks)), dim3(T), \
+                           0, s, b, n16, sink);                                             \
+        return hipGetLastError();                                                           \
+    }
+    DARB_READ_SHAPE(64, 4) DARB_READ_SHAPE(64, 8) DARB_READ_SHAPE(128, 4)
+    DARB_READ_SHAPE(256, 1) DARB_READ_SHAPE(256, 2) DARB_READ_SHAPE(256, 4) DARB_READ_SHAPE(256, 8)
+    DARB_READ_SHAPE(512, 1) DARB_READ_SHAPE(512, 2) DARB_READ_SHAPE(512, 4)
+    DARB_READ_SHAPE(1024, 1) DARB_READ_SHAPE(1024, 2) DARB_READ_SHAPE(1024, 4)
+#undef DARB_READ_SHAPE
+    return hipErrorInvalidValue;
 }
 
 hipError_t launch_stream_copy(void *dst, const void *src, int64_t bytes, hipStream_t s) {

@@ -13,10 +13,13 @@
 // of its loads back to back.
 //
 // SpMV: `lanes` lanes per row, 64 / lanes rows per wave; each lane holds up to
-// kVmax 16-byte vectors of values (plus their offset bytes) in registers.  The
-// workgroup stages x into LDS after issuing those loads, so HBM latency overlaps
-// the staging; the gathers then hit LDS.  A row's partial sums are combined by an
-// xor butterfly in a fixed order (deterministic) and written in original row order.
+// kVmax 16-byte vectors of values (plus their offset bytes) in registers.  Every
+// wave first issues its share of the loads that stage x into LDS, then the loads of
+// its vectors, so both memory latencies overlap; the gathers then hit LDS.  (Gathers
+// from L2 instead cost several times the staging, and the fp32 products keep the
+// exact x.)  A row's partial sums are combined by a
+// fixed-order lane reduction (DPP within 16-lane rows, then lane exchanges; the
+// result is deterministic) and written in original row order.
 //
 // SpMM: lanes map to batch columns (X is [N x B] row-major, so one weight's
 // activations X[c, :] are contiguous), CPL columns per lane with 16-byte loads, or
@@ -60,6 +63,27 @@ __device__ __forceinline__ float half_bits_to_f32(uint32_t h) {
 }
 
 __device__ __forceinline__ int wave_uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
+
+// v plus its value in the lane DPP control CTRL selects (all rows and banks)
+template <int CTRL> __device__ __forceinline__ float add_dpp(float v) {
+    return v + __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(
+                   0, __builtin_bit_cast(int, v), CTRL, 0xF, 0xF, false));
+}
+
+// Sum over aligned groups of 2^lgL lanes (lgL <= 6, wave-uniform): every lane of a
+// group ends with the group's sum.  The pairs are lanes 1 apart, then 2 (quad
+// permutations), then mirrored inside 8 and 16 lanes (row_half_mirror, row_mirror),
+// then 16 and 32 apart (bpermute); each step adds two equal partial sums, so the
+// result depends only on lgL and is the same in every lane of the group.
+__device__ __forceinline__ float group_sum(float v, int lgL) {
+    if (lgL >= 1) v = add_dpp<0xB1>(v);     // quad_perm [1, 0, 3, 2]
+    if (lgL >= 2) v = add_dpp<0x4E>(v);     // quad_perm [2, 3, 0, 1]
+    if (lgL >= 3) v = add_dpp<0x141>(v);    // row_half_mirror
+    if (lgL >= 4) v = add_dpp<0x140>(v);    // row_mirror
+    if (lgL >= 5) v += __shfl_xor(v, 16, kWave);
+    if (lgL >= 6) v += __shfl_xor(v, 32, kWave);
+    return v;
+}
 
 // Uniform selection of a per-group table entry (compile-time indices only, so the
 // table stays in scalar registers).
@@ -203,26 +227,30 @@ template <> struct WVec<int8_t> {
     }
 };
 
-// Copy x (N elements) into LDS as fp32: SB 16-byte loads per thread in flight
-// (addresses clamped, stores masked), then the scalar tail.
-template <typename Tx, int SB>
-__device__ __forceinline__ void stage_x(float *xs, const Tx *__restrict__ x, int N) {
-    constexpr int E = 16 / int(sizeof(Tx));
-    const bool aligned = (reinterpret_cast<uintptr_t>(x) & 15) == 0;
-    const int nv = aligned ? N / E : 0;
-    const u32x4 *x4 = reinterpret_cast<const u32x4 *>(x);
-    for (int base = 0; base < nv; base += SB * kSpmvThreads) {
-        u32x4 t[SB];
+// x (N elements) into LDS as fp32 through registers, in two halves so that other
+// loads can be issued between them: issue() loads up to SB 16-byte vectors per
+// thread (addresses clamped), commit() waits for them, widens and stores them, and
+// copies the scalar tail.  The launcher picks SB so that one round covers x.
+template <typename Tx, int SB> struct XStage {
+    static constexpr int E = 16 / int(sizeof(Tx));
+    u32x4 t[SB];
+    int nv;
+    __device__ __forceinline__ void issue(const Tx *__restrict__ x, int N) {
+        const bool aligned = (reinterpret_cast<uintptr_t>(x) & 15) == 0;
+        nv = aligned ? N / E : 0;
+        const u32x4 *x4 = reinterpret_cast<const u32x4 *>(x);
 #pragma unroll
         for (int u = 0; u < SB; ++u) {
-            if (base + u * kSpmvThreads < nv) {          // wave-uniform: skip empty rounds
-                const int i = base + u * kSpmvThreads + int(threadIdx.x);
+            if (u * kSpmvThreads < nv) {                  // wave-uniform: skip empty rounds
+                const int i = u * kSpmvThreads + int(threadIdx.x);
                 t[u] = x4[i < nv ? i : nv - 1];
             }
         }
+    }
+    __device__ __forceinline__ void commit(float *xs, const Tx *__restrict__ x, int N) const {
 #pragma unroll
         for (int u = 0; u < SB; ++u) {
-            const int i = base + u * kSpmvThreads + int(threadIdx.x);
+            const int i = u * kSpmvThreads + int(threadIdx.x);
             if (i < nv) {
                 if constexpr (sizeof(Tx) == 4) {
                     *reinterpret_cast<u32x4 *>(xs + i * E) = t[u];
@@ -235,14 +263,15 @@ __device__ __forceinline__ void stage_x(float *xs, const Tx *__restrict__ x, int
                 }
             }
         }
+        for (int c = nv * E + int(threadIdx.x); c < N; c += kSpmvThreads)
+            xs[c] = to_f32<Tx>(x[c]);
     }
-    for (int c = nv * E + int(threadIdx.x); c < N; c += kSpmvThreads) xs[c] = to_f32<Tx>(x[c]);
-}
+};
 
 // fp32 x straight into LDS: each wave moves 1 KiB chunks with direct global-to-LDS
-// loads (lane i's 16 bytes land at chunk + 16 i), so no registers hold x on the way;
-// the rest (a partial chunk, a tail shorter than 16 bytes) goes through registers.
-// The caller waits for the loads and synchronises the workgroup.
+// loads (lane i's 16 bytes land at chunk + 16 i), so no registers hold x on the way.
+// stage_x_direct issues them; stage_x_tail copies the rest (a partial chunk)
+// through registers.  The caller waits for the loads and synchronises the workgroup.
 __device__ __forceinline__ void stage_x_direct(float *xs, const float *__restrict__ x, int N) {
     typedef __attribute__((address_space(1))) const float *gptr;
     typedef __attribute__((address_space(3))) void *lptr;
@@ -252,7 +281,10 @@ __device__ __forceinline__ void stage_x_direct(float *xs, const float *__restric
     for (int j = wave; j < chunks; j += kSpmvWaves)
         __builtin_amdgcn_global_load_lds((gptr)(x + (j * kWave + lane) * 4),
                                          (lptr)(xs + j * kWave * 4), 16, 0, 0);
-    for (int c = chunks * kWave * 4 + int(threadIdx.x); c < N; c += kSpmvThreads) xs[c] = x[c];
+}
+__device__ __forceinline__ void stage_x_tail(float *xs, const float *__restrict__ x, int N) {
+    for (int c = N / (kWave * 4) * (kWave * 4) + int(threadIdx.x); c < N; c += kSpmvThreads)
+        xs[c] = x[c];
 }
 
 template <typename Tw, typename Tx, bool LDS, int SB, bool PK, bool LOOP>
@@ -273,8 +305,9 @@ __global__ __launch_bounds__(kSpmvThreads) void spmv_kernel(
     // A workgroup stages x once and then takes blocks blockIdx.x, + gridDim.x, ...
     // (LOOP; otherwise the grid has one workgroup per block, and the kernel keeps
     // no state across blocks, so it needs fewer registers); each block is
-    // kSpmvWaves tiles of one group.  setup() reads a block's group geometry and
-    // issues the first round of the lane's vectors.
+    // kSpmvWaves tiles of one group.  geometry() reads a block's group geometry and
+    // issues the load of the lane's output row; issue() issues the first round of the
+    // lane's vectors.
     int g, lgL, L, lb, nblk, sub, nvec;
     int64_t rows, first_row, first_elem, row, j0, e0;
     bool vec_path, row_ok;
@@ -284,7 +317,7 @@ __global__ __launch_bounds__(kSpmvThreads) void spmv_kernel(
     const typename WV::V *vrow;
     typename WV::V wv[kVmax];
     typename OV::Raw ov[kVmax];
-    auto setup = [&](int blk) {
+    auto geometry = [&](int blk) {
         g = block_group(sch, blk);
         lgL = pick(sch.log2_lanes, g);
         L = 1 << lgL;
@@ -304,8 +337,9 @@ __global__ __launch_bounds__(kSpmvThreads) void spmv_kernel(
         nvec = vec_path ? nblk / VEC : nblk;
         go = group_offsets(offs, bins, g);
         dest = perm[first_row + row_c];
-        scale = kScaled<Tw> ? scales[dest] : 1.0f;
         vrow = reinterpret_cast<const typename WV::V *>(values + e0);
+    };
+    auto issue = [&]() {
         if (vec_path) {
 #pragma unroll
             for (int t = 0; t < kVmax; ++t) {
@@ -317,17 +351,28 @@ __global__ __launch_bounds__(kSpmvThreads) void spmv_kernel(
                 }
             }
         }
+        // INT8: the row's scale, loaded once its index has arrived (the vector loads
+        // are already on their way)
+        scale = kScaled<Tw> ? scales[dest] : 1.0f;
     };
 
-    // the first block's vectors are issued before x is staged
+    // The output row's index, then x's loads, then the first block's vectors: the
+    // staging's memory latency overlaps the format's instead of queueing behind it.
+    constexpr bool kDirect = SB == 0 && std::is_same<Tx, float>::value;  // fp32 x, 16 B aligned
+    XStage<Tx, (SB > 0 ? SB : 1)> xst;
     int blk = int(blockIdx.x);
-    setup(blk);
+    geometry(blk);
     if constexpr (LDS) {
-        if constexpr (SB == 0 && std::is_same<Tx, float>::value) {   // fp32 x, 16 B aligned
-            stage_x_direct(xs, x, N);
-            __builtin_amdgcn_s_waitcnt(0);                // the direct loads have landed
+        if constexpr (kDirect) stage_x_direct(xs, x, N);
+        else xst.issue(x, N);
+    }
+    issue();
+    if constexpr (LDS) {
+        if constexpr (kDirect) {
+            stage_x_tail(xs, x, N);
+            __builtin_amdgcn_s_waitcnt(0);                 // the direct loads have landed
         } else {
-            stage_x<Tx, SB>(xs, x, N);
+            xst.commit(xs, x, N);
         }
         __syncthreads();
     }
@@ -373,13 +418,14 @@ __global__ __launch_bounds__(kSpmvThreads) void spmv_kernel(
             }
         }
 
-        for (int m = L >> 1; m >= 1; m >>= 1) acc += __shfl_xor(acc, m, kWave);
+        acc = group_sum(acc, lgL);
         if (row_ok && sub == 0) y[dest] = kScaled<Tw> ? acc * scale : acc;
 
         if constexpr (!LOOP) break;
         blk += int(gridDim.x);
         if (blk >= total_blocks) break;                  // uniform
-        setup(blk);
+        geometry(blk);
+        issue();
     }
 }
 
