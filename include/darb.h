@@ -274,6 +274,23 @@ int darb_prune_counts(int64_t M, int64_t N, int wdtype, const void *W, int64_t l
                       int64_t *counts, void *workspace, int64_t workspace_bytes, void *stream);
 
 /*
+ * darb_prune_counts for callers that cannot allocate device memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid allocation): the same
+ * arguments and the same counts, bit for bit, without the workspace.  Its scratch
+ * is a fixed 8 MiB array in the library's device code, one per device, held until
+ * the process ends; the first call on a device looks up that device's copy (no
+ * allocation).  The array holds the per-row counters (16 bytes per row), so M is
+ * limited to 490 464 rows (larger M: DARB_E_INVALID, naming the limit);
+ * the rest is candidate room, and a matrix whose candidates do not fit takes more
+ * passes over W with the same result.  Every call on a device shares its array and
+ * leaves its contents there (each call clears what must start at zero), so calls
+ * that overlap on one device -- on different streams or threads -- race.
+ * Errors: DARB_E_INVALID, DARB_E_DTYPE, DARB_E_HIP.
+ */
+int darb_prune_counts_noalloc(int64_t M, int64_t N, int wdtype, const void *W, int64_t ldw,
+                              int64_t k, int64_t *counts, void *stream);
+
+/*
  * One LSTM layer over a sequence with DARB-stored weights (the recurrent
  * models of section 4.1): no bias, gate order (i, f, g, o),
  *   gates_t = W_ih x_t + W_hh h_{t-1},

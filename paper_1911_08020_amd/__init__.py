@@ -89,6 +89,7 @@ def _load_library():
         "darb_plan_create_counts": ([I64, I64, P, I64, I, I, I, ctypes.POINTER(P)], I),
         "darb_prune_workspace": ([I64, I64, I, ctypes.POINTER(I64)], I),
         "darb_prune_counts": ([I64, I64, I, P, I64, I64, P, P, I64, P], I),
+        "darb_prune_counts_noalloc": ([I64, I64, I, P, I64, I64, P, P], I),
         "darb_pack_offsets": ([P, P, P, P], I),
         "darb_unpack_offsets": ([P, P, P, P], I),
         "darb_spmv_packed": ([P, I, P, P, I, P, P, P], I),
@@ -113,7 +114,7 @@ _lib = _load_library()
 
 #: every symbol include/darb.h declares
 EXPORTED = ("darb_plan_create", "darb_plan_create_counts", "darb_prune_workspace",
-            "darb_prune_counts", "darb_plan_info", "darb_plan_export", "darb_plan_upload",
+            "darb_prune_counts", "darb_prune_counts_noalloc", "darb_plan_info", "darb_plan_export", "darb_plan_upload",
             "darb_plan_destroy", "darb_encode", "darb_decode", "darb_spmv", "darb_spmm",
             "darb_pack_offsets", "darb_unpack_offsets", "darb_spmv_packed", "darb_spmm_packed",
             "darb_quantize_i8", "darb_spmv_i8", "darb_spmm_i8", "darb_lstm_layer",

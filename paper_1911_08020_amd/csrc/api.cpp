@@ -491,6 +491,27 @@ int darb_prune_counts(int64_t M, int64_t N, int wdtype, const void *W, int64_t l
                                         static_cast<hipStream_t>(stream)), "prune launch");
 }
 
+int darb_prune_counts_noalloc(int64_t M, int64_t N, int wdtype, const void *W, int64_t ldw,
+                              int64_t k, int64_t *counts, void *stream) {
+    clear_error();
+    if (M < 1 || M >= (int64_t(1) << 31) || N < 1 || N >= (int64_t(1) << 31))
+        return fail(DARB_E_INVALID, "M and N must be in [1, 2^31)");
+    if (!valid_dtype(wdtype)) return fail(DARB_E_DTYPE, "unknown weight dtype");
+    if (!W || !counts) return fail(DARB_E_INVALID, "NULL buffer");
+    if (ldw < N) return fail(DARB_E_INVALID, "ldw < N");
+    if (k < 0 || k > M * N) return fail(DARB_E_INVALID, "k must be in [0, M*N]");
+    if ((reinterpret_cast<uintptr_t>(counts) & 7) != 0)
+        return fail(DARB_E_INVALID, "counts must be 8-byte aligned");
+    const int64_t max_rows = prune_static_max_rows();
+    if (M > max_rows)
+        return fail(DARB_E_INVALID, "M = " + std::to_string(M) + " exceeds the fixed pruning "
+                                    "scratch (at most " + std::to_string(max_rows) +
+                                    " rows); use darb_prune_counts with a workspace");
+    const hipError_t e = launch_prune_counts_static(M, N, wdtype, W, ldw, k, counts,
+                                                    static_cast<hipStream_t>(stream));
+    return launched(e, "prune launch (fixed scratch)");
+}
+
 // Workspace of the LSTM layer, in floats: U [4H x T*batch] and G [4H x batch].
 static int64_t lstm_workspace_floats(int64_t H, int64_t T, int64_t batch) {
     return 4 * H * T * batch + 4 * H * batch;

@@ -93,6 +93,11 @@ hipError_t launch_unpack_offsets(const darb_plan &p, const uint32_t *packed, uin
 int64_t prune_workspace_bytes(int64_t M, int64_t N, int wdtype);
 hipError_t launch_prune_counts(int64_t M, int64_t N, int wdtype, const void *W, int64_t ldw,
                                int64_t k, int64_t *counts, void *workspace, hipStream_t s);
+// the same with the workspace in the library's fixed per-device array (no allocation);
+// M must be at most prune_static_max_rows()
+int64_t prune_static_max_rows();
+hipError_t launch_prune_counts_static(int64_t M, int64_t N, int wdtype, const void *W,
+                                      int64_t ldw, int64_t k, int64_t *counts, hipStream_t s);
 // One fused LSTM step (recurrent product and gate cell of every hidden unit), when
 // lstm_step_fusable: h_in is read, h_out written (distinct buffers).
 bool lstm_step_fusable(const darb_plan &whh, int64_t batch, const float *h, const float *h2);

@@ -35,6 +35,8 @@
 // All state stays on the device; nothing returns to the host between passes.
 #include <algorithm>
 
+#include <mutex>
+
 #include "darb_internal.h"
 
 namespace darb {
@@ -721,7 +723,7 @@ PruneWorkspace prune_workspace(int64_t M, int64_t N, void *base) {
 
 template <typename Bits>
 hipError_t launch_prune_t(int64_t M, int64_t N, const void *Wv, int64_t ldw, int64_t k,
-                          int64_t *counts, void *workspace, hipStream_t s) {
+                          int64_t *counts, void *workspace, int64_t cand_room, hipStream_t s) {
     using Tr = PruneTraits<Bits>;
     const Bits *W = static_cast<const Bits *>(Wv);
     const PruneWorkspace w = prune_workspace(M, N, workspace);
@@ -747,7 +749,7 @@ hipError_t launch_prune_t(int64_t M, int64_t N, const void *Wv, int64_t ldw, int
     const int widths32[3] = {11, 10, 10}, widths16[2] = {8, 7};
     const int *widths = Tr::KEY_BITS == 31 ? widths32 : widths16;
     const int passes = Tr::KEY_BITS == 31 ? 3 : 2;
-    const uint64_t cap = uint64_t(cand_capacity(M, N));
+    const uint64_t cap = uint64_t(cand_room);
     auto *gt1_u = reinterpret_cast<unsigned long long *>(w.gt1);
     // more predicted candidates than this and the sample's bracket is not used
     const uint64_t cand_limit =
@@ -810,8 +812,71 @@ int64_t prune_workspace_bytes(int64_t M, int64_t N, int wdtype) {
 
 hipError_t launch_prune_counts(int64_t M, int64_t N, int wdtype, const void *W, int64_t ldw,
                                int64_t k, int64_t *counts, void *workspace, hipStream_t s) {
-    if (wdtype == DARB_F32) return launch_prune_t<uint32_t>(M, N, W, ldw, k, counts, workspace, s);
-    return launch_prune_t<uint16_t>(M, N, W, ldw, k, counts, workspace, s);
+    const int64_t room = cand_capacity(M, N);
+    if (wdtype == DARB_F32)
+        return launch_prune_t<uint32_t>(M, N, W, ldw, k, counts, workspace, room, s);
+    return launch_prune_t<uint16_t>(M, N, W, ldw, k, counts, workspace, room, s);
+}
+
+// ---------------------------------------------------------------------------------
+// The same pruning with its workspace in a fixed device array, for callers that
+// cannot allocate.  Every call on a device shares that device's array (the init
+// kernel clears what must start at zero on each call), so calls that overlap on one
+// device race.  The array holds the radix-select state, the digit totals, the two
+// per-row counters (16 bytes per row) and a candidate room of whatever is left,
+// never less than kStaticMinRoom keys; a smaller room than the allocating call's
+// only sends more of the later passes back to W (same counts).
+// ---------------------------------------------------------------------------------
+
+namespace {
+constexpr int64_t kStaticScratchBytes = int64_t(8) << 20;
+constexpr int64_t kStaticMinRoom = int64_t(1) << 16;
+constexpr int kMaxDevices = 64;
+}  // namespace
+
+static __device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
+
+int64_t prune_static_max_rows() {
+    const PruneOffsets o = prune_offsets(1, 1);
+    // fixed part, then 2 x align256(8 M) of row counters, then the minimum room
+    const int64_t fixed = o.eq;
+    const int64_t avail = kStaticScratchBytes - fixed - kStaticMinRoom * int64_t(sizeof(uint64_t));
+    return avail / (2 * int64_t(sizeof(int64_t))) / 32 * 32;   // keeps each counter 256-aligned
+}
+
+// The device address of `scratch` on the current device, looked up once per device
+// (each device holds its own copy of the array at its own address).
+static hipError_t static_scratch(void **ptr) {
+    static std::mutex mu;
+    static void *addr[kMaxDevices] = {};
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(mu);
+    if (!addr[dev]) {
+        void *p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        addr[dev] = p;
+    }
+    *ptr = addr[dev];
+    return hipSuccess;
+}
+
+hipError_t launch_prune_counts_static(int64_t M, int64_t N, int wdtype, const void *W,
+                                      int64_t ldw, int64_t k, int64_t *counts, hipStream_t s) {
+    void *ws = nullptr;
+    const hipError_t e = static_scratch(&ws);
+    if (e != hipSuccess) return e;
+    const PruneOffsets o = prune_offsets(M, N);
+    const int64_t avail = (kStaticScratchBytes - o.cand) / int64_t(sizeof(uint64_t));
+    const int64_t full = cand_capacity(M, N);
+    if (avail < full && avail < kStaticMinRoom) return hipErrorInvalidValue;   // caller checked M
+    const int64_t room = avail < full ? avail : full;
+    if (wdtype == DARB_F32)
+        return launch_prune_t<uint32_t>(M, N, W, ldw, k, counts, ws, room, s);
+    return launch_prune_t<uint16_t>(M, N, W, ldw, k, counts, ws, room, s);
 }
 
 }  // namespace darb

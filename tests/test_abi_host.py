@@ -203,6 +203,11 @@ def test_null_arguments_and_not_uploaded():
     assert L.darb_plan_upload(p.handle, ctypes.c_void_p(0x1000), 4, None) == darb.E_WORKSPACE
     assert L.darb_stream_read(None, 16, buf, None) == darb.E_INVALID
     assert L.darb_stream_copy(buf, buf, 15, None) == darb.E_INVALID
+    # the pruning call without a workspace names its row limit before touching a device
+    assert L.darb_prune_counts_noalloc(1 << 20, 4, darb.F32, buf, 4, 0, buf, None) == \
+        darb.E_INVALID
+    assert b"fixed pruning scratch" in L.darb_last_error()
+    assert L.darb_prune_counts_noalloc(4, 4, 7, buf, 4, 0, buf, None) == darb.E_DTYPE
     L.darb_plan_destroy(None)                        # ignored
 
 
