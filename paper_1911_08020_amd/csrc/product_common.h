@@ -201,6 +201,7 @@ template <> struct Off<true, 16> {
 constexpr int kSpmvThreads = 256;
 constexpr int kSpmvWaves = kSpmvThreads / kWave;
 constexpr int kVmax = 8;                         // vectors per lane per round
+constexpr int kLoopVmax = 4;                     // the same for the looping form
 constexpr int kLdsMaxFloats = 16384;             // x staged in LDS up to 64 KiB
 constexpr int64_t kLdsPerCu = 160 * 1024;        // LDS of one gfx950 CU
 
@@ -297,76 +298,125 @@ __global__ __launch_bounds__(kSpmvThreads) void spmv_kernel(
     constexpr int VEC = WV::VEC;
     using OV = Off<PK, VEC>;
     using OS = Off<PK, 1>;
+    // vectors per lane and round: the looping form keeps two blocks in registers, so it
+    // holds half as many per block (its launches are scheduled for kLoopVmax)
+    constexpr int KV = LOOP ? kLoopVmax : kVmax;
     extern __shared__ float xs[];
 
     const int wave = wave_uniform(int(threadIdx.x) / kWave);
     const int lane = int(threadIdx.x) & (kWave - 1);
 
     // A workgroup stages x once and then takes blocks blockIdx.x, + gridDim.x, ...
-    // (LOOP; otherwise the grid has one workgroup per block, and the kernel keeps
-    // no state across blocks, so it needs fewer registers); each block is
-    // kSpmvWaves tiles of one group.  geometry() reads a block's group geometry and
-    // issues the load of the lane's output row; issue() issues the first round of the
-    // lane's vectors.
-    int g, lgL, L, lb, nblk, sub, nvec;
-    int64_t rows, first_row, first_elem, row, j0, e0;
-    bool vec_path, row_ok;
-    GroupOffsets go;
-    int32_t dest;
-    float scale;
-    const typename WV::V *vrow;
-    typename WV::V wv[kVmax];
-    typename OV::Raw ov[kVmax];
-    auto geometry = [&](int blk) {
-        g = block_group(sch, blk);
-        lgL = pick(sch.log2_lanes, g);
-        L = 1 << lgL;
-        lb = pick(bins.log2b, g);
-        nblk = int(pick(bins.nblk, g));
-        rows = pick(bins.rows, g);
-        first_row = pick(bins.first_row, g);
-        first_elem = pick(bins.first_elem, g);
-        vec_path = pick(sch.vec, g) == VEC;
-        const int64_t tile = int64_t(blk - block_begin_of(sch, g)) * kSpmvWaves + wave;
-        row = (tile << (6 - lgL)) + (lane >> lgL);
-        row_ok = row < rows;
-        const int64_t row_c = row_ok ? row : rows - 1;
-        sub = lane & (L - 1);
-        j0 = row_c * nblk;                                // the row's first slot in its group
-        e0 = first_elem + j0;
-        nvec = vec_path ? nblk / VEC : nblk;
-        go = group_offsets(offs, bins, g);
-        dest = perm[first_row + row_c];
-        vrow = reinterpret_cast<const typename WV::V *>(values + e0);
+    // (LOOP; otherwise the grid has one workgroup per block and keeps one block's
+    // state, so it needs fewer registers); each block is kSpmvWaves tiles of one
+    // group.  A Tile holds one block's state: geometry() reads the block's group
+    // geometry and issues the load of the lane's output row, issue() the first round of
+    // the lane's vectors, finish() sums them and writes the row.  LOOP keeps two Tiles
+    // and issues the next block's loads before summing the current one.
+    struct Tile {
+        int g, lgL, L, lb, nblk, sub, nvec;
+        int64_t j0, e0;
+        bool vec_path, row_ok;
+        GroupOffsets go;
+        int32_t dest;
+        float scale;
+        const typename WV::V *vrow;
+        typename WV::V wv[KV];
+        typename OV::Raw ov[KV];
     };
-    auto issue = [&]() {
-        if (vec_path) {
+    auto geometry = [&](Tile &T, int blk) {
+        T.g = block_group(sch, blk);
+        T.lgL = pick(sch.log2_lanes, T.g);
+        T.L = 1 << T.lgL;
+        T.lb = pick(bins.log2b, T.g);
+        T.nblk = int(pick(bins.nblk, T.g));
+        const int64_t rows = pick(bins.rows, T.g);
+        const int64_t first_row = pick(bins.first_row, T.g);
+        T.vec_path = pick(sch.vec, T.g) == VEC;
+        const int64_t tile = int64_t(blk - block_begin_of(sch, T.g)) * kSpmvWaves + wave;
+        const int64_t row = (tile << (6 - T.lgL)) + (lane >> T.lgL);
+        T.row_ok = row < rows;
+        const int64_t row_c = T.row_ok ? row : rows - 1;
+        T.sub = lane & (T.L - 1);
+        T.j0 = row_c * T.nblk;                            // the row's first slot in its group
+        T.e0 = pick(bins.first_elem, T.g) + T.j0;
+        T.nvec = T.vec_path ? T.nblk / VEC : T.nblk;
+        T.go = group_offsets(offs, bins, T.g);
+        T.dest = perm[first_row + row_c];
+        T.vrow = reinterpret_cast<const typename WV::V *>(values + T.e0);
+    };
+    auto issue = [&](Tile &T) {
+        if (T.vec_path) {
 #pragma unroll
-            for (int t = 0; t < kVmax; ++t) {
-                if (t * L < nvec) {                      // wave-uniform
-                    const int vi = sub + t * L;
-                    const int vc = vi < nvec ? vi : nvec - 1;
-                    wv[t] = __builtin_nontemporal_load(vrow + vc);
-                    ov[t] = OV::load(go, j0 + int64_t(vc) * VEC);
+            for (int t = 0; t < KV; ++t) {
+                if (t * T.L < T.nvec) {                  // wave-uniform
+                    const int vi = T.sub + t * T.L;
+                    const int vc = vi < T.nvec ? vi : T.nvec - 1;
+                    T.wv[t] = __builtin_nontemporal_load(T.vrow + vc);
+                    T.ov[t] = OV::load(T.go, T.j0 + int64_t(vc) * VEC);
                 }
             }
         }
         // INT8: the row's scale, loaded once its index has arrived (the vector loads
         // are already on their way)
-        scale = kScaled<Tw> ? scales[dest] : 1.0f;
+        T.scale = kScaled<Tw> ? scales[T.dest] : 1.0f;
+    };
+    auto xat = [&](int c) -> float {
+        // offsets from the encode always give c < N; the global path clamps anyway
+        // so a malformed offset cannot read outside x
+        if constexpr (LDS) return xs[c];
+        else return to_f32<Tx>(x[c < N ? c : N - 1]);
+    };
+    auto finish = [&](Tile &T) {
+        float acc = 0.0f;
+        if (T.vec_path) {
+            for (int base = 0;; base += T.L * KV) {
+#pragma unroll
+                for (int t = 0; t < KV; ++t) {
+                    const int vi = base + T.sub + t * T.L;
+                    if (vi < T.nvec) {
+                        const typename OV::Bits ob = OV::bits(T.ov[t], T.go);
+#pragma unroll
+                        for (int q = 0; q < VEC; ++q) {
+                            const int c = ((vi * VEC + q) << T.lb) + OV::field(ob, q, T.go);
+                            acc = fmaf(WV::get(T.wv[t], q), xat(c), acc);
+                        }
+                    }
+                }
+                if (base + T.L * KV >= T.nvec) break;
+#pragma unroll
+                for (int t = 0; t < KV; ++t) {
+                    if (base + T.L * KV + t * T.L < T.nvec) {   // wave-uniform
+                        const int vi = base + T.L * KV + T.sub + t * T.L;
+                        const int vc = vi < T.nvec ? vi : T.nvec - 1;
+                        T.wv[t] = __builtin_nontemporal_load(T.vrow + vc);
+                        T.ov[t] = OV::load(T.go, T.j0 + int64_t(vc) * VEC);
+                    }
+                }
+            }
+        } else {
+            const Tw *vr = values + T.e0;
+            for (int k = T.sub; k < T.nblk; k += T.L) {
+                const int o = OS::field(OS::bits(OS::load(T.go, T.j0 + k), T.go), 0, T.go);
+                acc = fmaf(to_f32<Tw>(vr[k]), xat((k << T.lb) + o), acc);
+            }
+        }
+        acc = group_sum(acc, T.lgL);
+        if (T.row_ok && T.sub == 0) y[T.dest] = kScaled<Tw> ? acc * T.scale : acc;
     };
 
     // The output row's index, then x's loads, then the first block's vectors: the
     // staging's memory latency overlaps the format's instead of queueing behind it.
     constexpr bool kDirect = SB == 0 && std::is_same<Tx, float>::value;  // fp32 x, 16 B aligned
     XStage<Tx, (SB > 0 ? SB : 1)> xst;
+    Tile A;
     int blk = int(blockIdx.x);
-    geometry(blk);
+    geometry(A, blk);
     if constexpr (LDS) {
         if constexpr (kDirect) stage_x_direct(xs, x, N);
         else xst.issue(x, N);
     }
-    issue();
+    issue(A);
     if constexpr (LDS) {
         if constexpr (kDirect) {
             stage_x_tail(xs, x, N);
@@ -376,56 +426,27 @@ __global__ __launch_bounds__(kSpmvThreads) void spmv_kernel(
         }
         __syncthreads();
     }
-    auto xat = [&](int c) -> float {
-        // offsets from the encode always give c < N; the global path clamps anyway
-        // so a malformed offset cannot read outside x
-        if constexpr (LDS) return xs[c];
-        else return to_f32<Tx>(x[c < N ? c : N - 1]);
-    };
-
-    for (;;) {
-        float acc = 0.0f;
-        if (vec_path) {
-            for (int base = 0;; base += L * kVmax) {
-#pragma unroll
-                for (int t = 0; t < kVmax; ++t) {
-                    const int vi = base + sub + t * L;
-                    if (vi < nvec) {
-                        const typename OV::Bits ob = OV::bits(ov[t], go);
-#pragma unroll
-                        for (int q = 0; q < VEC; ++q) {
-                            const int c = ((vi * VEC + q) << lb) + OV::field(ob, q, go);
-                            acc = fmaf(WV::get(wv[t], q), xat(c), acc);
-                        }
-                    }
-                }
-                if (base + L * kVmax >= nvec) break;
-#pragma unroll
-                for (int t = 0; t < kVmax; ++t) {
-                    if (base + L * kVmax + t * L < nvec) {   // wave-uniform
-                        const int vi = base + L * kVmax + sub + t * L;
-                        const int vc = vi < nvec ? vi : nvec - 1;
-                        wv[t] = __builtin_nontemporal_load(vrow + vc);
-                        ov[t] = OV::load(go, j0 + int64_t(vc) * VEC);
-                    }
-                }
+    if constexpr (!LOOP) {
+        finish(A);
+    } else {
+        // software pipelined over the workgroup's blocks: the next block's loads are
+        // on their way while this one is summed
+        Tile B;
+        auto step = [&](Tile &cur, Tile &nxt) -> bool {
+            const int nb = blk + int(gridDim.x);
+            const bool more = nb < total_blocks;           // uniform
+            if (more) {
+                geometry(nxt, nb);
+                issue(nxt);
             }
-        } else {
-            const Tw *vr = values + e0;
-            for (int k = sub; k < nblk; k += L) {
-                const int o = OS::field(OS::bits(OS::load(go, j0 + k), go), 0, go);
-                acc = fmaf(to_f32<Tw>(vr[k]), xat((k << lb) + o), acc);
-            }
+            finish(cur);
+            blk = nb;
+            return more;
+        };
+        for (;;) {
+            if (!step(A, B)) break;
+            if (!step(B, A)) break;
         }
-
-        acc = group_sum(acc, lgL);
-        if (row_ok && sub == 0) y[dest] = kScaled<Tw> ? acc * scale : acc;
-
-        if constexpr (!LOOP) break;
-        blk += int(gridDim.x);
-        if (blk >= total_blocks) break;                  // uniform
-        geometry(blk);
-        issue();
     }
 }
 
@@ -906,9 +927,10 @@ inline bool offsets_aligned(const uint8_t *offsets, int vec) {
     return !offsets || reinterpret_cast<uintptr_t>(offsets) % vec == 0;
 }
 
+// vmax: vectors per lane the lanes-per-row choice aims at (<= kVmax)
 template <typename Tw>
 bool spmv_schedule(const darb_plan &p, const void *values, const uint8_t *offsets,
-                   ProductSchedule &s) {
+                   ProductSchedule &s, int vmax = kVmax) {
     constexpr int VEC = WVec<Tw>::VEC;
     s = ProductSchedule{};
     s.nbins = p.bins.nbins;
@@ -922,8 +944,8 @@ bool spmv_schedule(const darb_plan &p, const void *values, const uint8_t *offset
         const bool vec = ptr_ok && nblk % VEC == 0 && p.bins.first_elem[g] % VEC == 0;
         s.vec[g] = vec ? VEC : 1;
         const int64_t nvec = vec ? nblk / VEC : nblk;
-        int lgL = 0;     // fewest lanes per row that keep each lane within kVmax vectors
-        while (lgL < 6 && ((nvec + (int64_t(1) << lgL) - 1) >> lgL) > kVmax) ++lgL;
+        int lgL = 0;     // fewest lanes per row that keep each lane within vmax vectors
+        while (lgL < 6 && ((nvec + (int64_t(1) << lgL) - 1) >> lgL) > vmax) ++lgL;
         s.log2_lanes[g] = lgL;
         s.block_begin[g] = int32_t(blocks);
         const int64_t rows_per_wave = int64_t(kWave) >> lgL;
@@ -939,8 +961,16 @@ template <typename Tw, typename Tx, bool PK>
 hipError_t launch_spmv_t(const darb_plan &p, const void *values, const uint8_t *offsets,
                          const uint32_t *packed, const void *x, float *y, const float *scales,
                          hipStream_t st) {
+    // Up to kVmax vectors per lane, but a launch with fewer workgroups than compute
+    // units leaves CUs idle while each lane waits on a long run of loads: then rows
+    // spread over more lanes (4, then 2 vectors per lane).  INT8 and fp16 vectors hold
+    // 8 weights, so their small matrices need this most.
     ProductSchedule s;
-    if (!spmv_schedule<Tw>(p, values, offsets, s)) return hipErrorInvalidConfiguration;
+    const int64_t cus = p.cus > 0 ? p.cus : 256;
+    for (int vmax = kVmax;; vmax /= 2) {
+        if (!spmv_schedule<Tw>(p, values, offsets, s, vmax)) return hipErrorInvalidConfiguration;
+        if (vmax <= 2 || s.block_begin[s.nbins] >= cus) break;
+    }
     const int blocks = s.block_begin[s.nbins];
     if (blocks == 0) return hipSuccess;
     const Tw *v = static_cast<const Tw *>(values);
@@ -953,21 +983,25 @@ hipError_t launch_spmv_t(const darb_plan &p, const void *values, const uint8_t *
     int64_t per_cu = lds_per_group > 0 ? kLdsPerCu / lds_per_group : 8;
     per_cu = per_cu < 1 ? 1 : (per_cu > 8 ? 8 : per_cu);
     const int64_t resident = int64_t(p.cus > 0 ? p.cus : 256) * per_cu;
-    const int grid = int(blocks < resident ? blocks : resident);
+    // more blocks than fit at once: the looping form, scheduled for its registers
+    if (blocks > resident && !spmv_schedule<Tw>(p, values, offsets, s, kLoopVmax))
+        return hipErrorInvalidConfiguration;
+    const int blocks_l = s.block_begin[s.nbins];
+    const int grid = int(blocks_l < resident ? blocks_l : resident);
     if (p.N <= kLdsMaxFloats) {
         const size_t lds = size_t(p.N) * sizeof(float);
         const int64_t nv = p.N / (16 / int64_t(sizeof(Tx)));
         const int64_t per_thread = (nv + kSpmvThreads - 1) / kSpmvThreads;
 #define DARB_SPMV_LDS(SB)                                                                    \
     do {                                                                                    \
-        if (grid < blocks)                                                                  \
+        if (grid < blocks_l)                                                                  \
             hipLaunchKernelGGL((spmv_kernel<Tw, Tx, true, SB, PK, true>), dim3(grid),       \
                                dim3(kSpmvThreads), lds, st, v, offs, xx, y, p.d_perm, N,    \
-                               p.bins, s, scales, blocks);                                  \
+                               p.bins, s, scales, blocks_l);                                  \
         else                                                                                \
             hipLaunchKernelGGL((spmv_kernel<Tw, Tx, true, SB, PK, false>), dim3(grid),      \
                                dim3(kSpmvThreads), lds, st, v, offs, xx, y, p.d_perm, N,    \
-                               p.bins, s, scales, blocks);                                  \
+                               p.bins, s, scales, blocks_l);                                  \
     } while (0)
         bool direct = false;
         if constexpr (std::is_same<Tx, float>::value) {
@@ -982,14 +1016,14 @@ hipError_t launch_spmv_t(const darb_plan &p, const void *values, const uint8_t *
         else DARB_SPMV_LDS(16);
 #undef DARB_SPMV_LDS
     } else {
-        if (grid < blocks)
+        if (grid < blocks_l)
             hipLaunchKernelGGL((spmv_kernel<Tw, Tx, false, 1, PK, true>), dim3(grid),
                                dim3(kSpmvThreads), 0, st, v, offs, xx, y, p.d_perm, N, p.bins, s,
-                               scales, blocks);
+                               scales, blocks_l);
         else
             hipLaunchKernelGGL((spmv_kernel<Tw, Tx, false, 1, PK, false>), dim3(grid),
                                dim3(kSpmvThreads), 0, st, v, offs, xx, y, p.d_perm, N, p.bins, s,
-                               scales, blocks);
+                               scales, blocks_l);
     }
     return hipGetLastError();
 }
