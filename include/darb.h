@@ -115,6 +115,28 @@ int darb_plan_create(int64_t M, int64_t N, const double *row_density, double mat
 int darb_plan_create_counts(int64_t M, int64_t N, const int64_t *row_count, int64_t kept,
                             int round_mode, int b_min, int b_max, darb_plan **out);
 
+/*
+ * The plan built on the device, from kept counts in device memory (the flow of
+ * section 3.2 from the irregular mask to block sizes, with darb_prune_counts' output
+ * left where it is).  The same block-size rule as darb_plan_create_counts, in both
+ * rounding modes and with the same results; the storage order and the per-row table
+ * are written straight into `workspace`, which becomes the plan's device workspace
+ * (the plan comes back uploaded on the current device; darb_plan_upload is refused
+ * for it).  Only the group sizes (32 int64) travel to the host, so the call waits for
+ * `stream`.  darb_plan_export copies the tables back from the device.
+ *   row_count  device int64 [M], 8-byte aligned, each in [0, N] (as darb_prune_counts
+ *              writes them; larger values count as N, negative ones as 0)
+ *   kept       the matrix's kept count k, in [0, M * N] (D = k / (M N))
+ *   workspace  device, 256-byte aligned, >= darb_plan_device_workspace(M) bytes; it must
+ *              stay allocated and unmodified while the plan is used
+ * Other arguments as for darb_plan_create.
+ * Errors: DARB_E_INVALID, DARB_E_WORKSPACE, DARB_E_NOMEM, DARB_E_HIP.
+ */
+int darb_plan_device_workspace(int64_t M, int64_t *bytes);
+int darb_plan_create_device(int64_t M, int64_t N, const int64_t *row_count, int64_t kept,
+                            int round_mode, int b_min, int b_max, void *workspace,
+                            int64_t workspace_bytes, void *stream, darb_plan **out);
+
 /* Sizes and groups of a plan.  Errors: DARB_E_INVALID (null pointer). */
 int darb_plan_info(const darb_plan *plan, darb_plan_info_t *info);
 

@@ -87,6 +87,8 @@ def _load_library():
         "darb_spmv": ([P, I, P, P, I, P, P, P], I),
         "darb_spmm": ([P, I, P, P, I, I64, P, I64, P, I64, P], I),
         "darb_plan_create_counts": ([I64, I64, P, I64, I, I, I, ctypes.POINTER(P)], I),
+        "darb_plan_device_workspace": ([I64, ctypes.POINTER(I64)], I),
+        "darb_plan_create_device": ([I64, I64, P, I64, I, I, I, P, I64, P, ctypes.POINTER(P)], I),
         "darb_prune_workspace": ([I64, I64, I, ctypes.POINTER(I64)], I),
         "darb_prune_counts": ([I64, I64, I, P, I64, I64, P, P, I64, P], I),
         "darb_prune_counts_noalloc": ([I64, I64, I, P, I64, I64, P, P], I),
@@ -113,7 +115,8 @@ def _load_library():
 _lib = _load_library()
 
 #: every symbol include/darb.h declares
-EXPORTED = ("darb_plan_create", "darb_plan_create_counts", "darb_prune_workspace",
+EXPORTED = ("darb_plan_create", "darb_plan_create_counts", "darb_plan_device_workspace",
+            "darb_plan_create_device", "darb_prune_workspace",
             "darb_prune_counts", "darb_prune_counts_noalloc", "darb_plan_info", "darb_plan_export", "darb_plan_upload",
             "darb_plan_destroy", "darb_encode", "darb_decode", "darb_spmv", "darb_spmm",
             "darb_pack_offsets", "darb_unpack_offsets", "darb_spmv_packed", "darb_spmm_packed",
@@ -199,6 +202,10 @@ class Plan:
             _check(_lib.darb_plan_create_counts(int(M), int(N), c.ctypes.data_as(ctypes.c_void_p),
                                                 int(kept), int(mode), int(b_min), int(b_max),
                                                 ctypes.byref(h)), "darb_plan_create_counts")
+        self._take(h)
+        self.workspace = None
+
+    def _take(self, h):
         self._h = h
         info = _Info()
         _check(_lib.darb_plan_info(h, ctypes.byref(info)), "darb_plan_info")
@@ -208,7 +215,32 @@ class Plan:
         self.bins = [dict(log2b=b.log2b, first_row=b.first_row, rows=b.rows,
                           first_elem=b.first_elem, nblk=b.nblk, first_word=b.first_word)
                      for b in info.bins[:info.nbins]]
-        self.workspace = None
+
+    @classmethod
+    def from_device_counts(cls, N: int, row_count, kept: int, mode: int = ROUND_FLOOR,
+                           b_min: int = 1, b_max: int = 128, stream=None):
+        """Plan built on the device from kept counts in device memory (``prune_counts``'s
+        output, never copied to the host); comes back uploaded, its workspace being the
+        one the tables were built in."""
+        torch = _torch()
+        _require_cuda(row_count)
+        if row_count.dim() != 1:
+            raise ValueError("row_count must be 1-D")
+        M = row_count.shape[0]
+        _check_format(row_count, M, "row_count", (torch.int64,))
+        need = ctypes.c_int64()
+        _check(_lib.darb_plan_device_workspace(M, ctypes.byref(need)), "darb_plan_device_workspace")
+        ws = torch.empty(need.value, dtype=torch.uint8, device=row_count.device)
+        h = ctypes.c_void_p()
+        with torch.cuda.device(row_count.device):
+            _check(_lib.darb_plan_create_device(int(M), int(N), _ptr(row_count), int(kept),
+                                                int(mode), int(b_min), int(b_max), _ptr(ws),
+                                                ws.numel(), _stream_ptr(stream), ctypes.byref(h)),
+                   "darb_plan_create_device")
+        self = cls.__new__(cls)
+        self._take(h)
+        self.workspace = ws
+        return self
 
     @classmethod
     def from_counts(cls, N: int, row_count, kept: int, mode: int = ROUND_FLOOR, b_min: int = 1,

@@ -8,7 +8,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libdarb.so")
 SOURCES = ["api.cpp", "encode.hip", "product.hip", "product_i8.hip", "packed.hip", "prune.hip",
-           "misc.hip"]
+           "plan.hip", "misc.hip"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",

@@ -208,6 +208,25 @@ int darb_plan_info(const darb_plan *p, darb_plan_info_t *info) {
 int darb_plan_export(const darb_plan *p, uint8_t *log2b, int64_t *row_start, int32_t *perm) {
     clear_error();
     if (!p) return fail(DARB_E_INVALID, "plan is NULL");
+    if (p->device_built) {
+        // the tables live only in the build workspace: copy them back
+        std::vector<int64_t> rowinfo;
+        try {
+            rowinfo.resize(p->M);
+        } catch (const std::bad_alloc &) {
+            return fail(DARB_E_NOMEM, "rowinfo");
+        }
+        hipError_t e = hipMemcpy(rowinfo.data(), p->d_rowinfo, p->M * sizeof(int64_t),
+                                 hipMemcpyDeviceToHost);
+        if (e == hipSuccess && perm)
+            e = hipMemcpy(perm, p->d_perm, p->M * sizeof(int32_t), hipMemcpyDeviceToHost);
+        if (e != hipSuccess) return fail(DARB_E_HIP, std::string("plan export: ") + hipGetErrorString(e));
+        for (int64_t r = 0; r < p->M; ++r) {
+            if (log2b) log2b[r] = uint8_t(rowinfo[r] & 0xFF);
+            if (row_start) row_start[r] = rowinfo[r] >> 8;
+        }
+        return DARB_OK;
+    }
     if (log2b) std::memcpy(log2b, p->log2b.data(), p->M * sizeof(uint8_t));
     if (row_start) std::memcpy(row_start, p->row_start.data(), p->M * sizeof(int64_t));
     if (perm) std::memcpy(perm, p->perm.data(), p->M * sizeof(int32_t));
@@ -217,6 +236,8 @@ int darb_plan_export(const darb_plan *p, uint8_t *log2b, int64_t *row_start, int
 int darb_plan_upload(darb_plan *p, void *workspace, int64_t workspace_bytes, void *stream) {
     clear_error();
     if (!p || !workspace) return fail(DARB_E_INVALID, "NULL argument");
+    if (p->device_built)
+        return fail(DARB_E_INVALID, "a plan built on the device stays in its build workspace");
     if ((reinterpret_cast<uintptr_t>(workspace) & 255) != 0)
         return fail(DARB_E_INVALID, "workspace must be 256-byte aligned");
     if (workspace_bytes < p->workspace_bytes)
@@ -254,6 +275,98 @@ int darb_plan_upload(darb_plan *p, void *workspace, int64_t workspace_bytes, voi
 }
 
 void darb_plan_destroy(darb_plan *p) { delete p; }
+
+static int64_t device_plan_bytes(int64_t M) {
+    return perm_bytes(M) + (M * int64_t(sizeof(int64_t)) + 255) / 256 * 256 +
+           plan_device_scratch_bytes(M);
+}
+
+int darb_plan_device_workspace(int64_t M, int64_t *bytes) {
+    clear_error();
+    if (!bytes || M < 1 || M >= (int64_t(1) << 31))
+        return fail(DARB_E_INVALID, "bytes is NULL or M not in [1, 2^31)");
+    *bytes = device_plan_bytes(M);
+    return DARB_OK;
+}
+
+int darb_plan_create_device(int64_t M, int64_t N, const int64_t *row_count, int64_t kept,
+                            int round_mode, int b_min, int b_max, void *workspace,
+                            int64_t workspace_bytes, void *stream, darb_plan **out) {
+    clear_error();
+    if (!out) return fail(DARB_E_INVALID, "out is NULL");
+    *out = nullptr;
+    if (M < 1 || M >= (int64_t(1) << 31)) return fail(DARB_E_INVALID, "M must be in [1, 2^31)");
+    if (N < 1 || N > kMaxColumns) return fail(DARB_E_INVALID, "N must be in [1, 2^31 - 256]");
+    if (!row_count || !workspace) return fail(DARB_E_INVALID, "NULL buffer");
+    if ((reinterpret_cast<uintptr_t>(row_count) & 7) != 0)
+        return fail(DARB_E_INVALID, "row_count must be 8-byte aligned");
+    if ((reinterpret_cast<uintptr_t>(workspace) & 255) != 0)
+        return fail(DARB_E_INVALID, "workspace must be 256-byte aligned");
+    if (kept < 0 || kept > M * N) return fail(DARB_E_INVALID, "kept must be in [0, M*N]");
+    if (round_mode != DARB_ROUND_FLOOR && round_mode != DARB_ROUND_PAPER)
+        return fail(DARB_E_INVALID, "unknown round_mode");
+    if (!is_pow2(b_min) || !is_pow2(b_max) || b_min > b_max || b_max > 128)
+        return fail(DARB_E_INVALID, "b_min, b_max must be powers of two, 1 <= b_min <= b_max <= 128");
+    const int64_t need = device_plan_bytes(M);
+    if (workspace_bytes < need)
+        return fail(DARB_E_WORKSPACE, "device plan needs " + std::to_string(need) + " bytes, got " +
+                                          std::to_string(workspace_bytes));
+    int dev = -1, cus = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e != hipSuccess) return fail(DARB_E_HIP, std::string("device: ") + hipGetErrorString(e));
+    char *base = static_cast<char *>(workspace);
+    int32_t *d_perm = reinterpret_cast<int32_t *>(base);
+    int64_t *d_rowinfo = reinterpret_cast<int64_t *>(base + perm_bytes(M));
+    void *scratch = base + perm_bytes(M) + (M * int64_t(sizeof(int64_t)) + 255) / 256 * 256;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    e = launch_plan_device(M, N, row_count, kept, round_mode, log2_exact(b_min), log2_exact(b_max),
+                           d_perm, d_rowinfo, scratch, s);
+    int64_t summary[4 * kMaxBins];
+    if (e == hipSuccess)
+        e = hipMemcpyAsync(summary, scratch, sizeof(summary), hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return fail(DARB_E_HIP, std::string("device plan: ") + hipGetErrorString(e));
+    darb_plan *p = new (std::nothrow) darb_plan();
+    if (!p) return fail(DARB_E_NOMEM, "plan allocation");
+    p->M = M;
+    p->N = N;
+    p->mode = round_mode;
+    p->b_min = b_min;
+    p->b_max = b_max;
+    BinTable &bt = p->bins;
+    bt.nbins = 0;
+    int64_t elem = 0, words = 0;
+    for (int l = 0; l <= kMaxLog2B; ++l) {
+        const int64_t rows = summary[l];
+        const int64_t nblk = (N + (int64_t(1) << l) - 1) >> l;
+        if (rows > 0) {
+            const int g = bt.nbins++;
+            bt.log2b[g] = l;
+            bt.first_row[g] = summary[kMaxBins + l];
+            bt.rows[g] = rows;
+            bt.first_elem[g] = summary[2 * kMaxBins + l];
+            bt.nblk[g] = nblk;
+            bt.first_word[g] = summary[3 * kMaxBins + l];
+        }
+        elem += rows * nblk;
+        words += (rows * nblk + 31) / 32 * l;
+    }
+    if (elem >= (int64_t(1) << 55)) {
+        delete p;
+        return fail(DARB_E_INVALID, "more than 2^55 retained weights");
+    }
+    p->nnz = elem;
+    p->packed_words = words;
+    p->workspace_bytes = need;
+    p->d_perm = d_perm;
+    p->d_rowinfo = d_rowinfo;
+    p->device = dev;
+    p->cus = cus;
+    p->device_built = true;
+    *out = p;
+    return DARB_OK;
+}
 
 }  // extern "C"
 

@@ -55,6 +55,7 @@ struct darb_plan {
     int64_t *d_rowinfo = nullptr;   // [M] (row_start[r] << 8) | log2b[r], original order
     int device = -1;
     int cus = 0;                    // compute units of that device
+    bool device_built = false;      // built on the device: the host vectors are empty
 };
 
 namespace darb {
@@ -108,6 +109,13 @@ hipError_t launch_lstm_step(const darb_plan &whh, int wdtype, const void *values
 hipError_t launch_lstm_cell(int64_t H, int64_t batch, const float *G, const float *U,
                             int64_t ldu, float *h, float *c, float *h_seq, int64_t ld_seq,
                             hipStream_t s);
+// The plan's storage order and per-row table from device-side kept counts, and the
+// group summary (rows, first_row, first_elem, first_word: 8 int64 each) at the start
+// of `scratch` (plan_device_scratch_bytes(M), 256-byte aligned).
+int64_t plan_device_scratch_bytes(int64_t M);
+hipError_t launch_plan_device(int64_t M, int64_t N, const int64_t *counts, int64_t kept, int mode,
+                              int lmin, int lmax, int32_t *perm, int64_t *rowinfo, void *scratch,
+                              hipStream_t s);
 hipError_t launch_stream_read(const void *buf, int64_t bytes, float *sink, hipStream_t s);
 hipError_t launch_stream_read_shape(const void *buf, int64_t bytes, int threads, int vectors,
                                    float *sink, hipStream_t s);

@@ -208,6 +208,24 @@ def test_null_arguments_and_not_uploaded():
         darb.E_INVALID
     assert b"fixed pruning scratch" in L.darb_last_error()
     assert L.darb_prune_counts_noalloc(4, 4, 7, buf, 4, 0, buf, None) == darb.E_DTYPE
+    # the device-built plan checks its arguments before touching a device
+    nb = ctypes.c_int64()
+    assert L.darb_plan_device_workspace(1000, ctypes.byref(nb)) == darb.OK and nb.value > 12000
+    assert L.darb_plan_device_workspace(0, ctypes.byref(nb)) == darb.E_INVALID
+    hp = ctypes.c_void_p()
+    ws = ctypes.c_void_p(0x100000)
+    assert L.darb_plan_create_device(10, 10, buf, 5, 0, 1, 128, None, 1 << 20, None,
+                                     ctypes.byref(hp)) == darb.E_INVALID
+    assert L.darb_plan_create_device(10, 10, buf, 5, 0, 1, 128, ctypes.c_void_p(0x100010),
+                                     1 << 20, None, ctypes.byref(hp)) == darb.E_INVALID
+    assert L.darb_plan_create_device(10, 10, buf, 5, 2, 1, 128, ws, 1 << 20, None,
+                                     ctypes.byref(hp)) == darb.E_INVALID
+    assert L.darb_plan_create_device(10, 10, buf, 101, 0, 1, 128, ws, 1 << 20, None,
+                                     ctypes.byref(hp)) == darb.E_INVALID
+    assert L.darb_plan_create_device(10, 10, buf, 5, 0, 4, 2, ws, 1 << 20, None,
+                                     ctypes.byref(hp)) == darb.E_INVALID
+    assert L.darb_plan_create_device(10, 10, buf, 5, 0, 1, 128, ws, 16, None,
+                                     ctypes.byref(hp)) == darb.E_WORKSPACE
     L.darb_plan_destroy(None)                        # ignored
 
 
