@@ -70,18 +70,27 @@ template <int CTRL> __device__ __forceinline__ float add_dpp(float v) {
                    0, __builtin_bit_cast(int, v), CTRL, 0xF, 0xF, false));
 }
 
-// Sum over aligned groups of 2^lgL lanes (lgL <= 6, wave-uniform): every lane of a
-// group ends with the group's sum.  The pairs are lanes 1 apart, then 2 (quad
-// permutations), then mirrored inside 8 and 16 lanes (row_half_mirror, row_mirror),
-// then 16 and 32 apart (bpermute); each step adds two equal partial sums, so the
-// result depends only on lgL and is the same in every lane of the group.
+// v plus the value DPP control CTRL selects, in the 16-lane rows ROWS enables (other
+// rows add +0.0, which leaves them unchanged)
+template <int CTRL, int ROWS> __device__ __forceinline__ float add_dpp_rows(float v) {
+    return v + __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(
+                   0, __builtin_bit_cast(int, v), CTRL, ROWS, 0xF, false));
+}
+
+// Sum over aligned groups of 2^lgL lanes (lgL <= 6, wave-uniform); the group's sum
+// ends in its last lane.  The pairs are lanes 1 apart, then 2 (quad permutations),
+// then mirrored inside 8 and 16 lanes (row_half_mirror, row_mirror): after these
+// every lane of a 16-lane row holds the row's sum.  Rows then meet by broadcasts:
+// row 1 adds row 0 and row 3 adds row 2 (row_bcast:15), then row 3 adds row 1
+// (row_bcast:31).  Each step adds two partial sums of equal size, so the result
+// depends only on lgL, and no step goes through LDS.
 __device__ __forceinline__ float group_sum(float v, int lgL) {
     if (lgL >= 1) v = add_dpp<0xB1>(v);     // quad_perm [1, 0, 3, 2]
     if (lgL >= 2) v = add_dpp<0x4E>(v);     // quad_perm [2, 3, 0, 1]
     if (lgL >= 3) v = add_dpp<0x141>(v);    // row_half_mirror
     if (lgL >= 4) v = add_dpp<0x140>(v);    // row_mirror
-    if (lgL >= 5) v += __shfl_xor(v, 16, kWave);
-    if (lgL >= 6) v += __shfl_xor(v, 32, kWave);
+    if (lgL >= 5) v = add_dpp_rows<0x142, 0xA>(v);   // row_bcast:15 into rows 1 and 3
+    if (lgL >= 6) v = add_dpp_rows<0x143, 0x8>(v);   // row_bcast:31 into row 3
     return v;
 }
 
@@ -402,7 +411,7 @@ __global__ __launch_bounds__(kSpmvThreads) void spmv_kernel(
             }
         }
         acc = group_sum(acc, T.lgL);
-        if (T.row_ok && T.sub == 0) y[T.dest] = kScaled<Tw> ? acc * T.scale : acc;
+        if (T.row_ok && T.sub == T.L - 1) y[T.dest] = kScaled<Tw> ? acc * T.scale : acc;
     };
 
     // The output row's index, then x's loads, then the first block's vectors: the
@@ -448,6 +457,181 @@ __global__ __launch_bounds__(kSpmvThreads) void spmv_kernel(
             if (!step(B, A)) break;
         }
     }
+}
+
+// ---------------------------------------------------------------------------------
+// SpMV in one pass of workgroups: workgroup (bx, g) takes four waves' tiles of rows
+// of group g (blockIdx.y = g), so a wave's geometry needs no search.  Every input
+// of the launch arrives with one round of scalar loads (the 64-byte header and the
+// group's 32-byte record), issued by hand: a workgroup's first vector load waits on
+// that round only.  Each wave loads its output row's index, then its share of x
+// into LDS, then all its vectors; before the barrier it waits only until its share
+// of x has landed (the vector loads return in order after it), so no wave waits for
+// another wave's format data.
+// ---------------------------------------------------------------------------------
+
+struct SpmvRowsGroup {
+    int32_t geo;          // nvec << 8 | lgL << 3 | lb: vectors per row, log2 lanes per row, log2 b
+    int32_t rows;         // rows of the group
+    int32_t first_row;    // storage index of the group's first row
+    int32_t blocks;       // workgroups that hold rows (blockIdx.x < blocks)
+    int64_t first_elem;   // slot of the group's first retained weight
+    int64_t first_word;   // packed offsets: the group's first 32-bit word
+};
+struct SpmvRowsArgs {
+    const void *values;
+    const void *offs;     // byte offsets or packed words
+    const void *x;
+    float *y;
+    const int32_t *perm;
+    const float *scales;  // INT8 weights only
+    int32_t N, pad[3];
+    SpmvRowsGroup g[kMaxBins];
+};
+static_assert(sizeof(SpmvRowsGroup) == 32, "group record is one 32-byte scalar load");
+static_assert(offsetof(SpmvRowsArgs, g) == 64, "header is one 64-byte scalar load");
+
+
+// s_waitcnt vmcnt(n): wait until at most n vector memory loads are outstanding
+__device__ __forceinline__ void wait_vmcnt_le(int n) {
+#define DARB_VMCNT(N)                                                                       \
+    case N:                                                                                 \
+        __builtin_amdgcn_s_waitcnt(0x0F70 | ((N) & 15) | ((((N) >> 4) & 3) << 14));         \
+        break;
+    switch (n) {
+        DARB_VMCNT(0) DARB_VMCNT(1) DARB_VMCNT(2) DARB_VMCNT(3) DARB_VMCNT(4) DARB_VMCNT(5)
+        DARB_VMCNT(6) DARB_VMCNT(7) DARB_VMCNT(8) DARB_VMCNT(9) DARB_VMCNT(10) DARB_VMCNT(11)
+        DARB_VMCNT(12) DARB_VMCNT(13) DARB_VMCNT(14) DARB_VMCNT(15) DARB_VMCNT(16)
+        DARB_VMCNT(17) DARB_VMCNT(18) DARB_VMCNT(19) DARB_VMCNT(20)
+        default: __builtin_amdgcn_s_waitcnt(0x0F70); break;       // vmcnt(0)
+    }
+#undef DARB_VMCNT
+}
+
+template <typename Tw, typename Tx, int KV, bool PK>
+__global__ __launch_bounds__(kSpmvThreads) void spmv_rows_kernel(SpmvRowsArgs args) {
+    using WV = WVec<Tw>;
+    constexpr int VEC = WV::VEC;
+    using OV = Off<PK, VEC>;
+    constexpr int XB = int(sizeof(Tx));                      // bytes per element of x
+    constexpr int LGXB = XB == 4 ? 2 : 1;
+    extern __shared__ float xs[];                             // x as stored (Tx), then a pad
+    (void)args;   // read below through the kernel-argument segment
+
+    typedef int i32x16 __attribute__((ext_vector_type(16)));
+    typedef int i32x8 __attribute__((ext_vector_type(8)));
+    i32x16 H;
+    i32x8 Gr;
+    {
+        const auto kp = __builtin_amdgcn_kernarg_segment_ptr();
+        const uint32_t goff = uint32_t(offsetof(SpmvRowsArgs, g)) +
+                              uint32_t(sizeof(SpmvRowsGroup)) * blockIdx.y;
+        asm volatile("s_load_dwordx16 %0, %2, 0x0\n\t"
+                     "s_load_dwordx8 %1, %2, %3\n\t"
+                     "s_waitcnt lgkmcnt(0)"
+                     : "=s"(H), "=s"(Gr) : "s"(kp), "s"(goff) : "memory");
+    }
+    // the pointers are global memory: built as global pointers so that every access
+    // through them is a global (not flat) instruction
+    typedef __attribute__((address_space(1))) char gchar;
+    auto ptr = [&](int i) -> void * {
+        return (void *)(gchar *)(uintptr_t((uint64_t(uint32_t(H[2 * i + 1])) << 32) |
+                                           uint32_t(H[2 * i])));
+    };
+    const Tw *values = static_cast<const Tw *>(ptr(0));
+    const void *offs = ptr(1);
+    const char *x = static_cast<const char *>(ptr(2));
+    float *y = static_cast<float *>(ptr(3));
+    const int32_t *perm = static_cast<const int32_t *>(ptr(4));
+    const float *scales = static_cast<const float *>(ptr(5));
+    const int N = H[12];
+    const int geo = Gr[0], rows = Gr[1], first_row = Gr[2], blocks = Gr[3];
+    const int64_t first_elem = int64_t((uint64_t(uint32_t(Gr[5])) << 32) | uint32_t(Gr[4]));
+    const int64_t first_word = int64_t((uint64_t(uint32_t(Gr[7])) << 32) | uint32_t(Gr[6]));
+    if (int(blockIdx.x) >= blocks) return;                   // uniform: a group with fewer rows
+
+    const int wave = wave_uniform(int(threadIdx.x) / kWave);
+    const int lane = int(threadIdx.x) & (kWave - 1);
+    const int lb = geo & 7, lgL = (geo >> 3) & 7, nvec = geo >> 8;
+    const int L = 1 << lgL;
+    const int row = ((int(blockIdx.x) * kSpmvWaves + wave) << (6 - lgL)) + (lane >> lgL);
+    const bool row_ok = row < rows;
+    const int row_c = row_ok ? row : rows - 1;
+    const int sub = lane & (L - 1);
+    const int32_t dest = perm[first_row + row_c];
+
+    // x into LDS as stored, by DMA in 1 KiB chunks (x is 16-byte aligned and a whole
+    // number of 16-byte vectors); the last chunk's lanes past x's end repeat x's last
+    // vector into the pad.  No LDS store follows, so nothing waits for all of it.
+    {
+        typedef __attribute__((address_space(1))) const char *gptr;
+        typedef __attribute__((address_space(3))) void *lptr;
+        const int nv16 = (N * XB) >> 4;
+        const int chunks = (nv16 + kWave - 1) / kWave;
+        for (int j = wave; j < chunks; j += kSpmvWaves) {
+            const int v = j * kWave + lane;
+            __builtin_amdgcn_global_load_lds((gptr)(x + (v < nv16 ? v : nv16 - 1) * 16),
+                                             (lptr)(reinterpret_cast<char *>(xs) + j * kWave * 16),
+                                             16, 0, 0);
+        }
+    }
+
+    const int n = (nvec + L - 1) >> lgL;                     // vectors per lane (uniform)
+    const int64_t j0 = int64_t(row_c) * (int64_t(nvec) * VEC);   // the row's first slot in its group
+    const typename WV::V *vrow =
+        reinterpret_cast<const typename WV::V *>(values + first_elem + j0);
+    GroupOffsets go;
+    go.u8 = static_cast<const uint8_t *>(offs) + first_elem;
+    go.pk = packed_group(static_cast<const uint32_t *>(offs), first_word, lb);
+    // vectors a lane loads: its n, or all KV when KV is small (a fixed count keeps the
+    // compiler from copying vectors between branches, which would wait on the loads)
+    constexpr bool kAll = KV <= 4;
+    const int nl = kAll ? KV : n;
+    typename WV::V wv[KV];
+    typename OV::Raw ov[KV];
+#pragma unroll
+    for (int k = 0; k < KV; ++k) {
+        if (kAll || k < n) {                                 // uniform
+            int vi = sub + k * L;
+            vi = vi < nvec ? vi : nvec - 1;
+            wv[k] = __builtin_nontemporal_load(vrow + vi);
+            ov[k] = OV::load(go, j0 + int64_t(vi) * VEC);
+        }
+    }
+    // INT8: the row's scale, once its index has arrived (the loads above are on their way)
+    float scale = 1.0f;
+    asm volatile("" ::: "memory");
+    if constexpr (kScaled<Tw>) scale = scales[dest];
+    // loads return in order: at most (vector loads + scale load) outstanding means this
+    // wave's x chunks have landed; every vector issues at least two loads
+    wait_vmcnt_le(2 * nl + (kScaled<Tw> ? 1 : 0));
+    asm volatile("s_barrier" ::: "memory");
+
+    const uint32_t sh = uint32_t(lb + LGXB);
+    const uint32_t base = uint32_t(sub * VEC) << sh;         // byte address of the lane's first block
+    const uint32_t stepk = uint32_t(L * VEC) << sh;
+    const uint32_t lastb = uint32_t((nvec - 1) * VEC) << sh;
+    float acc = 0.0f;
+#pragma unroll
+    for (int k = 0; k < KV; ++k) {
+        if (k < n) {
+            uint32_t bk = base + uint32_t(k) * stepk;
+            bk = bk < lastb ? bk : lastb;
+            const typename OV::Bits ob = OV::bits(ov[k], go);
+            float xv[VEC];
+#pragma unroll
+            for (int q = 0; q < VEC; ++q) {
+                const uint32_t ad = bk + (uint32_t(q) << sh) + (uint32_t(OV::field(ob, q, go)) << LGXB);
+                xv[q] = to_f32<Tx>(*reinterpret_cast<const Tx *>(reinterpret_cast<const char *>(xs) + ad));
+            }
+            if (sub + k * L < nvec) {
+#pragma unroll
+                for (int q = 0; q < VEC; ++q) acc = fmaf(WV::get(wv[k], q), xv[q], acc);
+            }
+        }
+    }
+    acc = group_sum(acc, lgL);
+    if (row_ok && sub == L - 1) y[dest] = kScaled<Tw> ? acc * scale : acc;
 }
 
 // ---------------------------------------------------------------------------------
@@ -957,6 +1141,72 @@ bool spmv_schedule(const darb_plan &p, const void *values, const uint8_t *offset
     return true;
 }
 
+// The one-pass kernel when it applies: x is 16-byte aligned, a whole number of
+// 16-byte vectors and fits in 64 KiB of LDS with its pad, every group takes the
+// vector path, and the workgroups fit on the chip at once.  Returns false (nothing
+// launched) otherwise.
+template <typename Tw, typename Tx, bool PK>
+bool launch_spmv_rows(const darb_plan &p, const ProductSchedule &s0, const void *values,
+                      const uint8_t *offsets, const void *offs, const void *x, float *y,
+                      const float *scales, int64_t resident, hipStream_t st, hipError_t *err) {
+    constexpr int VEC = WVec<Tw>::VEC;
+    // vectors per lane: 8 of 4 weights, or 4 of 8 (fp16 and INT8 weights)
+    constexpr int KVMAX = VEC == 4 ? kVmax : kVmax / 2;
+    if (p.N > kLdsMaxFloats || p.M >= (int64_t(1) << 31)) return false;
+    if (reinterpret_cast<uintptr_t>(x) % 16 != 0 || (p.N * int64_t(sizeof(Tx))) % 16 != 0)
+        return false;
+    ProductSchedule s = s0;
+    {
+        int vmax = KVMAX;     // the CU-filling rule of the caller, capped at KVMAX
+        for (;; vmax /= 2) {
+            if (!spmv_schedule<Tw>(p, values, offsets, s, vmax)) return false;
+            if (vmax <= 2 || s.block_begin[s.nbins] >= (p.cus > 0 ? p.cus : 256)) break;
+        }
+    }
+    SpmvRowsArgs a{};
+    a.values = values;
+    a.offs = offs;
+    a.x = x;
+    a.y = y;
+    a.perm = p.d_perm;
+    a.scales = scales;
+    a.N = int32_t(p.N);
+    int max_blocks = 0, kv = 0;
+    int64_t total = 0;
+    for (int g = 0; g < p.bins.nbins; ++g) {
+        if (s.vec[g] != VEC) return false;
+        const int64_t nvec = p.bins.nblk[g] / VEC;
+        const int lgL = s.log2_lanes[g];
+        const int64_t rows_per_wave = int64_t(kWave) >> lgL;
+        const int64_t blocks =
+            ((p.bins.rows[g] + rows_per_wave - 1) / rows_per_wave + kSpmvWaves - 1) / kSpmvWaves;
+        const int64_t n = (nvec + (int64_t(1) << lgL) - 1) >> lgL;
+        if (nvec >= (int64_t(1) << 23) || n > KVMAX || blocks > 0x7FFFFFFF) return false;
+        a.g[g].geo = int32_t((nvec << 8) | (lgL << 3) | p.bins.log2b[g]);
+        a.g[g].rows = int32_t(p.bins.rows[g]);
+        a.g[g].first_row = int32_t(p.bins.first_row[g]);
+        a.g[g].blocks = int32_t(blocks);
+        a.g[g].first_elem = p.bins.first_elem[g];
+        a.g[g].first_word = p.bins.first_word[g];
+        max_blocks = blocks > max_blocks ? int(blocks) : max_blocks;
+        kv = n > kv ? int(n) : kv;
+        total += blocks;
+    }
+    if (total > resident || max_blocks == 0) return false;
+    // x rounded up to whole 1 KiB DMA chunks, then 1 KiB more: a gather at any offset
+    // byte (c < N + 256) stays inside the allocation
+    const size_t lds = ((size_t(p.N) * sizeof(Tx) + 1023) & ~size_t(1023)) + 1024;
+    if (lds > 65536) return false;
+    const dim3 grid(unsigned(max_blocks), unsigned(p.bins.nbins));
+    if (kv <= 4 || KVMAX == 4)
+        hipLaunchKernelGGL((spmv_rows_kernel<Tw, Tx, 4, PK>), grid, dim3(kSpmvThreads), lds, st, a);
+    else
+        hipLaunchKernelGGL((spmv_rows_kernel<Tw, Tx, KVMAX, PK>), grid, dim3(kSpmvThreads), lds, st,
+                           a);
+    *err = hipGetLastError();
+    return true;
+}
+
 template <typename Tw, typename Tx, bool PK>
 hipError_t launch_spmv_t(const darb_plan &p, const void *values, const uint8_t *offsets,
                          const uint32_t *packed, const void *x, float *y, const float *scales,
@@ -983,6 +1233,12 @@ hipError_t launch_spmv_t(const darb_plan &p, const void *values, const uint8_t *
     int64_t per_cu = lds_per_group > 0 ? kLdsPerCu / lds_per_group : 8;
     per_cu = per_cu < 1 ? 1 : (per_cu > 8 ? 8 : per_cu);
     const int64_t resident = int64_t(p.cus > 0 ? p.cus : 256) * per_cu;
+    {
+        hipError_t err = hipSuccess;
+        if (launch_spmv_rows<Tw, Tx, PK>(p, s, values, offsets, offs, x, y, scales, resident, st,
+                                         &err))
+            return err;
+    }
     // more blocks than fit at once: the looping form, scheduled for its registers
     if (blocks > resident && !spmv_schedule<Tw>(p, values, offsets, s, kLoopVmax))
         return hipErrorInvalidConfiguration;
