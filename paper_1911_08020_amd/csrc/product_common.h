@@ -162,6 +162,10 @@ template <int NV> struct Off<false, NV> {
         if constexpr (NV <= 4) return int((uint32_t(b) >> (8 * q)) & 0xFFu);
         else return int((b[q >> 2] >> (8 * (q & 3))) & 0xFFu);
     }
+    // the same with q a compile-time index (the block size is implied by the byte)
+    template <int LB> __device__ static int field_c(const Bits &b, int q) {
+        return field(b, q, GroupOffsets{});
+    }
 };
 
 // packed, up to 4 indices (<= 28 bits): two words
@@ -174,6 +178,9 @@ template <int NV> struct Off<true, NV> {
     __device__ static int field(Bits b, int q, const GroupOffsets &go) {
         return packed_field(b, q, go.pk);
     }
+    template <int LB> __device__ static int field_c(Bits b, int q) {
+        return int((b >> (q * LB)) & ((1u << LB) - 1u));
+    }
 };
 
 // packed, 8 indices (<= 56 bits): three words
@@ -184,6 +191,9 @@ template <> struct Off<true, 8> {
     __device__ static Bits bits(const Raw &r, const GroupOffsets &) { return packed_bits64(r); }
     __device__ static int field(Bits b, int q, const GroupOffsets &go) {
         return packed_field(b, q, go.pk);
+    }
+    template <int LB> __device__ static int field_c(Bits b, int q) {
+        return int(uint32_t(b >> (q * LB)) & ((1u << LB) - 1u));
     }
 };
 
@@ -460,14 +470,19 @@ __global__ __launch_bounds__(kSpmvThreads) void spmv_kernel(
 }
 
 // ---------------------------------------------------------------------------------
-// SpMV in one pass of workgroups: workgroup (bx, g) takes four waves' tiles of rows
-// of group g (blockIdx.y = g), so a wave's geometry needs no search.  Every input
-// of the launch arrives with one round of scalar loads (the 64-byte header and the
-// group's 32-byte record), issued by hand: a workgroup's first vector load waits on
-// that round only.  Each wave loads its output row's index, then its share of x
-// into LDS, then all its vectors; before the barrier it waits only until its share
-// of x has landed (the vector loads return in order after it), so no wave waits for
-// another wave's format data.
+// SpMV by row blocks: a block is four waves' tiles of rows of one group; workgroup
+// (bx, g) takes blocks bx, bx + stride_g, ... of group g (blockIdx.y = g), so a
+// wave's geometry needs no search.  Every input of the launch arrives with one round
+// of scalar loads (the 64-byte header, the group's stride and its 32-byte record),
+// issued by hand: a workgroup's first vector load waits on that round only.  Each
+// wave loads its output row's index, then its share of x into LDS, then all its
+// vectors; before the barrier it waits only until its share of x has landed (the
+// vector loads return in order after it), so no wave waits for another wave's format
+// data.  With one block per workgroup (LOOP false) the launch is one pass; with
+// LOOP, workgroups stay resident, x is staged once, and each wave goes through its
+// blocks load, wait, sum: the other waves of the CU hide its latency, and the next
+// block's row index is loaded a block ahead so that the INT8 scale load never waits
+// on a dependent round trip.
 // ---------------------------------------------------------------------------------
 
 struct SpmvRowsGroup {
@@ -486,10 +501,12 @@ struct SpmvRowsArgs {
     const int32_t *perm;
     const float *scales;  // INT8 weights only
     int32_t N, pad[3];
+    int32_t stride[kMaxBins];   // workgroups of group g: each takes blocks bx, bx + stride, ...
     SpmvRowsGroup g[kMaxBins];
 };
 static_assert(sizeof(SpmvRowsGroup) == 32, "group record is one 32-byte scalar load");
-static_assert(offsetof(SpmvRowsArgs, g) == 64, "header is one 64-byte scalar load");
+static_assert(offsetof(SpmvRowsArgs, stride) == 64, "header is one 64-byte scalar load");
+static_assert(offsetof(SpmvRowsArgs, g) == 96, "group records follow the strides");
 
 
 // s_waitcnt vmcnt(n): wait until at most n vector memory loads are outstanding
@@ -508,8 +525,8 @@ __device__ __forceinline__ void wait_vmcnt_le(int n) {
 #undef DARB_VMCNT
 }
 
-template <typename Tw, typename Tx, int KV, bool PK>
-__global__ __launch_bounds__(kSpmvThreads) void spmv_rows_kernel(SpmvRowsArgs args) {
+template <typename Tw, typename Tx, int KV, bool PK, bool LOOP>
+__global__ __launch_bounds__(kSpmvThreads, 4) void spmv_rows_kernel(SpmvRowsArgs args) {
     using WV = WVec<Tw>;
     constexpr int VEC = WV::VEC;
     using OV = Off<PK, VEC>;
@@ -522,14 +539,17 @@ __global__ __launch_bounds__(kSpmvThreads) void spmv_rows_kernel(SpmvRowsArgs ar
     typedef int i32x8 __attribute__((ext_vector_type(8)));
     i32x16 H;
     i32x8 Gr;
+    int stride;
     {
         const auto kp = __builtin_amdgcn_kernarg_segment_ptr();
         const uint32_t goff = uint32_t(offsetof(SpmvRowsArgs, g)) +
                               uint32_t(sizeof(SpmvRowsGroup)) * blockIdx.y;
-        asm volatile("s_load_dwordx16 %0, %2, 0x0\n\t"
-                     "s_load_dwordx8 %1, %2, %3\n\t"
+        const uint32_t soff = uint32_t(offsetof(SpmvRowsArgs, stride)) + 4u * blockIdx.y;
+        asm volatile("s_load_dwordx16 %0, %3, 0x0\n\t"
+                     "s_load_dwordx8 %1, %3, %4\n\t"
+                     "s_load_dword %2, %3, %5\n\t"
                      "s_waitcnt lgkmcnt(0)"
-                     : "=s"(H), "=s"(Gr) : "s"(kp), "s"(goff) : "memory");
+                     : "=s"(H), "=s"(Gr), "=s"(stride) : "s"(kp), "s"(goff), "s"(soff) : "memory");
     }
     // the pointers are global memory: built as global pointers so that every access
     // through them is a global (not flat) instruction
@@ -548,17 +568,25 @@ __global__ __launch_bounds__(kSpmvThreads) void spmv_rows_kernel(SpmvRowsArgs ar
     const int geo = Gr[0], rows = Gr[1], first_row = Gr[2], blocks = Gr[3];
     const int64_t first_elem = int64_t((uint64_t(uint32_t(Gr[5])) << 32) | uint32_t(Gr[4]));
     const int64_t first_word = int64_t((uint64_t(uint32_t(Gr[7])) << 32) | uint32_t(Gr[6]));
-    if (int(blockIdx.x) >= blocks) return;                   // uniform: a group with fewer rows
+    // uniform: a group with fewer blocks, or fewer resident workgroups, than the grid row
+    if (int(blockIdx.x) >= blocks || int(blockIdx.x) >= stride) return;
 
     const int wave = wave_uniform(int(threadIdx.x) / kWave);
     const int lane = int(threadIdx.x) & (kWave - 1);
     const int lb = geo & 7, lgL = (geo >> 3) & 7, nvec = geo >> 8;
     const int L = 1 << lgL;
-    const int row = ((int(blockIdx.x) * kSpmvWaves + wave) << (6 - lgL)) + (lane >> lgL);
-    const bool row_ok = row < rows;
-    const int row_c = row_ok ? row : rows - 1;
     const int sub = lane & (L - 1);
-    const int32_t dest = perm[first_row + row_c];
+    const int n = (nvec + L - 1) >> lgL;                     // vectors per lane (uniform)
+    // the lane's row in block blk (clamped into the group) and whether it exists
+    auto row_of = [&](int blk, bool &ok) {
+        const int row = ((blk * kSpmvWaves + wave) << (6 - lgL)) + (lane >> lgL);
+        ok = row < rows;
+        return ok ? row : rows - 1;
+    };
+    int blk = int(blockIdx.x);
+    bool row_ok;
+    int row_c = row_of(blk, row_ok);
+    int32_t dest = perm[first_row + row_c];
 
     // x into LDS as stored, by DMA in 1 KiB chunks (x is 16-byte aligned and a whole
     // number of 16-byte vectors); the last chunk's lanes past x's end repeat x's last
@@ -576,10 +604,6 @@ __global__ __launch_bounds__(kSpmvThreads) void spmv_rows_kernel(SpmvRowsArgs ar
         }
     }
 
-    const int n = (nvec + L - 1) >> lgL;                     // vectors per lane (uniform)
-    const int64_t j0 = int64_t(row_c) * (int64_t(nvec) * VEC);   // the row's first slot in its group
-    const typename WV::V *vrow =
-        reinterpret_cast<const typename WV::V *>(values + first_elem + j0);
     GroupOffsets go;
     go.u8 = static_cast<const uint8_t *>(offs) + first_elem;
     go.pk = packed_group(static_cast<const uint32_t *>(offs), first_word, lb);
@@ -589,15 +613,57 @@ __global__ __launch_bounds__(kSpmvThreads) void spmv_rows_kernel(SpmvRowsArgs ar
     const int nl = kAll ? KV : n;
     typename WV::V wv[KV];
     typename OV::Raw ov[KV];
+    auto load_block = [&](int rc) {
+        const int64_t j0 = int64_t(rc) * (int64_t(nvec) * VEC);   // the row's first slot in its group
+        const typename WV::V *vrow =
+            reinterpret_cast<const typename WV::V *>(values + first_elem + j0);
 #pragma unroll
-    for (int k = 0; k < KV; ++k) {
-        if (kAll || k < n) {                                 // uniform
-            int vi = sub + k * L;
-            vi = vi < nvec ? vi : nvec - 1;
-            wv[k] = __builtin_nontemporal_load(vrow + vi);
-            ov[k] = OV::load(go, j0 + int64_t(vi) * VEC);
+        for (int k = 0; k < KV; ++k) {
+            if (kAll || k < n) {                             // uniform
+                // keeps the loads inside the branch: issued unconditionally they would
+                // cost load slots for nothing
+                if constexpr (!kAll) asm volatile("" ::: "memory");
+                int vi = sub + k * L;
+                vi = vi < nvec ? vi : nvec - 1;
+                wv[k] = __builtin_nontemporal_load(vrow + vi);
+                ov[k] = OV::load(go, j0 + int64_t(vi) * VEC);
+            }
         }
-    }
+    };
+    // the sums of one block: block size b = 2^LB fixed at compile time, so each
+    // gather's in-block position is an immediate of its LDS load and an offset costs one
+    // extract and one add
+    auto sum_block = [&](float scale, bool ok, int32_t d, auto lbc) {
+        constexpr int LB = decltype(lbc)::value;
+        constexpr uint32_t sh = uint32_t(LB + LGXB);
+        const uint32_t base = uint32_t(sub * VEC) << sh;     // byte address of the lane's first block
+        const uint32_t stepk = uint32_t(L * VEC) << sh;
+        const uint32_t lastb = uint32_t((nvec - 1) * VEC) << sh;
+        float acc = 0.0f;
+#pragma unroll
+        for (int k = 0; k < KV; ++k) {
+            if (k < n) {
+                uint32_t bk = base + uint32_t(k) * stepk;
+                bk = bk < lastb ? bk : lastb;
+                const typename OV::Bits ob = OV::bits(ov[k], go);
+                float xv[VEC];
+#pragma unroll
+                for (int q = 0; q < VEC; ++q) {
+                    const uint32_t ad = bk + (uint32_t(OV::template field_c<LB>(ob, q)) << LGXB);
+                    xv[q] = to_f32<Tx>(*reinterpret_cast<const Tx *>(
+                        reinterpret_cast<const char *>(xs) + ad + (uint32_t(q) << sh)));
+                }
+                if (sub + k * L < nvec) {
+#pragma unroll
+                    for (int q = 0; q < VEC; ++q) acc = fmaf(WV::get(wv[k], q), xv[q], acc);
+                }
+            }
+        }
+        acc = group_sum(acc, lgL);
+        if (ok && sub == L - 1) y[d] = kScaled<Tw> ? acc * scale : acc;
+    };
+
+    load_block(row_c);
     // INT8: the row's scale, once its index has arrived (the loads above are on their way)
     float scale = 1.0f;
     asm volatile("" ::: "memory");
@@ -606,32 +672,40 @@ __global__ __launch_bounds__(kSpmvThreads) void spmv_rows_kernel(SpmvRowsArgs ar
     // wave's x chunks have landed; every vector issues at least two loads
     wait_vmcnt_le(2 * nl + (kScaled<Tw> ? 1 : 0));
     asm volatile("s_barrier" ::: "memory");
-
-    const uint32_t sh = uint32_t(lb + LGXB);
-    const uint32_t base = uint32_t(sub * VEC) << sh;         // byte address of the lane's first block
-    const uint32_t stepk = uint32_t(L * VEC) << sh;
-    const uint32_t lastb = uint32_t((nvec - 1) * VEC) << sh;
-    float acc = 0.0f;
-#pragma unroll
-    for (int k = 0; k < KV; ++k) {
-        if (k < n) {
-            uint32_t bk = base + uint32_t(k) * stepk;
-            bk = bk < lastb ? bk : lastb;
-            const typename OV::Bits ob = OV::bits(ov[k], go);
-            float xv[VEC];
-#pragma unroll
-            for (int q = 0; q < VEC; ++q) {
-                const uint32_t ad = bk + (uint32_t(q) << sh) + (uint32_t(OV::field(ob, q, go)) << LGXB);
-                xv[q] = to_f32<Tx>(*reinterpret_cast<const Tx *>(reinterpret_cast<const char *>(xs) + ad));
+    auto sum_any = [&](float sc, bool ok, int32_t d) {
+        switch (lb) {                                        // uniform
+            case 0: sum_block(sc, ok, d, std::integral_constant<int, 0>{}); break;
+            case 1: sum_block(sc, ok, d, std::integral_constant<int, 1>{}); break;
+            case 2: sum_block(sc, ok, d, std::integral_constant<int, 2>{}); break;
+            case 3: sum_block(sc, ok, d, std::integral_constant<int, 3>{}); break;
+            case 4: sum_block(sc, ok, d, std::integral_constant<int, 4>{}); break;
+            case 5: sum_block(sc, ok, d, std::integral_constant<int, 5>{}); break;
+            case 6: sum_block(sc, ok, d, std::integral_constant<int, 6>{}); break;
+            default: sum_block(sc, ok, d, std::integral_constant<int, 7>{}); break;
+        }
+    };
+    if constexpr (!LOOP) {
+        sum_any(scale, row_ok, dest);
+    } else {
+        for (;;) {
+            const int nxt = blk + stride;
+            const bool more = nxt < blocks;                  // uniform
+            bool nok = false;
+            int nrc = 0;
+            int32_t ndest = 0;
+            if (more) {
+                nrc = row_of(nxt, nok);
+                ndest = perm[first_row + nrc];               // one block ahead
             }
-            if (sub + k * L < nvec) {
-#pragma unroll
-                for (int q = 0; q < VEC; ++q) acc = fmaf(WV::get(wv[k], q), xv[q], acc);
-            }
+            sum_any(scale, row_ok, dest);
+            if (!more) break;
+            blk = nxt;
+            row_ok = nok;
+            dest = ndest;
+            load_block(nrc);
+            if constexpr (kScaled<Tw>) scale = scales[dest];
         }
     }
-    acc = group_sum(acc, lgL);
-    if (row_ok && sub == L - 1) y[dest] = kScaled<Tw> ? acc * scale : acc;
 }
 
 // ---------------------------------------------------------------------------------
@@ -1141,27 +1215,34 @@ bool spmv_schedule(const darb_plan &p, const void *values, const uint8_t *offset
     return true;
 }
 
-// The one-pass kernel when it applies: x is 16-byte aligned, a whole number of
-// 16-byte vectors and fits in 64 KiB of LDS with its pad, every group takes the
-// vector path, and the workgroups fit on the chip at once.  Returns false (nothing
-// launched) otherwise.
+// The row-block kernel when it applies: x is 16-byte aligned, a whole number of
+// 16-byte vectors and fits in 64 KiB of LDS with its pad, and every group takes the
+// vector path.  Blocks that fit on the chip at once run in one pass; more blocks run
+// on resident workgroups, each group getting a share of them in proportion to its
+// blocks.  Returns false (nothing launched) otherwise.
 template <typename Tw, typename Tx, bool PK>
-bool launch_spmv_rows(const darb_plan &p, const ProductSchedule &s0, const void *values,
-                      const uint8_t *offsets, const void *offs, const void *x, float *y,
-                      const float *scales, int64_t resident, hipStream_t st, hipError_t *err) {
+bool launch_spmv_rows(const darb_plan &p, const void *values, const uint8_t *offsets,
+                      const void *offs, const void *x, float *y, const float *scales,
+                      hipStream_t st, hipError_t *err) {
     constexpr int VEC = WVec<Tw>::VEC;
-    // vectors per lane: 8 of 4 weights, or 4 of 8 (fp16 and INT8 weights)
-    constexpr int KVMAX = VEC == 4 ? kVmax : kVmax / 2;
+    // vectors per lane: up to 8 (of 4 or 8 weights)
+    constexpr int KVMAX = kVmax;
     if (p.N > kLdsMaxFloats || p.M >= (int64_t(1) << 31)) return false;
     if (reinterpret_cast<uintptr_t>(x) % 16 != 0 || (p.N * int64_t(sizeof(Tx))) % 16 != 0)
         return false;
-    ProductSchedule s = s0;
-    {
-        int vmax = KVMAX;     // the CU-filling rule of the caller, capped at KVMAX
-        for (;; vmax /= 2) {
-            if (!spmv_schedule<Tw>(p, values, offsets, s, vmax)) return false;
-            if (vmax <= 2 || s.block_begin[s.nbins] >= (p.cus > 0 ? p.cus : 256)) break;
-        }
+    // x rounded up to whole 1 KiB DMA chunks, then 1 KiB more: a gather at any offset
+    // byte (c < N + 256) stays inside the allocation
+    const size_t lds = ((size_t(p.N) * sizeof(Tx) + 1023) & ~size_t(1023)) + 1024;
+    if (lds > 65536) return false;
+    const int64_t cus = p.cus > 0 ? p.cus : 256;
+    int64_t per_cu = kLdsPerCu / int64_t(lds);
+    per_cu = per_cu > 8 ? 8 : per_cu;
+    const int64_t resident = cus * per_cu;
+    ProductSchedule s;
+    for (int vmax = KVMAX;; vmax /= 2) {
+        // a launch with fewer blocks than CUs spreads rows over more lanes
+        if (!spmv_schedule<Tw>(p, values, offsets, s, vmax)) return false;
+        if (vmax <= 2 || s.block_begin[s.nbins] >= cus) break;
     }
     SpmvRowsArgs a{};
     a.values = values;
@@ -1171,38 +1252,53 @@ bool launch_spmv_rows(const darb_plan &p, const ProductSchedule &s0, const void 
     a.perm = p.d_perm;
     a.scales = scales;
     a.N = int32_t(p.N);
-    int max_blocks = 0, kv = 0;
-    int64_t total = 0;
+    int kv = 0;
+    int64_t total = 0, blocks[kMaxBins] = {};
     for (int g = 0; g < p.bins.nbins; ++g) {
         if (s.vec[g] != VEC) return false;
         const int64_t nvec = p.bins.nblk[g] / VEC;
         const int lgL = s.log2_lanes[g];
         const int64_t rows_per_wave = int64_t(kWave) >> lgL;
-        const int64_t blocks =
+        blocks[g] =
             ((p.bins.rows[g] + rows_per_wave - 1) / rows_per_wave + kSpmvWaves - 1) / kSpmvWaves;
         const int64_t n = (nvec + (int64_t(1) << lgL) - 1) >> lgL;
-        if (nvec >= (int64_t(1) << 23) || n > KVMAX || blocks > 0x7FFFFFFF) return false;
+        if (nvec >= (int64_t(1) << 23) || n > KVMAX || blocks[g] > 0x7FFFFFFF) return false;
         a.g[g].geo = int32_t((nvec << 8) | (lgL << 3) | p.bins.log2b[g]);
         a.g[g].rows = int32_t(p.bins.rows[g]);
         a.g[g].first_row = int32_t(p.bins.first_row[g]);
-        a.g[g].blocks = int32_t(blocks);
+        a.g[g].blocks = int32_t(blocks[g]);
         a.g[g].first_elem = p.bins.first_elem[g];
         a.g[g].first_word = p.bins.first_word[g];
-        max_blocks = blocks > max_blocks ? int(blocks) : max_blocks;
         kv = n > kv ? int(n) : kv;
-        total += blocks;
+        total += blocks[g];
     }
-    if (total > resident || max_blocks == 0) return false;
-    // x rounded up to whole 1 KiB DMA chunks, then 1 KiB more: a gather at any offset
-    // byte (c < N + 256) stays inside the allocation
-    const size_t lds = ((size_t(p.N) * sizeof(Tx) + 1023) & ~size_t(1023)) + 1024;
-    if (lds > 65536) return false;
-    const dim3 grid(unsigned(max_blocks), unsigned(p.bins.nbins));
-    if (kv <= 4 || KVMAX == 4)
-        hipLaunchKernelGGL((spmv_rows_kernel<Tw, Tx, 4, PK>), grid, dim3(kSpmvThreads), lds, st, a);
-    else
-        hipLaunchKernelGGL((spmv_rows_kernel<Tw, Tx, KVMAX, PK>), grid, dim3(kSpmvThreads), lds, st,
-                           a);
+    if (total == 0) return false;
+    const bool loop = total > resident;
+    int max_stride = 0;
+    for (int g = 0; g < p.bins.nbins; ++g) {
+        // resident workgroups in proportion to the group's blocks (at least one)
+        int64_t sg = loop ? (blocks[g] * resident) / total : blocks[g];
+        sg = sg < 1 ? 1 : (sg > blocks[g] ? blocks[g] : sg);
+        a.stride[g] = int32_t(sg);
+        max_stride = sg > max_stride ? int(sg) : max_stride;
+    }
+    const dim3 grid(unsigned(max_stride), unsigned(p.bins.nbins));
+    // the kernel's unrolled vector count: the smallest of 4, 6, 8 that holds every lane's
+    // vectors (fewer unrolled steps, fewer uniform branches)
+#define DARB_ROWS(KV, L)                                                                    \
+    hipLaunchKernelGGL((spmv_rows_kernel<Tw, Tx, KV, PK, L>), grid, dim3(kSpmvThreads), lds, st, a)
+    constexpr int KV6 = KVMAX > 6 ? 6 : KVMAX;
+    if (kv <= 4 || KVMAX == 4) {
+        if (loop) DARB_ROWS(4, true);
+        else DARB_ROWS(4, false);
+    } else if (kv <= 6) {
+        if (loop) DARB_ROWS(KV6, true);
+        else DARB_ROWS(KV6, false);
+    } else {
+        if (loop) DARB_ROWS(KVMAX, true);
+        else DARB_ROWS(KVMAX, false);
+    }
+#undef DARB_ROWS
     *err = hipGetLastError();
     return true;
 }
@@ -1215,6 +1311,13 @@ hipError_t launch_spmv_t(const darb_plan &p, const void *values, const uint8_t *
     // units leaves CUs idle while each lane waits on a long run of loads: then rows
     // spread over more lanes (4, then 2 vectors per lane).  INT8 and fp16 vectors hold
     // 8 weights, so their small matrices need this most.
+    {
+        const void *offs0 = offset_source(p, offsets, packed);
+        hipError_t err = hipSuccess;
+        if (launch_spmv_rows<Tw, Tx, PK>(p, values, offsets, offs0, x, y, scales, st, &err))
+            return err;
+    }
+    // otherwise (x past LDS, misaligned or scalar-path groups) the general kernel
     ProductSchedule s;
     const int64_t cus = p.cus > 0 ? p.cus : 256;
     for (int vmax = kVmax;; vmax /= 2) {
@@ -1233,12 +1336,7 @@ hipError_t launch_spmv_t(const darb_plan &p, const void *values, const uint8_t *
     int64_t per_cu = lds_per_group > 0 ? kLdsPerCu / lds_per_group : 8;
     per_cu = per_cu < 1 ? 1 : (per_cu > 8 ? 8 : per_cu);
     const int64_t resident = int64_t(p.cus > 0 ? p.cus : 256) * per_cu;
-    {
-        hipError_t err = hipSuccess;
-        if (launch_spmv_rows<Tw, Tx, PK>(p, s, values, offsets, offs, x, y, scales, resident, st,
-                                         &err))
-            return err;
-    }
+
     // more blocks than fit at once: the looping form, scheduled for its registers
     if (blocks > resident && !spmv_schedule<Tw>(p, values, offsets, s, kLoopVmax))
         return hipErrorInvalidConfiguration;

@@ -424,3 +424,31 @@ def test_spmv_workgroups_take_several_blocks(darb):
     y8 = host(plan.spmv_i8(dev(q), dev(s), dev(x), packed=packed))
     compare(y8, oracle.spmm_i8(q, s, offs, lay, x), oracle.spmm_i8_absdot(q, s, offs, lay, x),
             1e-5, "looping spmv INT8")
+
+
+@pytest.mark.parametrize("wdtype", [np.float32, np.float16])
+def test_spmv_row_blocks_on_resident_workgroups(darb, wdtype):
+    # 4800 rows of 15 360 columns at b = 8, 16, 32: x takes 61 KiB of LDS, so two
+    # workgroups fit per CU (512 on 256 CUs) against about 700 row blocks of four
+    # waves; the row-block kernel then keeps its workgroups resident and each goes
+    # through several blocks of its group, the next block's row index loaded a block
+    # ahead.  fp32 and fp16 weights with fp32 x; byte, packed and INT8 forms.
+    say(f"spmv row blocks on resident workgroups, {np.dtype(wdtype).name} weights")
+    rng = np.random.default_rng(78)
+    M, N = 4800, 15360
+    W = rng.standard_normal((M, N)).astype(wdtype)
+    d = 1.0 / rng.choice([8, 16, 32], size=M)
+    plan, lay, vals, offs = encode_both(darb, W, d, 0.1, 0, 8, 32)
+    assert set(np.unique(lay.log2b).tolist()) == {3, 4, 5}
+    x = rng.standard_normal(N).astype(np.float32)
+    vd, od, xd = dev(vals), dev(offs), dev(x)
+    y = host(plan.spmv(vd, od, xd))
+    check_product(y, vals, offs, lay, x, wdtype, "row blocks spmv")
+    packed = plan.pack_offsets(od)
+    yp = host(plan.spmv_packed(vd, packed, xd))
+    assert np.array_equal(y.view(np.uint32), yp.view(np.uint32))
+    q, s = oracle.quantize_i8(vals, lay)
+    for label, kw in (("byte", dict(offsets=od)), ("packed", dict(packed=packed))):
+        y8 = host(plan.spmv_i8(dev(q), dev(s), xd, **kw))
+        compare(y8, oracle.spmm_i8(q, s, offs, lay, x), oracle.spmm_i8_absdot(q, s, offs, lay, x),
+                1e-5, f"row blocks spmv INT8 {label}")
