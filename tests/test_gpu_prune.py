@@ -183,7 +183,8 @@ def test_fp16_sampled_bracket(darb, kind):
     # 64 MiB of fp16 takes the sample and split path (8-bit first digit): normal
     # values kept at 0.5 % give a one-digit bracket with room for its keys; 61
     # distinct magnitudes kept at 5 % put 1.6 % of W in the threshold's digit, more
-    # than half the room, so the full first-digit histogram runs before the split
+    # than half the room, so the split pass takes the exact first digit of W instead
+    # and the later passes stream W
     rng = np.random.default_rng(8)
     M, N = 512, 65536
     if kind == "normal":
@@ -198,8 +199,9 @@ def test_fp16_sampled_bracket(darb, kind):
 
 def test_biased_sample_falls_back_to_w(darb):
     # from 64 MiB the first digit's candidates come from a bracket proposed by a
-    # sample of W (ranges at a fixed stride) and checked against the full
-    # histogram of the split pass.  Rows exactly one sample stride long put every
+    # sample of W (ranges at a fixed stride); the split pass counts the keys above
+    # the bracket, and the threshold must lie between that count and it plus the
+    # candidates.  Rows exactly one sample stride long put every
     # sampled range at the same columns (the first 1024, with the library's present
     # sample); values spread over 20 octaves only there make the sample propose a
     # narrow bracket near the top while the true threshold lies in the rest of W,
