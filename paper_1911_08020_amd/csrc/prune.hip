@@ -61,24 +61,43 @@ constexpr int kMaxDigitBits = 11;
 constexpr int kCopies = 4;                          // LDS histogram copies per workgroup
 constexpr int kMaxHistGroups = 256;                 // one 1024-thread workgroup per CU
 
-// Radix-select state, in the workspace.  The keys a pass looks at are taken
+// Radix-select state, in two slots of the workspace: each kernel reads one and
+// its first workgroup writes the other, which the next kernel reads (a kernel never
+// writes the slot its own workgroups read).  The keys a pass looks at are taken
 // relative to `base` (0, or the bracket's lowest key when the candidates hold the
-// threshold): rel = key - base; the digits chosen so far are rel >> hi.
+// threshold): rel = key - base; the digits chosen so far are rel >> hi.  A pass
+// leaves its digit's histogram in its own totals buffer, and the kernel after it
+// picks the digit (every workgroup of it, the same way) before its own work: no
+// workgroup waits for the others to finish, and no read-modify-write reads the
+// totals back.
 struct PruneState {
     uint32_t prefix;        // the digits chosen so far; with hi = 0, the threshold's rel
     uint32_t hi;            // low bits of rel still to choose (0: the threshold is known)
     uint32_t base;          // subtracted from every key
     uint32_t from_cand;     // every key that matches the prefix is among the candidates
-    uint32_t overflow;      // some workgroup's candidates did not fit
-    uint32_t done;          // workgroups finished in the running pass (0 between passes)
-    uint32_t single;        // the split pass keeps the sample's bracket
-    uint32_t dlo, dhi;      // first digits the split pass keeps as candidates
-    uint32_t pad;
     int64_t k_rem;          // keys still to take at or below the prefix
-    unsigned long long n_cand;   // candidates stored
-    unsigned long long n_above;  // keys whose first digit is above the bracket
     unsigned long long n_last;   // keys matching the prefix after the latest digit
+    uint32_t pend_width;    // > 0: the next pend_width bits' histogram is pending,
+    uint32_t pend_buf;      //      in totals buffer pend_buf
 };
+
+// What the split pass leaves for the passes after it (atomics, or its first
+// workgroup), and the count's last-workgroup counter.
+struct SplitInfo {
+    uint32_t overflow;      // some workgroup's candidates did not fit
+    uint32_t single;        // the split pass kept the sample's bracket
+    uint32_t dlo, dhi;      // the bracket of fine first digits
+    unsigned long long n_cand;   // candidates stored (reserved)
+    unsigned long long n_above;  // keys whose first digit is above the bracket
+    uint32_t done;          // workgroups of the count finished
+    uint32_t pad[3];
+};
+
+// Totals buffers, one per histogram of a call: the sample's coarse digit, the
+// split pass's first digit (when it takes one), then one per pass after it.
+constexpr int kDigitBins = 1 << kMaxDigitBits;
+constexpr int kTotalsBuffers = 5;
+constexpr int kBufSample = 0, kBufSplit = 1, kBufPass0 = 2;
 
 // What one histogram pass selects: the keys with (key - base) >> hi == prefix,
 // by their next digit, for the k_rem-th largest; from the candidates or from W.
@@ -86,6 +105,7 @@ struct Pass {
     uint32_t prefix, hi, base;
     bool cand;
     int64_t k_rem;
+    unsigned long long n_last;
 };
 
 // Width of the next digit when `hi` bits remain: at most kMaxDigitBits, and two
@@ -241,102 +261,113 @@ __device__ __forceinline__ uint64_t block_inclusive_scan(uint64_t v, uint64_t *w
     return v + before;
 }
 
-// Called by every thread of a workgroup after its global atomics, in the first
-// `active` workgroups of the grid (the others take no part in the pass): true in
-// the one workgroup that finishes the pass last, which also clears the counter for
-// the next pass.  Every value that crosses workgroups goes through device-wide
-// read-modify-write atomics, which are coherent across the chip's L2 caches: each
-// thread waits until its own atomics are acknowledged before the barrier, so they
-// precede the workgroup's increment of the counter, and the last workgroup reads
-// the totals with read-modify-write atomics too.  (An agent-scope fence would
-// write back and invalidate the L2 in every wave of every workgroup.)
-__device__ __forceinline__ bool last_workgroup(PruneState *st, uint32_t *flag, uint32_t active) {
+// Called by every thread of a workgroup after its global atomics: true in the one
+// workgroup that finishes last.  Values that cross workgroups go through
+// device-wide read-modify-write atomics, which are coherent across the chip's L2
+// caches: each thread waits until its own atomics are acknowledged before the
+// barrier, so they precede the workgroup's increment of the counter, and the last
+// workgroup reads them with read-modify-write atomics too.  (An agent-scope fence
+// would write back and invalidate the L2 in every wave of every workgroup.)
+__device__ __forceinline__ bool last_workgroup(uint32_t *done, uint32_t *flag) {
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     if (threadIdx.x == 0) {
-        const uint32_t before = atomicAdd(&st->done, 1u);
-        const bool last = before == active - 1;
-        if (last) atomicExch(&st->done, 0u);
-        *flag = last ? 1u : 0u;
+        const uint32_t before = atomicAdd(done, 1u);
+        *flag = before == gridDim.x - 1 ? 1u : 0u;
     }
     __syncthreads();
     return *flag != 0;
 }
 
-// One workgroup, after a histogram pass P with a digit of `width` bits: find the
-// digit d where the count of matching keys with digit > d is < k_rem <= that count
-// plus total[d], append it to the prefix, and clear `total` for the next pass.
-// Writes the whole selection (the pass may have derived base and source itself).
-__device__ __forceinline__ void select_digit(unsigned long long *__restrict__ total,
-                                             const Pass &P, int width,
-                                             PruneState *__restrict__ st, uint64_t *tot,
-                                             uint64_t *wave_tot) {
+// Number of bits needed to write v (0 for 0).
+__device__ __forceinline__ uint32_t bit_length(uint32_t v) { return v ? 32u - __clz(v) : 0u; }
+
+// Scratch of a workgroup that resolves a pending digit or the sample's bracket.
+struct ResolveLds {
+    uint64_t tot[kDigitBins];
+    uint64_t wave_tot[kHistWaves];
+    uint64_t v[8];
+    uint32_t d[4];
+};
+
+// The pass the state slot describes, with its pending digit chosen: the digit d of
+// the pending histogram where the count of matching keys with digit > d is < k_rem
+// <= that count plus total[d] is appended to the prefix.  Every workgroup of the
+// kernel does the same from the same totals, which the previous kernel completed
+// (plain loads suffice after the kernel boundary).
+__device__ __forceinline__ Pass resolve(const PruneState *__restrict__ S,
+                                        const unsigned long long *__restrict__ totals,
+                                        int key_bits, ResolveLds &L) {
+    Pass P;
+    P.prefix = S->prefix;
+    P.hi = S->hi < uint32_t(key_bits) ? S->hi : uint32_t(key_bits);
+    P.base = S->base;
+    P.cand = S->from_cand != 0;
+    P.k_rem = S->k_rem;
+    P.n_last = S->n_last;
+    const uint32_t width = S->pend_width < P.hi ? S->pend_width : P.hi;
+    if (width == 0) return P;                           // uniform
+    const unsigned long long *t = totals + size_t(S->pend_buf % kTotalsBuffers) * kDigitBins;
     const int bins = 1 << width;
-    for (int b = int(threadIdx.x); b < bins; b += kHistThreads) tot[b] = atomicExch(&total[b], 0ull);
+    for (int b = int(threadIdx.x); b < bins; b += kHistThreads) L.tot[b] = t[b];
+    if (threadIdx.x == 0) {                             // if no digit qualifies
+        L.v[0] = uint64_t(P.prefix) << width;
+        L.v[1] = uint64_t(P.k_rem);
+        L.v[2] = 0;
+    }
     __syncthreads();
     // thread t owns the digits bins-1-2t and bins-2-2t (descending order)
     const int d0 = bins - 1 - 2 * int(threadIdx.x), d1 = d0 - 1;
-    const uint64_t a = d0 >= 0 ? tot[d0] : 0, b = d1 >= 0 ? tot[d1] : 0;
-    const uint64_t incl = block_inclusive_scan(a + b, wave_tot);
+    const uint64_t a = d0 >= 0 ? L.tot[d0] : 0, b = d1 >= 0 ? L.tot[d1] : 0;
+    const uint64_t incl = block_inclusive_scan(a + b, L.wave_tot);
     const uint64_t excl = incl - a - b;
     const uint64_t k = uint64_t(P.k_rem);
-    if (threadIdx.x == 0) {
-        st->hi = P.hi - uint32_t(width);
-        st->base = P.base;
-        st->from_cand = P.cand ? 1u : 0u;
-    }
     if (excl < k && k <= incl) {                        // exactly one thread
-        uint32_t d;
-        uint64_t above;
-        if (k <= excl + a) {
-            d = uint32_t(d0);
-            above = excl;
-        } else {
-            d = uint32_t(d1);
-            above = excl + a;
-        }
-        st->prefix = (P.prefix << width) | d;
-        st->k_rem = int64_t(k - above);
-        st->n_last = d == uint32_t(d0) ? a : b;
+        const bool first = k <= excl + a;
+        const uint32_t d = first ? uint32_t(d0) : uint32_t(d1);
+        L.v[0] = (uint64_t(P.prefix) << width) | d;
+        L.v[1] = k - (first ? excl : excl + a);
+        L.v[2] = first ? a : b;
     }
+    __syncthreads();
+    P.prefix = uint32_t(L.v[0]);
+    P.hi -= width;
+    P.k_rem = int64_t(L.v[1]);
+    P.n_last = L.v[2];
+    return P;
 }
 
-// One workgroup, after the sample (n_s keys out of the matrix's total_keys, a
-// fraction f): the split pass's bracket [dlo, dhi] of fine first digits (the top FB
-// bits of the key) that holds the k-th largest key's, up to six standard
-// deviations of the sample count (a binomial) plus 8 keys: keys above dhi number
-// at most f*k - margin in the sample, keys at or above dlo at least f*k + margin.
-// One pass over W then suffices (`single`) unless the bracket's predicted
-// candidates exceed cand_limit.  The sample's totals are kept per coarse digit (the
-// top CB bits, in `total`, which this clears for the next pass) and per fine
-// digit (in `fine`, zeroed by the state reset): the coarse totals place the two
-// ends within a coarse digit each, and only those digits' fine totals are read
-// (reading every fine total from one workgroup costs about 10 us).
+// The split pass's bracket [dlo, dhi] of fine first digits (the top FB bits of the
+// key) from the sample (n_s keys out of the matrix's total_keys, a fraction f): it
+// holds the k-th largest key's digit up to six standard deviations of the sample
+// count (a binomial) plus 8 keys: keys above dhi number at most f*k - margin in the
+// sample, keys at or above dlo at least f*k + margin.  `single` unless the
+// bracket's predicted candidates exceed cand_limit.  The sample's totals are kept
+// per coarse digit (the top CB bits, totals buffer kBufSample) and per fine digit:
+// the coarse totals place the two ends within a coarse digit each, and only those
+// digits' fine totals are read.  Every workgroup of the split pass computes it,
+// thread t from the coarse totals a, b of digits CB-1-2t and CB-2-2t (loaded by the
+// caller, so that their latency overlaps other loads); results in L.d[0] (dlo),
+// L.d[1] (dhi), L.d[2] (single).
 template <int CB_BITS, int FB_BITS>
-__device__ __forceinline__ void select_bracket(unsigned long long *__restrict__ total,
-                                               unsigned long long *__restrict__ fine,
-                                               PruneState *__restrict__ st, int64_t total_keys,
-                                               int64_t k, uint64_t cand_limit, uint64_t *tot,
-                                               uint64_t *wave_tot, uint32_t *s_d, uint64_t *s_c,
-                                               uint64_t *s_f) {
+__device__ __forceinline__ void bracket(uint64_t a, uint64_t b,
+                                        const unsigned long long *__restrict__ fine,
+                                        int64_t total_keys, int64_t k, uint64_t cand_limit,
+                                        ResolveLds &L) {
     constexpr int CB = 1 << CB_BITS;
     constexpr int R = 1 << (FB_BITS - CB_BITS);         // fine digits per coarse digit
     constexpr uint32_t kNone = 0xFFFFFFFFu;
-    static_assert(2 * R <= kHistThreads, "one thread per boundary fine digit");
-    for (int b = int(threadIdx.x); b < CB; b += kHistThreads) tot[b] = atomicExch(&total[b], 0ull);
+    static_assert(2 * R <= kHistThreads && CB <= kDigitBins, "bracket scratch");
     if (threadIdx.x == 0) {
-        s_d[0] = kNone;                                 // coarse digit of dhi
-        s_d[1] = kNone;                                 // coarse digit of dlo
+        L.d[0] = kNone;                                 // coarse digit of dhi
+        L.d[1] = kNone;                                 // coarse digit of dlo
     }
-    __syncthreads();
-    // thread t owns the coarse digits CB-1-2t and CB-2-2t (descending order)
     const int d0 = CB - 1 - 2 * int(threadIdx.x), d1 = d0 - 1;
-    const uint64_t a = d0 >= 0 ? tot[d0] : 0, b = d1 >= 0 ? tot[d1] : 0;
-    const uint64_t incl = block_inclusive_scan(a + b, wave_tot);
+    const uint64_t incl = block_inclusive_scan(a + b, L.wave_tot);
     const uint64_t excl = incl - a - b;
-    if (threadIdx.x == kHistThreads - 1) s_c[4] = incl;
+    if (threadIdx.x == kHistThreads - 1) L.v[4] = incl;
     __syncthreads();
-    const uint64_t n_s = s_c[4];
+    const uint64_t n_s = L.v[4];
     const double q = double(k) / double(total_keys);
     const double ks = q * double(n_s);
     const double margin = 6.0 * sqrt(ks * (1.0 - q)) + 8.0;
@@ -345,29 +376,28 @@ __device__ __forceinline__ void select_bracket(unsigned long long *__restrict__ 
     // both non-increasing in d: dhi is the one digit with above <= lo < above + c
     // (or digit 0 with above <= lo), dlo the one with above < hi <= above + c (or
     // the top digit with above + c >= hi); first among the coarse digits
-    auto coarse = [&](int d, uint64_t above, uint64_t c) {
+    auto coarse_end = [&](int d, uint64_t above, uint64_t c) {
         if (d < 0) return;
         const double ab = double(above), at = double(above + c);
         if (ab <= lo && (d == 0 || at > lo)) {
-            s_d[0] = uint32_t(d);
-            s_c[0] = above;
-            s_c[1] = c;
+            L.d[0] = uint32_t(d);
+            L.v[0] = above;
         }
         if (at >= hi && (d == CB - 1 || ab < hi)) {
-            s_d[1] = uint32_t(d);
-            s_c[2] = above;
-            s_c[3] = c;
+            L.d[1] = uint32_t(d);
+            L.v[2] = above;
+            L.v[3] = c;
         }
     };
-    coarse(d0, excl, a);
-    coarse(d1, excl + a, b);
+    coarse_end(d0, excl, a);
+    coarse_end(d1, excl + a, b);
     __syncthreads();
-    const uint32_t chi = s_d[0], clo = s_d[1];
+    const uint32_t chi = L.d[0], clo = L.d[1];
     // then among the fine digits of those two coarse digits
+    uint64_t *f = L.tot;
     if (threadIdx.x < 2 * R) {
         const uint32_t c = threadIdx.x < R ? chi : clo;
-        s_f[threadIdx.x] =
-            c == kNone ? 0ull : atomicAdd(&fine[c * R + (threadIdx.x & (R - 1))], 0ull);
+        f[threadIdx.x] = c == kNone ? 0ull : fine[c * R + (threadIdx.x & (R - 1))];
     }
     __syncthreads();
     if (threadIdx.x == 0) {
@@ -378,30 +408,29 @@ __device__ __forceinline__ void select_bracket(unsigned long long *__restrict__ 
         uint64_t above_hi = 0, at_lo = n_s;
         if (chi != kNone) {
             dhi = chi * R + R - 1;
-            above_hi = s_c[0];
-            uint64_t ab = s_c[0];
+            above_hi = L.v[0];
+            uint64_t ab = L.v[0];
             for (int j = R - 1; j >= 0; --j) {
-                const uint32_t f = chi * R + uint32_t(j);
-                if (double(ab) <= lo && (f == 0 || double(ab + s_f[j]) > lo)) {
-                    dhi = f;
+                const uint32_t fd = chi * R + uint32_t(j);
+                if (double(ab) <= lo && (fd == 0 || double(ab + f[j]) > lo)) {
+                    dhi = fd;
                     above_hi = ab;
                     break;
                 }
-                ab += s_f[j];
+                ab += f[j];
             }
         }
         if (clo != kNone) {
             dlo = clo * R;
-            at_lo = s_c[2] + s_c[3];
-            uint64_t ab = s_c[2];
+            at_lo = L.v[2] + L.v[3];
+            uint64_t ab = L.v[2];
             for (int j = R - 1; j >= 0; --j) {
-                const uint32_t f = clo * R + uint32_t(j);
-                if (double(ab + s_f[R + j]) >= hi) {
-                    dlo = f;
-                    at_lo = ab + s_f[R + j];
+                if (double(ab + f[R + j]) >= hi) {
+                    dlo = clo * R + uint32_t(j);
+                    at_lo = ab + f[R + j];
                     break;
                 }
-                ab += s_f[R + j];
+                ab += f[R + j];
             }
         }
         // predicted candidates: the bracket's sample keys scaled by 1/f
@@ -409,10 +438,11 @@ __device__ __forceinline__ void select_bracket(unsigned long long *__restrict__ 
         const uint64_t in_all = ok ? at_lo - above_hi : 0;
         const bool fits = ok && n_s > 0 && double(in_all) * double(total_keys) <=
                                                double(cand_limit) * double(n_s);
-        st->single = fits ? 1u : 0u;
-        st->dlo = dlo;
-        st->dhi = dhi;
+        L.d[0] = dlo;
+        L.d[1] = dhi;
+        L.d[2] = fits ? 1u : 0u;
     }
+    __syncthreads();
 }
 
 // What a histogram pass is for.
@@ -422,71 +452,89 @@ enum HistRole {
                           // hold the threshold, else from W (from the first digit on)
 };
 
-// Number of bits needed to write v (0 for 0).
-__device__ __forceinline__ uint32_t bit_length(uint32_t v) { return v ? 32u - __clz(v) : 0u; }
-
-// The pass the state describes; for the first pass after a split pass that kept
-// the sample's bracket, the one its results call for (every workgroup derives the
-// same from the same state): the candidates' keys relative to the bracket's lowest
-// key when G < k <= G + candidates (G the keys above the bracket), else all of W
-// from the first digit.  `cap` bounds the candidate count read from the state.
+// The pass after a split pass that kept the sample's bracket: over the candidates'
+// keys relative to the bracket's lowest key when G < k <= G + candidates (G the
+// keys above the bracket), else over all of W from the first digit.  `cap` bounds
+// the candidate count read back.
 template <typename Bits>
-__device__ __forceinline__ Pass pass_from_state(const PruneState *__restrict__ st, int role,
-                                                int64_t k, uint64_t cap) {
+__device__ __forceinline__ Pass pass_after_split(const SplitInfo *__restrict__ I, int64_t k,
+                                                 uint64_t cap) {
     constexpr int KB = PruneTraits<Bits>::KEY_BITS;
+    constexpr int first_shift = KB - PruneTraits<Bits>::SAMPLE_BITS;
     Pass P;
-    if (role == kRoleAfterSplit && st->single) {
-        constexpr int first_shift = KB - PruneTraits<Bits>::SAMPLE_BITS;
-        const uint64_t G = st->n_above, n = st->n_cand, kk = uint64_t(k);
-        const uint32_t dlo = st->dlo, dhi = st->dhi;
-        if (!st->overflow && n <= cap && dlo <= dhi && G < kk && kk <= G + n) {
-            P.base = dlo << first_shift;
-            P.prefix = 0;
-            P.hi = uint32_t(first_shift) + bit_length(dhi - dlo);
-            P.cand = true;
-            P.k_rem = int64_t(kk - G);
-        } else {
-            P.base = 0;
-            P.prefix = 0;
-            P.hi = KB;
-            P.cand = false;
-            P.k_rem = k;
-        }
+    const uint64_t G = I->n_above, n = I->n_cand, kk = uint64_t(k);
+    const uint32_t dlo = I->dlo, dhi = I->dhi;
+    P.prefix = 0;
+    P.n_last = 0;
+    if (!I->overflow && n <= cap && dlo <= dhi && G < kk && kk <= G + n) {
+        P.base = dlo << first_shift;
+        P.hi = uint32_t(first_shift) + bit_length(dhi - dlo);
+        P.cand = true;
+        P.k_rem = int64_t(kk - G);
     } else {
-        P.base = st->base;
-        P.prefix = st->prefix;
-        P.hi = st->hi < uint32_t(KB) ? st->hi : uint32_t(KB);
-        P.cand = st->from_cand != 0;
-        P.k_rem = st->k_rem;
+        P.base = 0;
+        P.hi = KB;
+        P.cand = false;
+        P.k_rem = k;
     }
     return P;
 }
 
-// One workgroup's part of histogram pass P (digit of `width` bits): the LDS
-// histogram of its keys that match the prefix, added into `total`; the keys come
-// from W (ranges of per_wave elements range_stride apart) or from the n
-// candidates.  Over candidates only the workgroups they fill take part (returns
-// false at once in the others).  True in the workgroup that finishes last.
+// Write the state slot the next kernel reads: pass P, with its digit of `width`
+// bits pending in totals buffer `buf` (width 0: nothing pending).
+__device__ __forceinline__ void hand_on(PruneState *__restrict__ out, const Pass &P, int width,
+                                        int buf) {
+    out->prefix = P.prefix;
+    out->hi = P.hi;
+    out->base = P.base;
+    out->from_cand = P.cand ? 1u : 0u;
+    out->k_rem = P.k_rem;
+    out->n_last = P.n_last;
+    out->pend_width = uint32_t(width);
+    out->pend_buf = uint32_t(buf);
+}
+
+// A histogram pass: the pending digit chosen, the next digit's histogram (over W or
+// the candidates) into totals buffer `buf`.  Over candidates only the workgroups
+// they fill take part, and their keys are loaded before the pending digit is
+// chosen (one memory latency for both).  A pass that would find every bit chosen
+// once the pending digit is leaves that digit to the count and hands the state on.
 template <typename Bits, bool ALIGNED>
-__device__ __forceinline__ bool hist_pass(const Bits *__restrict__ W, int64_t ldw, int64_t M,
-                                          int64_t N, int64_t per_wave, int64_t range_stride,
-                                          const Pass &P, int width, uint64_t n,
-                                          PruneState *__restrict__ st,
-                                          unsigned long long *__restrict__ total,
-                                          const uint64_t *__restrict__ cand, uint32_t *hist,
-                                          uint32_t *flag) {
+__global__ __launch_bounds__(kHistThreads) void prune_hist_kernel(
+    const Bits *__restrict__ W, int64_t ldw, int64_t M, int64_t N, int64_t per_wave,
+    PruneState *__restrict__ slots, const SplitInfo *__restrict__ info,
+    unsigned long long *__restrict__ totals, const uint64_t *__restrict__ cand, int rd, int buf,
+    int role, int64_t k, uint64_t cap) {
     constexpr int kStride = (1 << kMaxDigitBits) + 1;   // copies land in different banks
-    const int bins = 1 << width;
-    // kCandPerThread candidates per thread: few workgroups, so few bins to flush
-    const uint64_t per_group = uint64_t(kCandPerThread) * kHistThreads;
+    constexpr int KB = PruneTraits<Bits>::KEY_BITS;
+    __shared__ uint32_t hist[kCopies * kStride];
+    __shared__ ResolveLds L;
+    const PruneState *S = slots + rd;
+    const bool derived = role == kRoleAfterSplit && info->single;   // uniform
+    Pass P;
+    bool from_cand;
+    if (derived) {
+        P = pass_after_split<Bits>(info, k, cap);
+        from_cand = P.cand;
+    } else {
+        const uint32_t hi = S->hi < uint32_t(KB) ? S->hi : uint32_t(KB);
+        if (hi <= S->pend_width) {                      // nothing after the pending digit
+            if (blockIdx.x == 0 && threadIdx.x == 0) slots[rd ^ 1] = *S;
+            return;
+        }
+        from_cand = S->from_cand != 0;
+    }
+    uint64_t n = 0;
     uint32_t active = gridDim.x;
-    if (P.cand) {
+    const uint64_t per_group = uint64_t(kCandPerThread) * kHistThreads;
+    if (from_cand) {
+        n = info->n_cand;
+        if (n > cap) n = cap;
+        // kCandPerThread candidates per thread: few workgroups, so few bins to flush
         const uint64_t g = n > per_group ? (n + per_group - 1) / per_group : 1;
         if (g < active) active = uint32_t(g);
     }
-    if (blockIdx.x >= active) return false;            // uniform
-    // over candidates, the thread's first keys are on their way while the histogram
-    // is cleared (the barrier waits for the LDS writes only)
+    if (blockIdx.x >= active) return;                   // uniform; workgroup 0 stays
     const uint64_t stride = uint64_t(active) * kHistThreads;
     uint64_t i0 = uint64_t(blockIdx.x) * kHistThreads + threadIdx.x;
     uint32_t kk[kCandPerThread];
@@ -497,7 +545,12 @@ __device__ __forceinline__ bool hist_pass(const Bits *__restrict__ W, int64_t ld
             kk[j] = i < n ? uint32_t(cand[i]) : 0u;
         }
     };
-    if (P.cand) load_batch();
+    if (from_cand) load_batch();
+    asm volatile("" ::: "memory");                      // the loads go out first
+    if (!derived) P = resolve(S, totals, KB, L);
+    const int width = digit_width(int(P.hi));
+    if (blockIdx.x == 0 && threadIdx.x == 0) hand_on(slots + (rd ^ 1), P, width, buf);
+    const int bins = 1 << width;
     for (int i = int(threadIdx.x); i < kCopies * kStride; i += kHistThreads) hist[i] = 0;
     asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
     const uint32_t prefix = P.prefix, base = P.base, hi = P.hi;   // hi <= key bits <= 31
@@ -508,7 +561,7 @@ __device__ __forceinline__ bool hist_pass(const Bits *__restrict__ W, int64_t ld
         const uint32_t rel = key - base;
         if ((rel >> hi) == prefix) atomicAdd(&mine[(rel >> shift) & dmask], 1u);
     };
-    if (P.cand) {
+    if (from_cand) {
         // all of a batch's loads issued before its LDS atomics
         while (i0 < n) {
 #pragma unroll
@@ -518,63 +571,32 @@ __device__ __forceinline__ bool hist_pass(const Bits *__restrict__ W, int64_t ld
             if (i0 < n) load_batch();
         }
     } else {
-        for_each_key<Bits, ALIGNED>(W, ldw, M, N, per_wave, range_stride, [](int64_t) {}, add);
+        for_each_key<Bits, ALIGNED>(W, ldw, M, N, per_wave, per_wave, [](int64_t) {}, add);
     }
     __syncthreads();
+    unsigned long long *total = totals + size_t(buf) * kDigitBins;
     for (int b = int(threadIdx.x); b < bins; b += kHistThreads) {
-        uint32_t s = 0;
+        uint32_t v = 0;
 #pragma unroll
-        for (int c = 0; c < kCopies; ++c) s += hist[c * kStride + b];
-        if (s) atomicAdd(&total[b], (unsigned long long)s);
+        for (int c = 0; c < kCopies; ++c) v += hist[c * kStride + b];
+        if (v) atomicAdd(&total[b], (unsigned long long)v);
     }
-    return last_workgroup(st, flag, active);
-}
-
-// A histogram pass (role above); the last workgroup picks the digit.  A pass that
-// finds every bit chosen does nothing.
-template <typename Bits, bool ALIGNED>
-__global__ __launch_bounds__(kHistThreads) void prune_hist_kernel(
-    const Bits *__restrict__ W, int64_t ldw, int64_t M, int64_t N, int64_t per_wave,
-    int64_t range_stride, PruneState *__restrict__ st, unsigned long long *__restrict__ total,
-    const uint64_t *__restrict__ cand, int role, int64_t k, uint64_t cap) {
-    constexpr int kStride = (1 << kMaxDigitBits) + 1;
-    __shared__ uint32_t hist[kCopies * kStride];
-    __shared__ uint64_t tot[1 << kMaxDigitBits];
-    __shared__ uint64_t wave_tot[kHistWaves];
-    __shared__ uint32_t flag;
-    const Pass P = pass_from_state<Bits>(st, role, k, cap);
-    if (P.hi == 0) return;                              // uniform: the threshold is known
-    const int width = digit_width(int(P.hi));
-    uint64_t n = 0;
-    if (P.cand) {
-        n = st->n_cand;
-        if (n > cap) n = cap;
-    }
-    if (!hist_pass<Bits, ALIGNED>(W, ldw, M, N, per_wave, range_stride, P, width, n, st, total,
-                                  cand, hist, &flag))
-        return;
-    select_digit(total, P, width, st, tot, wave_tot);
 }
 
 // The sample: the histogram of the keys' first SAMPLE_BITS bits over ranges of
 // chunk elements range_stride apart (one range per wave), added into `fine`, and
-// of their first digit_width(KEY_BITS) bits, added into `total`; the last
-// workgroup picks the split pass's bracket.
+// of their first digit_width(KEY_BITS) bits, added into `coarse`.
 template <typename Bits, bool ALIGNED>
 __global__ __launch_bounds__(kHistThreads) void prune_sample_kernel(
     const Bits *__restrict__ W, int64_t ldw, int64_t M, int64_t N, int64_t chunk,
-    int64_t range_stride, PruneState *__restrict__ st, unsigned long long *__restrict__ total,
-    unsigned long long *__restrict__ fine, int64_t k, uint64_t cand_limit) {
+    int64_t range_stride, unsigned long long *__restrict__ coarse,
+    unsigned long long *__restrict__ fine) {
     constexpr int KB = PruneTraits<Bits>::KEY_BITS;
     constexpr int FB = PruneTraits<Bits>::SAMPLE_BITS;
     constexpr int CB = digit_width(KB);
     constexpr int R = 1 << (FB - CB);
     constexpr uint32_t shift = uint32_t(KB - FB);
     __shared__ uint32_t hist[1 << FB];
-    __shared__ uint64_t tot[1 << CB];
-    __shared__ uint64_t wave_tot[kHistWaves];
-    __shared__ uint64_t s_c[5], s_f[2 * R];
-    __shared__ uint32_t s_d[2], flag;
     for (int i = int(threadIdx.x); i < (1 << FB); i += kHistThreads) hist[i] = 0;
     __syncthreads();
     for_each_key<Bits, ALIGNED>(W, ldw, M, N, chunk, range_stride, [](int64_t) {},
@@ -588,53 +610,77 @@ __global__ __launch_bounds__(kHistThreads) void prune_sample_kernel(
         uint32_t v = 0;
 #pragma unroll
         for (int j = 0; j < R; ++j) v += hist[c * R + j];
-        if (v) atomicAdd(&total[c], (unsigned long long)v);
+        if (v) atomicAdd(&coarse[c], (unsigned long long)v);
     }
-    if (!last_workgroup(st, &flag, gridDim.x)) return;
-    select_bracket<CB, FB>(total, fine, st, M * N, k, cand_limit, tot, wave_tot, s_d, s_c, s_f);
 }
 
-// The split pass, once the sample's bracket [dlo, dhi] of first digits is known:
-// per row, the keys with first digit > dhi go to gt1 (and their total to the
-// state's n_above); keys with first digit in the bracket are stored as
-// (row << 32 | key) candidates.  Runs in the same grid as the histogram passes.  If
-// any workgroup's candidates overflow its LDS or the workspace's room, the state's
-// overflow flag sends the later passes back to W.  Without `single` (the bracket
-// would hold too many keys) it takes the exact first digit over W instead.
+// The split pass.  Every workgroup computes the sample's bracket [dlo, dhi] of fine
+// first digits while the lines of its first round of W are on their way to the L2
+// (the coarse sample totals are requested first).  With `single`, per row the keys
+// with first digit > dhi go to gt1 (and their total to the split info's n_above)
+// and the keys inside the bracket are stored as (row << 32 | key) candidates; if a
+// wave's candidates overflow its LDS region or the workspace's room, the overflow
+// flag sends the later passes back to W.  Without `single` (the bracket would hold
+// too many keys) it takes the histogram of the first digit over W instead, into
+// totals buffer `buf`.  Runs in the same grid as the histogram passes.
 template <typename Bits, bool ALIGNED>
 __global__ __launch_bounds__(kHistThreads) void prune_split_kernel(
     const Bits *__restrict__ W, int64_t ldw, int64_t M, int64_t N, int64_t per_wave,
-    PruneState *__restrict__ st, unsigned long long *__restrict__ gt1,
-    uint64_t *__restrict__ cand, uint64_t cap, unsigned long long *__restrict__ total) {
+    PruneState *__restrict__ slots, SplitInfo *__restrict__ info,
+    unsigned long long *__restrict__ totals, const unsigned long long *__restrict__ fine,
+    unsigned long long *__restrict__ gt1, uint64_t *__restrict__ cand, uint64_t cap, int rd,
+    int buf, int64_t k, uint64_t cand_limit) {
     constexpr int kStride = (1 << kMaxDigitBits) + 1;
     constexpr int KB = PruneTraits<Bits>::KEY_BITS;
-    constexpr int first_shift = KB - PruneTraits<Bits>::SAMPLE_BITS;
-    __shared__ uint64_t buf[kSplitLds];
-    __shared__ uint32_t hist[kCopies * kStride];
-    __shared__ uint64_t tot[1 << kMaxDigitBits];
-    __shared__ uint64_t wave_tot[kHistWaves];
-    __shared__ uint32_t wave_n[kHistWaves], flag;
-    __shared__ uint64_t base;
-    if (!st->single) {                                  // uniform
-        Pass P;
-        P.prefix = 0;
-        P.hi = KB;
-        P.base = 0;
-        P.cand = false;
-        P.k_rem = st->k_rem;
-        if (hist_pass<Bits, ALIGNED>(W, ldw, M, N, per_wave, per_wave, P, digit_width(KB), 0, st,
-                                     total, cand, hist, &flag))
-            select_digit(total, P, digit_width(KB), st, tot, wave_tot);
-        return;
-    }
+    constexpr int FB = PruneTraits<Bits>::SAMPLE_BITS;
+    constexpr int CB = digit_width(KB);
+    constexpr int first_shift = KB - FB;
+    constexpr uint32_t hist_shift = uint32_t(KB - CB);
     static_assert(kWaveRoom * kHistWaves == kSplitLds, "one LDS region per wave");
-    const uint32_t dlo = st->dlo, dhi = st->dhi;
+    __shared__ uint64_t buf_lds[kSplitLds];
+    __shared__ uint32_t hist[kCopies * kStride];
+    __shared__ ResolveLds L;
+    __shared__ uint32_t wave_n[kHistWaves];
+    __shared__ uint64_t base;
+    // this thread's two coarse sample totals (digits (1<<CB)-1-2t and (1<<CB)-2-2t)
+    const unsigned long long *coarse = totals + size_t(kBufSample) * kDigitBins;
+    const int c0 = (1 << CB) - 1 - 2 * int(threadIdx.x), c1 = c0 - 1;
+    const uint64_t ca = c0 >= 0 ? coarse[c0] : 0, cb = c1 >= 0 ? coarse[c1] : 0;
+    asm volatile("" ::: "memory");                      // these loads go out first
     const int lane = int(threadIdx.x) & (kWave - 1);
     const int wave = __builtin_amdgcn_readfirstlane(int(threadIdx.x) / kWave);
-    uint64_t *mine = buf + wave * kWaveRoom;
+    uint64_t *mine = buf_lds + wave * kWaveRoom;
+    uint32_t *hmine = hist + (int(threadIdx.x) & (kCopies - 1)) * kStride;
+    uint32_t dlo = 0, dhi = 0;
+    bool single = true;
+    // the bracket, the split info and the next state slot (and, without `single`,
+    // the cleared histogram)
+    auto hook = [&]() {
+        bracket<CB, FB>(ca, cb, fine, M * N, k, cand_limit, L);
+        dlo = L.d[0];
+        dhi = L.d[1];
+        single = L.d[2] != 0;                           // uniform
+        if (blockIdx.x == 0 && threadIdx.x == 0) {
+            info->single = single ? 1u : 0u;
+            info->dlo = dlo;
+            info->dhi = dhi;
+            Pass P0;                                    // nothing chosen yet
+            P0.prefix = 0;
+            P0.hi = KB;
+            P0.base = 0;
+            P0.cand = false;
+            P0.k_rem = k;
+            P0.n_last = 0;
+            hand_on(slots + (rd ^ 1), P0, single ? 0 : CB, buf);
+        }
+        if (!single) {
+            for (int i = int(threadIdx.x); i < kCopies * kStride; i += kHistThreads) hist[i] = 0;
+            __syncthreads();
+        }
+    };
     // the wave's candidates so far and its keys above the bracket (wave-uniform):
-    // each wave fills its own LDS region, so no atomic (and no wait for one) sits
-    // between a round's keys and the next round's loads
+    // each wave fills its own LDS region, so no atomic sits between a round's keys
+    // and the next round's loads
     uint32_t wn = 0;
     uint64_t w_above = 0;
     int64_t cur = -1;
@@ -648,6 +694,29 @@ __global__ __launch_bounds__(kHistThreads) void prune_split_kernel(
         n_gt = 0;
     };
     constexpr int K = PruneTraits<Bits>::UNROLL * PruneTraits<Bits>::VEC;
+    {
+        // request the lines of the wave's first round now (plain loads: they stay in
+        // the L2), so that the bracket's two round trips overlap that round's
+        // latency instead of preceding it
+        constexpr int VEC = PruneTraits<Bits>::VEC;
+        const int64_t Np = padded_n<Bits>(N);
+        const int64_t a = (int64_t(blockIdx.x) * kHistWaves + wave) * per_wave;
+        constexpr int U = PruneTraits<Bits>::UNROLL;
+        // unconditional (a wave without a range reads row 0, indices are clamped into
+        // the row): the compiler then waits for the older coarse totals alone
+        const int64_t a0 = a < M * Np ? a : 0;
+        const int64_t r = a0 / Np, c = a0 - r * Np;
+        const Bits *row = W + r * ldw;
+        uint32_t warm[U];
+#pragma unroll
+        for (int q = 0; q < U; ++q) {
+            const int64_t cc = c + int64_t(q) * kWave * VEC + int64_t(lane) * VEC;
+            warm[q] = uint32_t(row[cc < N ? cc : N - 1]);
+        }
+        hook();
+#pragma unroll
+        for (int q = 0; q < U; ++q) asm volatile("" ::"v"(warm[q]));   // used (and done) here
+    }
     for_each_round<Bits, ALIGNED>(
         W, ldw, M, N, per_wave, per_wave,
         [&](int64_t r) {
@@ -657,6 +726,12 @@ __global__ __launch_bounds__(kHistThreads) void prune_split_kernel(
             }
         },
         [&](const uint32_t (&keys)[K], uint32_t mask) {
+            if (!single) {                              // uniform: the first digit's histogram
+#pragma unroll
+                for (int j = 0; j < K; ++j)
+                    if ((mask >> j) & 1u) atomicAdd(&hmine[keys[j] >> hist_shift], 1u);
+                return;
+            }
             // branch-free over the round's keys: the count above the bracket and a
             // mask of the candidates; then one ballot per key slot, and each lane
             // places its own candidates by the set bits below it in the ballot
@@ -681,10 +756,21 @@ __global__ __launch_bounds__(kHistThreads) void prune_split_kernel(
                 }
             }
         });
+    if (!single) {                                      // uniform
+        __syncthreads();
+        unsigned long long *total = totals + size_t(buf) * kDigitBins;
+        for (int b = int(threadIdx.x); b < (1 << CB); b += kHistThreads) {
+            uint32_t v = 0;
+#pragma unroll
+            for (int c = 0; c < kCopies; ++c) v += hist[c * kStride + b];
+            if (v) atomicAdd(&total[b], (unsigned long long)v);
+        }
+        return;
+    }
     flush();
     if (lane == 0) {
         wave_n[wave] = wn;
-        wave_tot[wave] = w_above;
+        L.wave_tot[wave] = w_above;
     }
     __syncthreads();
     if (threadIdx.x == 0) {
@@ -694,20 +780,20 @@ __global__ __launch_bounds__(kHistThreads) void prune_split_kernel(
         for (int w = 0; w < kHistWaves; ++w) {
             n += wave_n[w];
             over = over || wave_n[w] > uint32_t(kWaveRoom);
-            above += wave_tot[w];
+            above += L.wave_tot[w];
         }
         uint64_t b = 0;
         if (over) {
-            atomicExch(&st->overflow, 1u);
+            atomicExch(&info->overflow, 1u);
             b = cap;                                    // nothing is copied
         } else if (n > 0) {
-            b = atomicAdd(&st->n_cand, (unsigned long long)n);
+            b = atomicAdd(&info->n_cand, (unsigned long long)n);
             if (b + n > cap) {
-                atomicExch(&st->overflow, 1u);
+                atomicExch(&info->overflow, 1u);
                 b = cap;
             }
         }
-        if (above) atomicAdd(&st->n_above, (unsigned long long)above);
+        if (above) atomicAdd(&info->n_above, (unsigned long long)above);
         base = b;
     }
     __syncthreads();
@@ -720,11 +806,10 @@ __global__ __launch_bounds__(kHistThreads) void prune_split_kernel(
 
 // counts[r] (= keys > t) += the keys == t taken in ascending row order, need in
 // total; one workgroup.
-__device__ __forceinline__ void take_ties(int64_t M, const PruneState *__restrict__ st,
+__device__ __forceinline__ void take_ties(int64_t M, int64_t need,
                                           unsigned long long *__restrict__ counts,
                                           unsigned long long *__restrict__ eq,
                                           uint64_t *wave_tot, int64_t *tile_total) {
-    const int64_t need = st->k_rem;
     int64_t carry = 0;                                   // keys == t in rows before the tile
     for (int64_t base = 0; base < M; base += kHistThreads) {
         const int64_t r = base + threadIdx.x;
@@ -744,35 +829,47 @@ __device__ __forceinline__ void take_ties(int64_t M, const PruneState *__restric
     }
 }
 
-// Per-row counts of keys > t (into counts) and == t (into eq); t = base + prefix.
-// From the candidates when they hold the threshold (plus the split pass's gt1),
-// else from W.  When only some keys == t are kept, the last workgroup to finish
-// then adds those.
+// Per-row counts of keys > t (into counts) and == t (into eq); t = base + prefix
+// once the pending digit is chosen.  From the candidates when they hold the
+// threshold (plus the split pass's gt1), else from W.  When only some keys == t
+// are kept, the last workgroup to finish then adds those.
 template <typename Bits, bool ALIGNED>
 __global__ __launch_bounds__(kHistThreads) void prune_count_kernel(
     const Bits *__restrict__ W, int64_t ldw, int64_t M, int64_t N, int64_t per_wave,
-    PruneState *__restrict__ st, unsigned long long *__restrict__ gt,
+    const PruneState *__restrict__ slots, SplitInfo *__restrict__ info,
+    const unsigned long long *__restrict__ totals, unsigned long long *__restrict__ gt,
     unsigned long long *__restrict__ eq, const uint64_t *__restrict__ cand,
-    const unsigned long long *__restrict__ gt1, uint64_t cap) {
-    __shared__ uint64_t wave_tot[kHistWaves];
+    const unsigned long long *__restrict__ gt1, uint64_t cap, int rd) {
+    constexpr int KB = PruneTraits<Bits>::KEY_BITS;
+    __shared__ ResolveLds L;
     __shared__ int64_t tile_total;
     __shared__ uint32_t flag;
-    const uint32_t t = st->base + st->prefix;
+    const int lane = int(threadIdx.x) & (kWave - 1);
+    // over candidates, this lane's first one is loaded before the pending digit is
+    // chosen (one memory latency for both)
+    const bool from_cand = slots[rd].from_cand != 0;   // uniform
+    uint64_t n = 0;
+    if (from_cand) {
+        n = info->n_cand;
+        if (n > cap) n = cap;
+    }
+    const uint64_t stride = uint64_t(gridDim.x) * kHistThreads;
+    const uint64_t first = uint64_t(blockIdx.x) * kHistThreads + threadIdx.x;
+    uint64_t c_next = from_cand && first < n ? cand[first] : 0;
+    asm volatile("" ::: "memory");                      // the load goes out first
+    const Pass P = resolve(slots + rd, totals, KB, L);
+    const uint32_t t = P.base + P.prefix;
     // when every key equal to t is taken (always, without ties), they count with the
     // keys above t and nothing is left for the last workgroup
-    const bool all_ties = st->n_last == (unsigned long long)st->k_rem;
+    const bool all_ties = P.n_last == (unsigned long long)P.k_rem;
     unsigned long long *__restrict__ eqc = all_ties ? gt : eq;
-    const int lane = int(threadIdx.x) & (kWave - 1);
-    if (st->from_cand) {                                // uniform
+    if (from_cand) {                                    // uniform
         // a wave's 64 candidates come in runs from few rows (each run is one
         // wave-round of the split pass): one atomic per row present and kind
-        uint64_t n = st->n_cand;
-        if (n > cap) n = cap;
-        const uint64_t stride = uint64_t(gridDim.x) * kHistThreads;
-        const uint64_t first = uint64_t(blockIdx.x) * kHistThreads + threadIdx.x;
         for (uint64_t i0 = first - uint64_t(lane); i0 < n; i0 += stride) {   // wave-uniform
             const uint64_t i = i0 + uint64_t(lane);
-            const uint64_t c = i < n ? cand[i] : 0;
+            const uint64_t c = c_next;
+            c_next = i + stride < n ? cand[i + stride] : 0;
             const uint32_t key = uint32_t(c);
             const int64_t r = int64_t(c >> 32);
             const bool ok = i < n && r < M;
@@ -830,38 +927,35 @@ __global__ __launch_bounds__(kHistThreads) void prune_count_kernel(
         flush();
     }
     if (all_ties) return;                               // uniform
-    if (last_workgroup(st, &flag, gridDim.x)) take_ties(M, st, gt, eq, wave_tot, &tile_total);
+    if (last_workgroup(&info->done, &flag))
+        take_ties(M, P.k_rem, gt, eq, L.wave_tot, &tile_total);
 }
 
-// Zero counts, eq, gt1, the digit totals and the sample's fine totals, and set the state to (no digit
-// chosen: prefix 0, hi = the key's bits, base 0; k_rem = k, no candidates).
+// Zero counts, eq, gt1, the split info and every totals buffer, and write state
+// slot 0: nothing chosen yet (prefix 0, hi = the key's bits, base 0, k_rem = k).
 __global__ __launch_bounds__(256) void prune_init_kernel(int64_t M, int64_t k, int key_bits,
-                                                         PruneState *st, int64_t *counts,
-                                                         int64_t *eq, int64_t *gt1,
-                                                         uint64_t *total, uint64_t *fine) {
+                                                         PruneState *slots, SplitInfo *info,
+                                                         int64_t *counts, int64_t *eq,
+                                                         int64_t *gt1, uint64_t *totals,
+                                                         uint64_t *fine) {
     const int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x;
     if (i < M) {
         counts[i] = 0;
         eq[i] = 0;
         gt1[i] = 0;
     }
-    if (i < (int64_t(1) << kMaxDigitBits)) total[i] = 0;
+    if (i < int64_t(kTotalsBuffers) * kDigitBins) totals[i] = 0;
     if (i < kFineBins) fine[i] = 0;
-    if (i == 0 && st) {
-        st->prefix = 0;
-        st->hi = uint32_t(key_bits);
-        st->base = 0;
-        st->from_cand = 0;
-        st->overflow = 0;
-        st->done = 0;
-        st->single = 0;
-        st->dlo = 0;
-        st->dhi = 0;
-        st->pad = 0;
-        st->k_rem = k;
-        st->n_cand = 0;
-        st->n_above = 0;
-        st->n_last = 0;
+    if (i == 0) {
+        *info = SplitInfo{};
+        Pass P0;
+        P0.prefix = 0;
+        P0.hi = uint32_t(key_bits);
+        P0.base = 0;
+        P0.cand = false;
+        P0.k_rem = k;
+        P0.n_last = 0;
+        hand_on(slots, P0, 0, 0);
     }
 }
 
@@ -902,23 +996,26 @@ int64_t cand_capacity(int64_t M, int64_t N) {
     return c;
 }
 
-// Workspace: the state, the digit totals, the per-row counts of keys equal to the
-// threshold and of keys above the first digit, then the candidates.
+// Workspace: the two state slots and the split info, the totals buffers, the
+// sample's fine totals, the per-row counts of keys equal to the threshold and of
+// keys above the first digit, then the candidates.
 struct PruneWorkspace {
-    PruneState *st;
-    uint64_t *total;        // [2^kMaxDigitBits]
+    PruneState *slots;      // [2]
+    SplitInfo *info;
+    uint64_t *totals;       // [kTotalsBuffers][kDigitBins]
     uint64_t *fine;         // [kFineBins]
     int64_t *eq;            // [M]
     int64_t *gt1;           // [M]
     uint64_t *cand;         // [cand_capacity]
 };
 
-struct PruneOffsets { int64_t total, fine, eq, gt1, cand, bytes; };
+struct PruneOffsets { int64_t info, totals, fine, eq, gt1, cand, bytes; };
 
 PruneOffsets prune_offsets(int64_t M, int64_t N) {
     PruneOffsets o;
-    o.total = align256(int64_t(sizeof(PruneState)));
-    o.fine = o.total + align256((int64_t(1) << kMaxDigitBits) * 8);
+    o.info = align256(2 * int64_t(sizeof(PruneState)));
+    o.totals = o.info + align256(int64_t(sizeof(SplitInfo)));
+    o.fine = o.totals + align256(int64_t(kTotalsBuffers) * kDigitBins * 8);
     o.eq = o.fine + align256(int64_t(kFineBins) * 8);
     o.gt1 = o.eq + align256(M * int64_t(sizeof(int64_t)));
     o.cand = o.gt1 + align256(M * int64_t(sizeof(int64_t)));
@@ -930,8 +1027,9 @@ PruneWorkspace prune_workspace(int64_t M, int64_t N, void *base) {
     const PruneOffsets o = prune_offsets(M, N);
     char *c = static_cast<char *>(base);
     PruneWorkspace w;
-    w.st = reinterpret_cast<PruneState *>(c);
-    w.total = reinterpret_cast<uint64_t *>(c + o.total);
+    w.slots = reinterpret_cast<PruneState *>(c);
+    w.info = reinterpret_cast<SplitInfo *>(c + o.info);
+    w.totals = reinterpret_cast<uint64_t *>(c + o.totals);
     w.fine = reinterpret_cast<uint64_t *>(c + o.fine);
     w.eq = reinterpret_cast<int64_t *>(c + o.eq);
     w.gt1 = reinterpret_cast<int64_t *>(c + o.gt1);
@@ -945,80 +1043,89 @@ hipError_t launch_prune_t(int64_t M, int64_t N, const void *Wv, int64_t ldw, int
     using Tr = PruneTraits<Bits>;
     const Bits *W = static_cast<const Bits *>(Wv);
     const PruneWorkspace w = prune_workspace(M, N, workspace);
-    PruneState *st = w.st;
-    int64_t *eq = w.eq;
-    auto *total_u = reinterpret_cast<unsigned long long *>(w.total);
+    auto *totals_u = reinterpret_cast<unsigned long long *>(w.totals);
     auto *fine_u = reinterpret_cast<unsigned long long *>(w.fine);
     const PrunePartition part = prune_partition<Bits>(M, N);
     const int groups = part.groups;
     const int64_t per_wave = part.per_wave;
-    const int64_t init_n = M > kFineBins ? M : kFineBins;
+    constexpr int64_t kInitMin = int64_t(kTotalsBuffers) * kDigitBins > kFineBins
+                                     ? int64_t(kTotalsBuffers) * kDigitBins
+                                     : int64_t(kFineBins);
+    const int64_t init_n = M > kInitMin ? M : kInitMin;
     const int64_t init_blocks = (init_n + 255) / 256;
     if (init_blocks > 0x7FFFFFFF) return hipErrorInvalidConfiguration;
     hipLaunchKernelGGL(prune_init_kernel, dim3(unsigned(init_blocks)), dim3(256), 0, s, M, k,
-                       int(Tr::KEY_BITS), st, counts, eq, w.gt1, w.total, w.fine);
+                       int(Tr::KEY_BITS), w.slots, w.info, counts, w.eq, w.gt1, w.totals,
+                       w.fine);
     if (k == 0) return hipGetLastError();               // nothing kept: counts stay 0
 
     const bool aligned = (reinterpret_cast<uintptr_t>(W) % 16 == 0) &&
                          ((ldw * int64_t(sizeof(Bits))) % 16 == 0);
     // digits of the whole key (3 for fp32, 2 for fp16): every way through the
-    // passes needs at most that many after the first digit's pass or the split
+    // passes needs at most that many after the split
     constexpr int passes = digit_passes(Tr::KEY_BITS);
+    static_assert(kBufPass0 + passes <= kTotalsBuffers, "a totals buffer per pass");
     const uint64_t cap = uint64_t(cand_room);
     auto *gt1_u = reinterpret_cast<unsigned long long *>(w.gt1);
     // more predicted candidates than this and the split pass takes the first digit
     const uint64_t cand_limit =
         std::min<uint64_t>(cap / 2, uint64_t(groups) * uint64_t(kSplitLds) / 2);
-    auto hist = [&](int role) {
+    int rd = 0;                                         // the state slot the next kernel reads
+    auto hist = [&](int buf, int role) {
         if (aligned)
             hipLaunchKernelGGL((prune_hist_kernel<Bits, true>), dim3(groups), dim3(kHistThreads),
-                               0, s, W, ldw, M, N, per_wave, per_wave, st, total_u, w.cand, role,
-                               k, cap);
+                               0, s, W, ldw, M, N, per_wave, w.slots, w.info, totals_u, w.cand,
+                               rd, buf, role, k, cap);
         else
             hipLaunchKernelGGL((prune_hist_kernel<Bits, false>), dim3(groups),
-                               dim3(kHistThreads), 0, s, W, ldw, M, N, per_wave, per_wave, st,
-                               total_u, w.cand, role, k, cap);
+                               dim3(kHistThreads), 0, s, W, ldw, M, N, per_wave, w.slots, w.info,
+                               totals_u, w.cand, rd, buf, role, k, cap);
+        rd ^= 1;
     };
     // the split pass pays for its extra launches only on large matrices: below
     // kSplitMinBytes of W every pass streams W
     if (M * N * int64_t(sizeof(Bits)) >= kSplitMinBytes) {
         // the sample (ranges of kSampleChunk vectors per lane, one out of about every
         // kSampleEvery, the stride drifting by an odd number of vectors so that it
-        // does not follow power-of-two rows) proposes the bracket, in as many
-        // workgroups as it has ranges for; the split pass then reads W once
+        // does not follow power-of-two rows), in as many workgroups as it has ranges
+        // for; the split pass then reads W once
         const int64_t chunk = kSampleChunk * int64_t(kWave) * Tr::VEC;
         const int64_t range_stride = kSampleEvery * chunk + kSampleDrift * Tr::VEC;
         const int64_t ranges = (M * padded_n<Bits>(N) + range_stride - 1) / range_stride;
         const int64_t sample_groups =
             std::min<int64_t>(kSampleGroups, (ranges + kHistWaves - 1) / kHistWaves);
         const dim3 sgrid(unsigned(std::max<int64_t>(1, sample_groups)));
+        unsigned long long *coarse = totals_u + size_t(kBufSample) * kDigitBins;
         if (aligned)
             hipLaunchKernelGGL((prune_sample_kernel<Bits, true>), sgrid, dim3(kHistThreads), 0, s,
-                               W, ldw, M, N, chunk, range_stride, st, total_u, fine_u, k,
-                               cand_limit);
+                               W, ldw, M, N, chunk, range_stride, coarse, fine_u);
         else
             hipLaunchKernelGGL((prune_sample_kernel<Bits, false>), sgrid, dim3(kHistThreads), 0,
-                               s, W, ldw, M, N, chunk, range_stride, st, total_u, fine_u, k,
-                               cand_limit);
+                               s, W, ldw, M, N, chunk, range_stride, coarse, fine_u);
         if (aligned)
             hipLaunchKernelGGL((prune_split_kernel<Bits, true>), dim3(groups), dim3(kHistThreads),
-                               0, s, W, ldw, M, N, per_wave, st, gt1_u, w.cand, cap, total_u);
+                               0, s, W, ldw, M, N, per_wave, w.slots, w.info, totals_u, fine_u,
+                               gt1_u, w.cand, cap, rd, kBufSplit, k, cand_limit);
         else
             hipLaunchKernelGGL((prune_split_kernel<Bits, false>), dim3(groups),
-                               dim3(kHistThreads), 0, s, W, ldw, M, N, per_wave, st, gt1_u,
-                               w.cand, cap, total_u);
-        for (int p = 0; p < passes; ++p) hist(p == 0 ? kRoleAfterSplit : kRoleNext);
+                               dim3(kHistThreads), 0, s, W, ldw, M, N, per_wave, w.slots, w.info,
+                               totals_u, fine_u, gt1_u, w.cand, cap, rd, kBufSplit, k,
+                               cand_limit);
+        rd ^= 1;
+        for (int p = 0; p < passes; ++p) hist(kBufPass0 + p, p == 0 ? kRoleAfterSplit : kRoleNext);
     } else {
-        for (int p = 0; p < passes; ++p) hist(kRoleNext);
+        for (int p = 0; p < passes; ++p) hist(kBufPass0 + p, kRoleNext);
     }
     auto *gt_u = reinterpret_cast<unsigned long long *>(counts);
-    auto *eq_u = reinterpret_cast<unsigned long long *>(eq);
+    auto *eq_u = reinterpret_cast<unsigned long long *>(w.eq);
     if (aligned)
         hipLaunchKernelGGL((prune_count_kernel<Bits, true>), dim3(groups), dim3(kHistThreads), 0,
-                           s, W, ldw, M, N, per_wave, st, gt_u, eq_u, w.cand, gt1_u, cap);
+                           s, W, ldw, M, N, per_wave, w.slots, w.info, totals_u, gt_u, eq_u,
+                           w.cand, gt1_u, cap, rd);
     else
         hipLaunchKernelGGL((prune_count_kernel<Bits, false>), dim3(groups), dim3(kHistThreads), 0,
-                           s, W, ldw, M, N, per_wave, st, gt_u, eq_u, w.cand, gt1_u, cap);
+                           s, W, ldw, M, N, per_wave, w.slots, w.info, totals_u, gt_u, eq_u,
+                           w.cand, gt1_u, cap, rd);
     return hipGetLastError();
 }
 
