@@ -230,6 +230,76 @@ __device__ __forceinline__ void for_each_round(const Bits *__restrict__ W, int64
     }
 }
 
+// As for_each_round for 16-byte aligned rows, with each round handed over in two
+// halves, half(keys, valid, first) (first: the index of keys[0] in the round), and
+// the next round's loads issued half by half into the registers the current half's
+// keys have just left: half of each round's memory latency overlaps the previous
+// round's work without a second set of registers.  The loads stay unconditional
+// (a round past the piece's end reloads the piece's first vectors and keeps
+// nothing), so the compiler waits for exactly the loads a half needs.
+template <typename Bits, typename U, typename H>
+__device__ __forceinline__ void for_each_round_halves(const Bits *__restrict__ W, int64_t ldw,
+                                                      int64_t M, int64_t N, int64_t per_wave,
+                                                      U &&on_unit, H &&half) {
+    using Tr = PruneTraits<Bits>;
+    constexpr int VEC = Tr::VEC;
+    constexpr int kUnroll = Tr::UNROLL;
+    constexpr int HU = kUnroll / 2;                     // vectors per half
+    static_assert(kUnroll % 2 == 0, "two halves per round");
+    constexpr int64_t STEP = round_width<Bits>();
+    const int lane = int(threadIdx.x) & (kWave - 1);
+    const int wave = __builtin_amdgcn_readfirstlane(int(threadIdx.x) / kWave);
+    const int64_t gw = int64_t(blockIdx.x) * (blockDim.x / kWave) + wave;
+    const int64_t tw = int64_t(gridDim.x) * (blockDim.x / kWave);
+    const int64_t Np = padded_n<Bits>(N);
+    const int64_t total = M * Np;
+    typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+    for (int64_t a = gw * per_wave; a < total; a += tw * per_wave) {   // wave-uniform
+        const int64_t b = a + per_wave < total ? a + per_wave : total;
+        int64_t r = a / Np;
+        int64_t c = a - r * Np;
+        for (int64_t at = a; at < b; ++r, c = 0) {
+            const int64_t c_piece = c + (b - at) < Np ? c + (b - at) : Np;
+            const int64_t c_end = c_piece < N ? c_piece : N;
+            at += c_piece - c;
+            const Bits *row = W + r * ldw;
+            on_unit(r);
+            if (c >= c_end) continue;
+            PVec<Bits, VEC> v[kUnroll];
+            uint32_t valid[kUnroll];                    // bit e: element e is inside the row
+            // rows are whole 16-byte vectors apart, so the vector holding a row's last
+            // element lies inside the row's stride
+            auto load = [&](int q, int64_t c0) {
+                const int64_t cc = c0 + int64_t(q) * kWave * VEC + int64_t(lane) * VEC;
+                const int64_t left = c_end - cc;
+                const u32x4 t = __builtin_nontemporal_load(
+                    reinterpret_cast<const u32x4 *>(row + (left > 0 ? cc : c)));
+                v[q] = __builtin_bit_cast(PVec<Bits, VEC>, t);
+                valid[q] = left >= VEC ? (1u << VEC) - 1u : (left > 0 ? (1u << left) - 1u : 0u);
+            };
+#pragma unroll
+            for (int q = 0; q < kUnroll; ++q) load(q, c);
+            for (int64_t c0 = c; c0 < c_end; c0 += STEP) {
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    uint32_t keys[HU * VEC];
+                    uint32_t mask = 0;
+#pragma unroll
+                    for (int q = 0; q < HU; ++q) {
+#pragma unroll
+                        for (int e = 0; e < VEC; ++e)
+                            keys[q * VEC + e] = uint32_t(v[h * HU + q].e[e]) & Tr::MAG;
+                        mask |= valid[h * HU + q] << (q * VEC);
+                    }
+#pragma unroll
+                    for (int q = 0; q < HU; ++q) load(h * HU + q, c0 + STEP);
+                    half(keys, mask, h * HU * VEC);
+                }
+            }
+        }
+    }
+}
+
 // As for_each_round, with f(key) for every element inside the row (per lane).
 template <typename Bits, bool ALIGNED, typename U, typename F>
 __device__ __forceinline__ void for_each_key(const Bits *__restrict__ W, int64_t ldw, int64_t M,
@@ -717,45 +787,57 @@ __global__ __launch_bounds__(kHistThreads) void prune_split_kernel(
 #pragma unroll
         for (int q = 0; q < U; ++q) asm volatile("" ::"v"(warm[q]));   // used (and done) here
     }
-    for_each_round<Bits, ALIGNED>(
-        W, ldw, M, N, per_wave, per_wave,
-        [&](int64_t r) {
-            if (r != cur) {
-                flush();
-                cur = r;
-            }
-        },
-        [&](const uint32_t (&keys)[K], uint32_t mask) {
-            if (!single) {                              // uniform: the first digit's histogram
+    auto on_unit = [&](int64_t r) {
+        if (r != cur) {
+            flush();
+            cur = r;
+        }
+    };
+    // the keys of a round (or of half a round), KN of them
+    auto process = [&](const auto &keys, uint32_t mask) {
+        constexpr int KN = int(std::extent<std::remove_reference_t<decltype(keys)>>::value);
+        if (!single) {                                  // uniform: the first digit's histogram
 #pragma unroll
-                for (int j = 0; j < K; ++j)
-                    if ((mask >> j) & 1u) atomicAdd(&hmine[keys[j] >> hist_shift], 1u);
-                return;
-            }
-            // branch-free over the round's keys: the count above the bracket and a
-            // mask of the candidates; then one ballot per key slot, and each lane
-            // places its own candidates by the set bits below it in the ballot
-            uint32_t cm = 0;
+            for (int j = 0; j < KN; ++j)
+                if ((mask >> j) & 1u) atomicAdd(&hmine[keys[j] >> hist_shift], 1u);
+            return;
+        }
+        // branch-free over the keys: the count above the bracket and a mask of the
+        // candidates; then one ballot per key slot, and each lane places its own
+        // candidates by the set bits below it in the ballot
+        uint32_t cm = 0;
 #pragma unroll
-            for (int j = 0; j < K; ++j) {
-                const uint32_t top = keys[j] >> first_shift;
-                const bool in = (mask >> j) & 1u;
-                n_gt += (in && top > dhi) ? 1u : 0u;
-                cm |= (in && top >= dlo && top <= dhi) ? (1u << j) : 0u;
-            }
+        for (int j = 0; j < KN; ++j) {
+            const uint32_t top = keys[j] >> first_shift;
+            const bool in = (mask >> j) & 1u;
+            n_gt += (in && top > dhi) ? 1u : 0u;
+            cm |= (in && top >= dlo && top <= dhi) ? (1u << j) : 0u;
+        }
 #pragma unroll
-            for (int j = 0; j < K; ++j) {
-                const uint64_t bal = __ballot((cm >> j) & 1u);
-                if (bal) {                              // wave-uniform
-                    const uint32_t p = wn + __builtin_amdgcn_mbcnt_hi(
-                                                 uint32_t(bal >> 32),
-                                                 __builtin_amdgcn_mbcnt_lo(uint32_t(bal), 0u));
-                    if (((cm >> j) & 1u) && p < uint32_t(kWaveRoom))
-                        mine[p] = (uint64_t(cur) << 32) | keys[j];
-                    wn += uint32_t(__popcll(bal));
-                }
+        for (int j = 0; j < KN; ++j) {
+            const uint64_t bal = __ballot((cm >> j) & 1u);
+            if (bal) {                                  // wave-uniform
+                const uint32_t p = wn + __builtin_amdgcn_mbcnt_hi(
+                                             uint32_t(bal >> 32),
+                                             __builtin_amdgcn_mbcnt_lo(uint32_t(bal), 0u));
+                if (((cm >> j) & 1u) && p < uint32_t(kWaveRoom))
+                    mine[p] = (uint64_t(cur) << 32) | keys[j];
+                wn += uint32_t(__popcll(bal));
             }
-        });
+        }
+    };
+    if constexpr (ALIGNED) {
+        constexpr int KH = K / 2;
+        for_each_round_halves<Bits>(W, ldw, M, N, per_wave, on_unit,
+                                    [&](const uint32_t (&keys)[KH], uint32_t mask, int) {
+                                        process(keys, mask);
+                                    });
+    } else {
+        for_each_round<Bits, false>(W, ldw, M, N, per_wave, per_wave, on_unit,
+                                    [&](const uint32_t (&keys)[K], uint32_t mask) {
+                                        process(keys, mask);
+                                    });
+    }
     if (!single) {                                      // uniform
         __syncthreads();
         unsigned long long *total = totals + size_t(buf) * kDigitBins;
