@@ -237,3 +237,17 @@ def test_split_pass_paths(darb, case):
     k = int(ties.sum()) // 2 + 7
     say(f"split pass {case}: {int(ties.sum())} keys equal to the threshold, k = {k}")
     assert np.array_equal(gpu_counts(darb, dev(W), k), oracle.prune_counts(W, k))
+
+
+@pytest.mark.parametrize("keep", [0.10, 0.30])
+def test_gaussian_weights_at_split_size(darb, keep):
+    # 64 MiB of i.i.d. Gaussian fp32 weights takes the sample and split path.  At
+    # 10 % keep the threshold's 11-bit leading digit holds about 3 % of W, more than
+    # half the candidate room: the sample's 14-bit bracket is what keeps the
+    # candidates few (and at 30 % the density at the threshold is higher still).
+    # Which path ran is not visible here; the counts must be the oracle's either way.
+    rng = np.random.default_rng(11)
+    W = (rng.standard_normal((4096, 4096)) * 0.05).astype(np.float32)
+    k = int(keep * W.size)
+    say(f"gaussian 4096x4096 fp32, keep {keep}, k = {k}")
+    assert np.array_equal(gpu_counts(darb, dev(W), k), oracle.prune_counts(W, k))
