@@ -302,7 +302,7 @@ int darb_prune_counts(int64_t M, int64_t N, int wdtype, const void *W, int64_t l
  * is a fixed 8 MiB array in the library's device code, one per device, held until
  * the process ends; the first call on a device looks up that device's copy (no
  * allocation).  The array holds the per-row counters (16 bytes per row), so M is
- * limited to 478 176 rows (larger M: DARB_E_INVALID, naming the limit);
+ * limited to 483 296 rows (larger M: DARB_E_INVALID, naming the limit);
  * the rest is candidate room, and a matrix whose candidates do not fit takes more
  * passes over W with the same result.  Every call on a device shares its array and
  * leaves its contents there (each call clears what must start at zero), so calls

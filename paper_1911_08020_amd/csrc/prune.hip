@@ -93,11 +93,12 @@ struct SplitInfo {
     uint32_t pad[3];
 };
 
-// Totals buffers, one per histogram of a call: the sample's coarse digit, the
-// split pass's first digit (when it takes one), then one per pass after it.
+// Totals buffers, one per digit histogram of a call: the split pass's first digit
+// (when it takes one), then one per pass after it.  (The sample's totals are kept
+// apart, per fine digit.)
 constexpr int kDigitBins = 1 << kMaxDigitBits;
-constexpr int kTotalsBuffers = 5;
-constexpr int kBufSample = 0, kBufSplit = 1, kBufPass0 = 2;
+constexpr int kTotalsBuffers = 4;
+constexpr int kBufSplit = 0, kBufPass0 = 1;
 
 // What one histogram pass selects: the keys with (key - base) >> hi == prefix,
 // by their next digit, for the k_rem-th largest; from the candidates or from W.
@@ -412,32 +413,39 @@ __device__ __forceinline__ Pass resolve(const PruneState *__restrict__ S,
 // holds the k-th largest key's digit up to six standard deviations of the sample
 // count (a binomial) plus 8 keys: keys above dhi number at most f*k - margin in the
 // sample, keys at or above dlo at least f*k + margin.  `single` unless the
-// bracket's predicted candidates exceed cand_limit.  The sample's totals are kept
-// per coarse digit (the top CB bits, totals buffer kBufSample) and per fine digit:
-// the coarse totals place the two ends within a coarse digit each, and only those
-// digits' fine totals are read.  Every workgroup of the split pass computes it,
-// thread t from the coarse totals a, b of digits CB-1-2t and CB-2-2t (loaded by the
-// caller, so that their latency overlaps other loads); results in L.d[0] (dlo),
-// L.d[1] (dhi), L.d[2] (single).
+// bracket's predicted candidates exceed cand_limit.  Every workgroup of the split
+// pass computes it.  Thread t holds the sample's fine totals under the coarse
+// digits (the top CB bits) c0 = 2^CB-1-2t and c1 = c0-1, f[0..R) for c1 and
+// f[R..2R) for c0, loaded by the caller in one round trip; the coarse totals are
+// their sums, and the threads that hold the two ends' coarse digits find the ends
+// among their fine digits.  Results in L.d[0] (dlo), L.d[1] (dhi), L.d[2] (single).
 template <int CB_BITS, int FB_BITS>
-__device__ __forceinline__ void bracket(uint64_t a, uint64_t b,
-                                        const unsigned long long *__restrict__ fine,
+__device__ __forceinline__ void bracket(const uint32_t (&f)[2 << (FB_BITS - CB_BITS)],
                                         int64_t total_keys, int64_t k, uint64_t cand_limit,
                                         ResolveLds &L) {
     constexpr int CB = 1 << CB_BITS;
     constexpr int R = 1 << (FB_BITS - CB_BITS);         // fine digits per coarse digit
-    constexpr uint32_t kNone = 0xFFFFFFFFu;
-    static_assert(2 * R <= kHistThreads && CB <= kDigitBins, "bracket scratch");
-    if (threadIdx.x == 0) {
-        L.d[0] = kNone;                                 // coarse digit of dhi
-        L.d[1] = kNone;                                 // coarse digit of dlo
+    constexpr uint32_t kTop = (1u << FB_BITS) - 1;
+    static_assert(CB <= 2 * kHistThreads, "two coarse digits per thread");
+    const int c0 = CB - 1 - 2 * int(threadIdx.x), c1 = c0 - 1;
+    uint64_t a = 0, b = 0;                              // the coarse totals of c0, c1
+#pragma unroll
+    for (int j = 0; j < R; ++j) {
+        b += f[j];
+        a += f[R + j];
     }
-    const int d0 = CB - 1 - 2 * int(threadIdx.x), d1 = d0 - 1;
+    if (threadIdx.x == 0) {                             // an end no digit qualifies for
+        L.d[0] = 0;                                     // dlo: the whole range
+        L.d[1] = kTop;                                  // dhi: the whole range
+        L.v[1] = 0;                                     // sample keys above dhi
+    }
     const uint64_t incl = block_inclusive_scan(a + b, L.wave_tot);
     const uint64_t excl = incl - a - b;
     if (threadIdx.x == kHistThreads - 1) L.v[4] = incl;
     __syncthreads();
     const uint64_t n_s = L.v[4];
+    if (threadIdx.x == 0) L.v[0] = n_s;                 // sample keys at or above dlo
+    __syncthreads();
     const double q = double(k) / double(total_keys);
     const double ks = q * double(n_s);
     const double margin = 6.0 * sqrt(ks * (1.0 - q)) + 8.0;
@@ -445,71 +453,52 @@ __device__ __forceinline__ void bracket(uint64_t a, uint64_t b,
     // digit d has `above` keys with a larger digit and `above + c` at or above it,
     // both non-increasing in d: dhi is the one digit with above <= lo < above + c
     // (or digit 0 with above <= lo), dlo the one with above < hi <= above + c (or
-    // the top digit with above + c >= hi); first among the coarse digits
-    auto coarse_end = [&](int d, uint64_t above, uint64_t c) {
-        if (d < 0) return;
-        const double ab = double(above), at = double(above + c);
-        if (ab <= lo && (d == 0 || at > lo)) {
-            L.d[0] = uint32_t(d);
-            L.v[0] = above;
+    // the top digit with above + c >= hi); first among the coarse digits, then among
+    // the fine digits of the coarse digit found (its whole range if they disagree)
+    auto ends = [&](int c, uint64_t above, uint64_t cnt, int fo) {
+        if (c < 0) return;
+        const double ab = double(above), at = double(above + cnt);
+        if (ab <= lo && (c == 0 || at > lo)) {
+            uint32_t dhi = uint32_t(c) * R + R - 1;
+            uint64_t above_hi = above, x = above;
+            for (int j = R - 1; j >= 0; --j) {
+                const uint32_t fd = uint32_t(c) * R + uint32_t(j);
+                if (double(x) <= lo && (fd == 0 || double(x + f[fo + j]) > lo)) {
+                    dhi = fd;
+                    above_hi = x;
+                    break;
+                }
+                x += f[fo + j];
+            }
+            L.d[1] = dhi;
+            L.v[1] = above_hi;
         }
-        if (at >= hi && (d == CB - 1 || ab < hi)) {
-            L.d[1] = uint32_t(d);
-            L.v[2] = above;
-            L.v[3] = c;
+        if (at >= hi && (c == CB - 1 || ab < hi)) {
+            uint32_t dlo = uint32_t(c) * R;
+            uint64_t at_lo = above + cnt, x = above;
+            for (int j = R - 1; j >= 0; --j) {
+                if (double(x + f[fo + j]) >= hi) {
+                    dlo = uint32_t(c) * R + uint32_t(j);
+                    at_lo = x + f[fo + j];
+                    break;
+                }
+                x += f[fo + j];
+            }
+            L.d[0] = dlo;
+            L.v[0] = at_lo;
         }
     };
-    coarse_end(d0, excl, a);
-    coarse_end(d1, excl + a, b);
-    __syncthreads();
-    const uint32_t chi = L.d[0], clo = L.d[1];
-    // then among the fine digits of those two coarse digits
-    uint64_t *f = L.tot;
-    if (threadIdx.x < 2 * R) {
-        const uint32_t c = threadIdx.x < R ? chi : clo;
-        f[threadIdx.x] = c == kNone ? 0ull : fine[c * R + (threadIdx.x & (R - 1))];
-    }
+    ends(c0, excl, a, R);
+    ends(c1, excl + a, b, 0);
     __syncthreads();
     if (threadIdx.x == 0) {
-        constexpr uint32_t kTop = (1u << FB_BITS) - 1;
-        // defaults: the whole range at an end no digit qualifies for, the whole
-        // coarse digit if its fine totals disagree with it
-        uint32_t dhi = kTop, dlo = 0;
-        uint64_t above_hi = 0, at_lo = n_s;
-        if (chi != kNone) {
-            dhi = chi * R + R - 1;
-            above_hi = L.v[0];
-            uint64_t ab = L.v[0];
-            for (int j = R - 1; j >= 0; --j) {
-                const uint32_t fd = chi * R + uint32_t(j);
-                if (double(ab) <= lo && (fd == 0 || double(ab + f[j]) > lo)) {
-                    dhi = fd;
-                    above_hi = ab;
-                    break;
-                }
-                ab += f[j];
-            }
-        }
-        if (clo != kNone) {
-            dlo = clo * R;
-            at_lo = L.v[2] + L.v[3];
-            uint64_t ab = L.v[2];
-            for (int j = R - 1; j >= 0; --j) {
-                if (double(ab + f[R + j]) >= hi) {
-                    dlo = clo * R + uint32_t(j);
-                    at_lo = ab + f[R + j];
-                    break;
-                }
-                ab += f[R + j];
-            }
-        }
         // predicted candidates: the bracket's sample keys scaled by 1/f
+        const uint32_t dlo = L.d[0], dhi = L.d[1];
+        const uint64_t at_lo = L.v[0], above_hi = L.v[1];
         const bool ok = dlo <= dhi && at_lo >= above_hi;
         const uint64_t in_all = ok ? at_lo - above_hi : 0;
         const bool fits = ok && n_s > 0 && double(in_all) * double(total_keys) <=
                                                double(cand_limit) * double(n_s);
-        L.d[0] = dlo;
-        L.d[1] = dhi;
         L.d[2] = fits ? 1u : 0u;
     }
     __syncthreads();
@@ -654,17 +643,14 @@ __global__ __launch_bounds__(kHistThreads) void prune_hist_kernel(
 }
 
 // The sample: the histogram of the keys' first SAMPLE_BITS bits over ranges of
-// chunk elements range_stride apart (one range per wave), added into `fine`, and
-// of their first digit_width(KEY_BITS) bits, added into `coarse`.
+// chunk elements range_stride apart (one range per wave), added into `fine`
+// (32-bit totals: only the bracket's width depends on them).
 template <typename Bits, bool ALIGNED>
 __global__ __launch_bounds__(kHistThreads) void prune_sample_kernel(
     const Bits *__restrict__ W, int64_t ldw, int64_t M, int64_t N, int64_t chunk,
-    int64_t range_stride, unsigned long long *__restrict__ coarse,
-    unsigned long long *__restrict__ fine) {
+    int64_t range_stride, uint32_t *__restrict__ fine) {
     constexpr int KB = PruneTraits<Bits>::KEY_BITS;
     constexpr int FB = PruneTraits<Bits>::SAMPLE_BITS;
-    constexpr int CB = digit_width(KB);
-    constexpr int R = 1 << (FB - CB);
     constexpr uint32_t shift = uint32_t(KB - FB);
     __shared__ uint32_t hist[1 << FB];
     for (int i = int(threadIdx.x); i < (1 << FB); i += kHistThreads) hist[i] = 0;
@@ -674,19 +660,13 @@ __global__ __launch_bounds__(kHistThreads) void prune_sample_kernel(
     __syncthreads();
     for (int b = int(threadIdx.x); b < (1 << FB); b += kHistThreads) {
         const uint32_t v = hist[b];
-        if (v) atomicAdd(&fine[b], (unsigned long long)v);
-    }
-    for (int c = int(threadIdx.x); c < (1 << CB); c += kHistThreads) {
-        uint32_t v = 0;
-#pragma unroll
-        for (int j = 0; j < R; ++j) v += hist[c * R + j];
-        if (v) atomicAdd(&coarse[c], (unsigned long long)v);
+        if (v) atomicAdd(&fine[b], v);
     }
 }
 
 // The split pass.  Every workgroup computes the sample's bracket [dlo, dhi] of fine
 // first digits while the lines of its first round of W are on their way to the L2
-// (the coarse sample totals are requested first).  With `single`, per row the keys
+// (the sample's totals are requested first).  With `single`, per row the keys
 // with first digit > dhi go to gt1 (and their total to the split info's n_above)
 // and the keys inside the bracket are stored as (row << 32 | key) candidates; if a
 // wave's candidates overflow its LDS region or the workspace's room, the overflow
@@ -697,7 +677,7 @@ template <typename Bits, bool ALIGNED>
 __global__ __launch_bounds__(kHistThreads) void prune_split_kernel(
     const Bits *__restrict__ W, int64_t ldw, int64_t M, int64_t N, int64_t per_wave,
     PruneState *__restrict__ slots, SplitInfo *__restrict__ info,
-    unsigned long long *__restrict__ totals, const unsigned long long *__restrict__ fine,
+    unsigned long long *__restrict__ totals, const uint32_t *__restrict__ fine,
     unsigned long long *__restrict__ gt1, uint64_t *__restrict__ cand, uint64_t cap, int rd,
     int buf, int64_t k, uint64_t cand_limit) {
     constexpr int kStride = (1 << kMaxDigitBits) + 1;
@@ -712,10 +692,22 @@ __global__ __launch_bounds__(kHistThreads) void prune_split_kernel(
     __shared__ ResolveLds L;
     __shared__ uint32_t wave_n[kHistWaves];
     __shared__ uint64_t base;
-    // this thread's two coarse sample totals (digits (1<<CB)-1-2t and (1<<CB)-2-2t)
-    const unsigned long long *coarse = totals + size_t(kBufSample) * kDigitBins;
-    const int c0 = (1 << CB) - 1 - 2 * int(threadIdx.x), c1 = c0 - 1;
-    const uint64_t ca = c0 >= 0 ? coarse[c0] : 0, cb = c1 >= 0 ? coarse[c1] : 0;
+    // the sample's fine totals under this thread's two coarse digits
+    // ((1<<CB)-2-2t and (1<<CB)-1-2t: 2R consecutive totals, 16-byte loads)
+    constexpr int R = 1 << (FB - CB);
+    static_assert((2 * R) % 4 == 0, "whole 16-byte loads");
+    uint32_t ft[2 * R];
+    {
+        typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+        const int c1 = (1 << CB) - 2 - 2 * int(threadIdx.x);
+        const u32x4 *src = reinterpret_cast<const u32x4 *>(fine + (c1 >= 0 ? c1 : 0) * R);
+#pragma unroll
+        for (int i = 0; i < 2 * R / 4; ++i) {
+            const u32x4 v = src[i];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) ft[4 * i + e] = c1 >= 0 ? v[e] : 0u;
+        }
+    }
     asm volatile("" ::: "memory");                      // these loads go out first
     const int lane = int(threadIdx.x) & (kWave - 1);
     const int wave = __builtin_amdgcn_readfirstlane(int(threadIdx.x) / kWave);
@@ -726,7 +718,7 @@ __global__ __launch_bounds__(kHistThreads) void prune_split_kernel(
     // the bracket, the split info and the next state slot (and, without `single`,
     // the cleared histogram)
     auto hook = [&]() {
-        bracket<CB, FB>(ca, cb, fine, M * N, k, cand_limit, L);
+        bracket<CB, FB>(ft, M * N, k, cand_limit, L);
         dlo = L.d[0];
         dhi = L.d[1];
         single = L.d[2] != 0;                           // uniform
@@ -1019,7 +1011,7 @@ __global__ __launch_bounds__(256) void prune_init_kernel(int64_t M, int64_t k, i
                                                          PruneState *slots, SplitInfo *info,
                                                          int64_t *counts, int64_t *eq,
                                                          int64_t *gt1, uint64_t *totals,
-                                                         uint64_t *fine) {
+                                                         uint32_t *fine) {
     const int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x;
     if (i < M) {
         counts[i] = 0;
@@ -1085,7 +1077,7 @@ struct PruneWorkspace {
     PruneState *slots;      // [2]
     SplitInfo *info;
     uint64_t *totals;       // [kTotalsBuffers][kDigitBins]
-    uint64_t *fine;         // [kFineBins]
+    uint32_t *fine;         // [kFineBins]
     int64_t *eq;            // [M]
     int64_t *gt1;           // [M]
     uint64_t *cand;         // [cand_capacity]
@@ -1098,7 +1090,7 @@ PruneOffsets prune_offsets(int64_t M, int64_t N) {
     o.info = align256(2 * int64_t(sizeof(PruneState)));
     o.totals = o.info + align256(int64_t(sizeof(SplitInfo)));
     o.fine = o.totals + align256(int64_t(kTotalsBuffers) * kDigitBins * 8);
-    o.eq = o.fine + align256(int64_t(kFineBins) * 8);
+    o.eq = o.fine + align256(int64_t(kFineBins) * 4);
     o.gt1 = o.eq + align256(M * int64_t(sizeof(int64_t)));
     o.cand = o.gt1 + align256(M * int64_t(sizeof(int64_t)));
     o.bytes = o.cand + align256(cand_capacity(M, N) * int64_t(sizeof(uint64_t)));
@@ -1112,7 +1104,7 @@ PruneWorkspace prune_workspace(int64_t M, int64_t N, void *base) {
     w.slots = reinterpret_cast<PruneState *>(c);
     w.info = reinterpret_cast<SplitInfo *>(c + o.info);
     w.totals = reinterpret_cast<uint64_t *>(c + o.totals);
-    w.fine = reinterpret_cast<uint64_t *>(c + o.fine);
+    w.fine = reinterpret_cast<uint32_t *>(c + o.fine);
     w.eq = reinterpret_cast<int64_t *>(c + o.eq);
     w.gt1 = reinterpret_cast<int64_t *>(c + o.gt1);
     w.cand = reinterpret_cast<uint64_t *>(c + o.cand);
@@ -1126,7 +1118,6 @@ hipError_t launch_prune_t(int64_t M, int64_t N, const void *Wv, int64_t ldw, int
     const Bits *W = static_cast<const Bits *>(Wv);
     const PruneWorkspace w = prune_workspace(M, N, workspace);
     auto *totals_u = reinterpret_cast<unsigned long long *>(w.totals);
-    auto *fine_u = reinterpret_cast<unsigned long long *>(w.fine);
     const PrunePartition part = prune_partition<Bits>(M, N);
     const int groups = part.groups;
     const int64_t per_wave = part.per_wave;
@@ -1177,21 +1168,20 @@ hipError_t launch_prune_t(int64_t M, int64_t N, const void *Wv, int64_t ldw, int
         const int64_t sample_groups =
             std::min<int64_t>(kSampleGroups, (ranges + kHistWaves - 1) / kHistWaves);
         const dim3 sgrid(unsigned(std::max<int64_t>(1, sample_groups)));
-        unsigned long long *coarse = totals_u + size_t(kBufSample) * kDigitBins;
         if (aligned)
             hipLaunchKernelGGL((prune_sample_kernel<Bits, true>), sgrid, dim3(kHistThreads), 0, s,
-                               W, ldw, M, N, chunk, range_stride, coarse, fine_u);
+                               W, ldw, M, N, chunk, range_stride, w.fine);
         else
             hipLaunchKernelGGL((prune_sample_kernel<Bits, false>), sgrid, dim3(kHistThreads), 0,
-                               s, W, ldw, M, N, chunk, range_stride, coarse, fine_u);
+                               s, W, ldw, M, N, chunk, range_stride, w.fine);
         if (aligned)
             hipLaunchKernelGGL((prune_split_kernel<Bits, true>), dim3(groups), dim3(kHistThreads),
-                               0, s, W, ldw, M, N, per_wave, w.slots, w.info, totals_u, fine_u,
+                               0, s, W, ldw, M, N, per_wave, w.slots, w.info, totals_u, w.fine,
                                gt1_u, w.cand, cap, rd, kBufSplit, k, cand_limit);
         else
             hipLaunchKernelGGL((prune_split_kernel<Bits, false>), dim3(groups),
                                dim3(kHistThreads), 0, s, W, ldw, M, N, per_wave, w.slots, w.info,
-                               totals_u, fine_u, gt1_u, w.cand, cap, rd, kBufSplit, k,
+                               totals_u, w.fine, gt1_u, w.cand, cap, rd, kBufSplit, k,
                                cand_limit);
         rd ^= 1;
         for (int p = 0; p < passes; ++p) hist(kBufPass0 + p, p == 0 ? kRoleAfterSplit : kRoleNext);
