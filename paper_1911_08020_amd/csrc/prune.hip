@@ -11,41 +11,37 @@
 // counts the current digit of the keys that match the digits chosen so far (one
 // LDS histogram per workgroup, four interleaved copies so lanes with equal digits
 // rarely hit the same address; each workgroup then adds its non-zero bins into the
-// global totals), and the workgroup that finishes the pass last (a counter in the
-// state tells it) picks the digit where the count from the top reaches the
-// remaining K.  Finally, per row, the keys > t are counted and the keys == t taken
-// in flat order, which for row counts means rows in ascending order (by the count
-// pass's last workgroup).
+// pass's own totals buffer).  The next kernel picks the digit where the count from
+// the top reaches the remaining K: every one of its workgroups reads the totals
+// (the kernel boundary has made them visible) and chooses the same way, so no
+// workgroup waits for the others and no read-modify-write reads totals back.
+// Finally, per row, the keys > t are counted and the keys == t taken in flat
+// order, which for row counts means rows in ascending order (by the count pass's
+// last workgroup, only when some keys equal to t are not kept).
 //
 // From 64 MiB of W one pass streams all of W.  A sample of W (about 1/32) first
-// proposes a bracket of finer first digits (the key's top 14 bits for fp32, 11 for
-// fp16: a bracket as narrow as the sample's statistics allow, not the width of one
-// 11-bit digit) that holds the K-th key's, with a margin of six binomial standard
-// deviations.  The split pass then counts, per row, the keys whose first digit is
-// above the bracket (and their total, G) and copies the keys
-// inside it -- the candidates, typically about 1 % of W -- with their rows into the
-// workspace.  If G < K <= G + (candidates), the K-th key is a candidate: the
-// remaining selection runs over the candidates' keys relative to the bracket's
-// lowest key (17 + log2(bracket digits) bits for fp32), for the K - G-th
-// largest, and the final counts add the candidates above the threshold to the
-// per-row counts above the bracket.  Each workgroup gathers its candidates in LDS
-// and reserves room for them with one atomic; if a workgroup's LDS or the
-// workspace's candidate room overflows, or the K-th key lies outside the bracket,
-// the later passes stream W from the first digit on instead (the result is the
-// same).  When the sample predicts more candidates than half the room, the split
-// pass takes the exact first-digit histogram of W instead, and the later passes
-// stream W for the remaining digits.  The host launches as many passes after the
-// split as the digits of the key need; a pass that finds every bit chosen ends at
-// once.  Below 64 MiB of W there is no sample and no split: every pass streams W,
-// which there costs less than the extra launches.
-//
-// A pass over the candidates runs as many workgroups as they fill; only those take
-// part in finding the last workgroup (a device-wide counter that every
-// participating workgroup increments: 256 increments of one address cost about
-// 2 us on this chip, and so do 256 workgroups adding their bins into the same
-// totals).  The final count needs no last workgroup unless the threshold key has
-// ties that only some of its copies are kept for.
-// All state stays on the device; nothing returns to the host between passes.
+// histograms finer first digits (the key's top 14 bits for fp32, 11 for fp16), from
+// which the split pass's workgroups compute a bracket of them that holds the K-th
+// key's, with a margin of six binomial standard deviations: as narrow as the
+// sample's statistics allow, not the width of one 11-bit digit.  The split pass
+// then counts, per row, the keys whose first digit is above the bracket (and their
+// total, G) and copies the keys inside it -- the candidates, typically under 1 % of
+// W -- with their rows into the workspace (each wave fills its own LDS region, each
+// workgroup reserves room with one atomic).  If G < K <= G + (candidates), the K-th
+// key is a candidate: the remaining selection runs over the candidates' keys
+// relative to the bracket's lowest key (17 + log2(bracket digits) bits for fp32),
+// for the K - G-th largest, and the final counts add the candidates above the
+// threshold to the per-row counts above the bracket.  If a wave's region or the
+// workspace's room overflows, or the K-th key lies outside the bracket, the later
+// passes stream W from the first digit on instead (the result is the same).  When
+// the sample predicts more candidates than half the room, the split pass takes the
+// exact first-digit histogram of W instead, and the later passes stream W for the
+// remaining digits.  The host launches as many passes after the split as the
+// key's digits need; a pass with nothing left to choose hands the state on.  Below
+// 64 MiB of W there is no sample and no split: every pass streams W, which there
+// costs less than the extra launches.  A pass over the candidates runs only the
+// workgroups they fill.  All state stays on the device; nothing returns to the host
+// between passes.
 #include <algorithm>
 
 #include <mutex>
@@ -119,7 +115,7 @@ __host__ __device__ constexpr int digit_passes(int hi) {
 }
 
 constexpr int kSplitLds = 8192;                     // candidates a workgroup can hold
-constexpr int kWaveRoom = kSplitLds / (1024 / 64);  // of which each of its waves' own
+constexpr int kWaveRoom = kSplitLds / kHistWaves;   // of which each of its waves' own
 constexpr int64_t kSampleEvery = 32;                // the sample reads about 1/32 of W
 constexpr int64_t kSampleDrift = 37;                // vectors added to the sample stride
 constexpr int64_t kSampleChunk = 4;                 // vectors per lane in one sampled range
