@@ -1028,7 +1028,9 @@ __global__ __launch_bounds__(kSpmmThreads) void spmm_kernel(
 // columns, copies X[:, slab] (N x SC fp32, <= 128 KiB) into LDS once, then runs
 // every row of every group against it -- the X-row gathers hit LDS instead of L2.
 // The format is read by every workgroup, from L2.  One lane group of L lanes per
-// row, S weights per step, DEPTH steps of pairs per load round.
+// row; each lane loads a step's 16 (value, offset) pairs itself (offsets as bytes
+// or as packed words: the same sums either way), the next step's while this one
+// gathers.
 // ---------------------------------------------------------------------------------
 
 constexpr int kXldsThreads = 1024;
@@ -1063,9 +1065,9 @@ template <> struct Step16<__half> {
     }
 };
 
-template <typename Tw, int LGL>
+template <typename Tw, int LGL, bool PK>
 __global__ __launch_bounds__(kXldsThreads) void spmm_xlds_kernel(
-    const Tw *__restrict__ values, const uint8_t *__restrict__ offsets,
+    const Tw *__restrict__ values, const void *__restrict__ offs,
     const float *__restrict__ X, int64_t ldx, int64_t B, float *__restrict__ Y, int64_t ldy,
     const int32_t *__restrict__ perm, int N, BinTable bins, ProductSchedule sch) {
     constexpr int L = 1 << LGL;
@@ -1074,6 +1076,7 @@ __global__ __launch_bounds__(kXldsThreads) void spmm_xlds_kernel(
     constexpr int kStage = 8;                           // 16-byte staging loads in flight
     __shared__ float xs[kXldsFloats];
     using XL = XLoad<float, 4>;
+    using OV = Off<PK, kXldsStep>;                      // a step's 16 offsets
 
     const int64_t colbase = int64_t(blockIdx.x) * SC;
     // X[:, slab] -> xs[c * SC + j]; columns past B read as zero (4 divides B)
@@ -1116,26 +1119,29 @@ __global__ __launch_bounds__(kXldsThreads) void spmm_xlds_kernel(
         const int64_t rows = pick(bins.rows, g);
         const int64_t first_row = pick(bins.first_row, g);
         const int64_t first_elem = pick(bins.first_elem, g);
+        const GroupOffsets go = group_offsets(offs, bins, g);
         for (int64_t p0 = 0; p0 < rows; p0 += int64_t(kXldsWaves) * R) {
             const int64_t rl = p0 + wave * R + (lane >> LGL);
             const bool row_ok = rl < rows;
-            const int64_t e0 = first_elem + (row_ok ? rl : 0) * nblk;   // 16-aligned
+            const int64_t j0 = (row_ok ? rl : 0) * nblk;   // the row's first slot, 16-aligned
+            const int64_t e0 = first_elem + j0;
             float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
             // every lane of the row loads the step's 16 (value, offset) pairs itself
             // (equal addresses within one load merge), so no lane exchange is needed;
             // the next step's pairs load while this step gathers
             Step16<Tw> w = Step16<Tw>::load(values + e0);
-            u32x4 ob = *reinterpret_cast<const u32x4 *>(offsets + e0);
+            typename OV::Raw ob = OV::load(go, j0);
             for (int k0 = 0; k0 < nblk; k0 += kXldsStep) {
                 const int kn = k0 + kXldsStep < nblk ? k0 + kXldsStep : k0;
                 const Step16<Tw> w_next = Step16<Tw>::load(values + e0 + kn);
-                const u32x4 ob_next = *reinterpret_cast<const u32x4 *>(offsets + e0 + kn);
+                const typename OV::Raw ob_next = OV::load(go, j0 + kn);
+                const typename OV::Bits obits = OV::bits(ob, go);
                 static_for<0, kXldsStep / kXldsBatch>([&](auto bc) {
                     constexpr int b0 = decltype(bc)::value * kXldsBatch;
                     f32x4 xv[kXldsBatch];
                     static_for<0, kXldsBatch>([&](auto uc) {
                         constexpr int f = b0 + decltype(uc)::value;
-                        const int o = int((ob[f >> 2] >> (8 * (f & 3))) & 0xFFu);
+                        const int o = OV::field(obits, f, go);
                         int c = ((k0 + f) << lb) + o;
                         c = c < N ? c : N - 1;                // the encode gives c < N
                         xv[f - b0] = *reinterpret_cast<const f32x4 *>(xs + c * SC + xoff);
@@ -1468,7 +1474,7 @@ hipError_t launch_spmm_t(const darb_plan &p, const void *values, const uint8_t *
                          const uint32_t *packed, int64_t B, const void *X, int64_t ldx, float *Y,
                          int64_t ldy, const float *scales, hipStream_t st) {
     constexpr int CPL = 16 / int(sizeof(Tx));
-    if constexpr (std::is_same<Tx, float>::value && !PK && !kScaled<Tw>) {
+    if constexpr (std::is_same<Tx, float>::value && !kScaled<Tw>) {
         const bool vec = (reinterpret_cast<uintptr_t>(X) % 16 == 0) &&
                          ((ldx * int64_t(sizeof(Tx))) % 16 == 0) && (B % CPL == 0);
         int lgl = vec ? xlds_lgl(p, B) : -1;
@@ -1487,13 +1493,14 @@ hipError_t launch_spmm_t(const darb_plan &p, const void *values, const uint8_t *
             if (slabs > 0x7FFFFFFF) return hipErrorInvalidConfiguration;
             const Tw *v = static_cast<const Tw *>(values);
             const float *x = static_cast<const float *>(X);
+            const void *offs = offset_source(p, offsets, packed);
             if (lgl == 4)
-                hipLaunchKernelGGL((spmm_xlds_kernel<Tw, 4>), dim3(unsigned(slabs)),
-                                   dim3(kXldsThreads), 0, st, v, offsets, x, ldx, B, Y, ldy,
+                hipLaunchKernelGGL((spmm_xlds_kernel<Tw, 4, PK>), dim3(unsigned(slabs)),
+                                   dim3(kXldsThreads), 0, st, v, offs, x, ldx, B, Y, ldy,
                                    p.d_perm, int(p.N), p.bins, s);
             else
-                hipLaunchKernelGGL((spmm_xlds_kernel<Tw, 3>), dim3(unsigned(slabs)),
-                                   dim3(kXldsThreads), 0, st, v, offsets, x, ldx, B, Y, ldy,
+                hipLaunchKernelGGL((spmm_xlds_kernel<Tw, 3, PK>), dim3(unsigned(slabs)),
+                                   dim3(kXldsThreads), 0, st, v, offs, x, ldx, B, Y, ldy,
                                    p.d_perm, int(p.N), p.bins, s);
             return hipGetLastError();
         }

@@ -275,7 +275,8 @@ def test_large_shapes(darb, case):
 def test_spmm_wide_batch_short_rows(darb, case):
     # N small enough that a slab of X (32 or 64 columns) fits in LDS, B wide enough
     # for >= 128 slabs and rows in whole steps of 16 weights: the product stages X
-    # slabs in LDS (the last case has rows of ragged length and takes the general path)
+    # slabs in LDS (the last case has rows of ragged length and takes the general path);
+    # both offset forms take the same path
     N, B, wdt, bmax = case
     wdt = np.float32 if wdt == "f32" else np.float16
     say(f"wide-batch spmm N={N} B={B} w={wdt.__name__} b<={bmax}")
@@ -285,8 +286,12 @@ def test_spmm_wide_batch_short_rows(darb, case):
     d = rng.integers(0, N // 3, size=M) / N
     plan, lay, vals, offs = encode_both(darb, W, d, 0.1, 0, 1, bmax)
     X = rng.standard_normal((N, B)).astype(np.float32)
-    Y = host(plan.spmm(dev(vals), dev(offs), dev(X)))
+    vd, od, Xd = dev(vals), dev(offs), dev(X)
+    Y = host(plan.spmm(vd, od, Xd))
     check_product(Y, vals, offs, lay, X, wdt, f"wide B={B}")
+    # packed offsets take the same kernel and give the same bits
+    Yp = host(plan.spmm_packed(vd, plan.pack_offsets(od), Xd))
+    assert np.array_equal(Yp.view(np.uint32), Y.view(np.uint32)), "packed != byte form"
 
 
 def test_spmv_misaligned_values_uses_scalar_path(darb):
