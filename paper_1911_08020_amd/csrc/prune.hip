@@ -20,7 +20,9 @@
 // last workgroup, only when some keys equal to t are not kept).
 //
 // From 64 MiB of W one pass streams all of W.  A sample of W (about 1/32) first
-// histograms finer first digits (the key's top 14 bits for fp32, 11 for fp16), from
+// histograms finer first digits (the key's top 14 bits for fp32, 11 for fp16; the
+// same launch resets the state, and the count pass leaves the sample's histogram
+// at zero for the next call on the workspace), from
 // which the split pass's workgroups compute a bracket of them that holds the K-th
 // key's, with a margin of six binomial standard deviations: as narrow as the
 // sample's statistics allow, not the width of one 11-bit digit.  The split pass
@@ -38,8 +40,8 @@
 // exact first-digit histogram of W instead, and the later passes stream W for the
 // remaining digits.  The host launches as many passes after the split as the
 // key's digits need; a pass with nothing left to choose hands the state on.  Below
-// 64 MiB of W there is no sample and no split: every pass streams W, which there
-// costs less than the extra launches.  A pass over the candidates runs only the
+// 64 MiB of W there is no sample and no split: a reset launch, then every pass
+// streams W, which there costs less than the extra launches.  A pass over the candidates runs only the
 // workgroups they fill.  All state stays on the device; nothing returns to the host
 // between passes.
 #include <algorithm>
@@ -535,6 +537,18 @@ __device__ __forceinline__ Pass pass_after_split(const SplitInfo *__restrict__ I
     return P;
 }
 
+// The pass before any digit is chosen: prefix 0, every key bit left, base 0, K to find.
+__device__ __forceinline__ Pass first_pass(int key_bits, int64_t k) {
+    Pass P;
+    P.prefix = 0;
+    P.hi = uint32_t(key_bits);
+    P.base = 0;
+    P.cand = false;
+    P.k_rem = k;
+    P.n_last = 0;
+    return P;
+}
+
 // Write the state slot the next kernel reads: pass P, with its digit of `width`
 // bits pending in totals buffer `buf` (width 0: nothing pending).
 __device__ __forceinline__ void hand_on(PruneState *__restrict__ out, const Pass &P, int width,
@@ -638,18 +652,37 @@ __global__ __launch_bounds__(kHistThreads) void prune_hist_kernel(
     }
 }
 
-// The sample: the histogram of the keys' first SAMPLE_BITS bits over ranges of
-// chunk elements range_stride apart (one range per wave), added into `fine`
-// (32-bit totals: only the bracket's width depends on them).
+// The first kernel of a call that splits: the state reset (as prune_init_kernel,
+// except `fine`, which the previous call's count left at zero), then the sample:
+// the histogram of the keys' first SAMPLE_BITS bits over ranges of chunk elements
+// range_stride apart (one range per wave), added into `fine` (32-bit totals: only
+// the bracket depends on them, and a bracket that misses the K-th key, as one from
+// a workspace that held something else would, costs passes over W, not exactness).
 template <typename Bits, bool ALIGNED>
 __global__ __launch_bounds__(kHistThreads) void prune_sample_kernel(
     const Bits *__restrict__ W, int64_t ldw, int64_t M, int64_t N, int64_t chunk,
-    int64_t range_stride, uint32_t *__restrict__ fine) {
+    int64_t range_stride, uint32_t *__restrict__ fine, int64_t k, PruneState *slots,
+    SplitInfo *info, int64_t *counts, int64_t *eq, int64_t *gt1, uint64_t *totals) {
     constexpr int KB = PruneTraits<Bits>::KEY_BITS;
     constexpr int FB = PruneTraits<Bits>::SAMPLE_BITS;
     constexpr uint32_t shift = uint32_t(KB - FB);
     __shared__ uint32_t hist[1 << FB];
     for (int i = int(threadIdx.x); i < (1 << FB); i += kHistThreads) hist[i] = 0;
+    {
+        const int64_t stride = int64_t(gridDim.x) * kHistThreads;
+        const int64_t first = int64_t(blockIdx.x) * kHistThreads + threadIdx.x;
+        for (int64_t i = first; i < M; i += stride) {
+            counts[i] = 0;
+            eq[i] = 0;
+            gt1[i] = 0;
+        }
+        for (int64_t i = first; i < int64_t(kTotalsBuffers) * kDigitBins; i += stride)
+            totals[i] = 0;
+        if (first == 0) {
+            *info = SplitInfo{};
+            hand_on(slots, first_pass(KB, k), 0, 0);
+        }
+    }
     __syncthreads();
     for_each_key<Bits, ALIGNED>(W, ldw, M, N, chunk, range_stride, [](int64_t) {},
                                 [&](uint32_t key) { atomicAdd(&hist[key >> shift], 1u); });
@@ -722,14 +755,8 @@ __global__ __launch_bounds__(kHistThreads) void prune_split_kernel(
             info->single = single ? 1u : 0u;
             info->dlo = dlo;
             info->dhi = dhi;
-            Pass P0;                                    // nothing chosen yet
-            P0.prefix = 0;
-            P0.hi = KB;
-            P0.base = 0;
-            P0.cand = false;
-            P0.k_rem = k;
-            P0.n_last = 0;
-            hand_on(slots + (rd ^ 1), P0, single ? 0 : CB, buf);
+            // nothing chosen yet
+            hand_on(slots + (rd ^ 1), first_pass(KB, k), single ? 0 : CB, buf);
         }
         if (!single) {
             for (int i = int(threadIdx.x); i < kCopies * kStride; i += kHistThreads) hist[i] = 0;
@@ -909,7 +936,8 @@ __global__ __launch_bounds__(kHistThreads) void prune_count_kernel(
     const PruneState *__restrict__ slots, SplitInfo *__restrict__ info,
     const unsigned long long *__restrict__ totals, unsigned long long *__restrict__ gt,
     unsigned long long *__restrict__ eq, const uint64_t *__restrict__ cand,
-    const unsigned long long *__restrict__ gt1, uint64_t cap, int rd) {
+    const unsigned long long *__restrict__ gt1, uint64_t cap, int rd,
+    uint32_t *__restrict__ fine) {
     constexpr int KB = PruneTraits<Bits>::KEY_BITS;
     __shared__ ResolveLds L;
     __shared__ int64_t tile_total;
@@ -928,6 +956,8 @@ __global__ __launch_bounds__(kHistThreads) void prune_count_kernel(
     uint64_t c_next = from_cand && first < n ? cand[first] : 0;
     asm volatile("" ::: "memory");                      // the load goes out first
     const Pass P = resolve(slots + rd, totals, KB, L);
+    // the sample histogram is spent: zero it for the next call's sample
+    for (uint64_t i = first; i < uint64_t(kFineBins); i += stride) fine[i] = 0;
     const uint32_t t = P.base + P.prefix;
     // when every key equal to t is taken (always, without ties), they count with the
     // keys above t and nothing is left for the last workgroup
@@ -1018,14 +1048,7 @@ __global__ __launch_bounds__(256) void prune_init_kernel(int64_t M, int64_t k, i
     if (i < kFineBins) fine[i] = 0;
     if (i == 0) {
         *info = SplitInfo{};
-        Pass P0;
-        P0.prefix = 0;
-        P0.hi = uint32_t(key_bits);
-        P0.base = 0;
-        P0.cand = false;
-        P0.k_rem = k;
-        P0.n_last = 0;
-        hand_on(slots, P0, 0, 0);
+        hand_on(slots, first_pass(key_bits, k), 0, 0);
     }
 }
 
@@ -1123,9 +1146,13 @@ hipError_t launch_prune_t(int64_t M, int64_t N, const void *Wv, int64_t ldw, int
     const int64_t init_n = M > kInitMin ? M : kInitMin;
     const int64_t init_blocks = (init_n + 255) / 256;
     if (init_blocks > 0x7FFFFFFF) return hipErrorInvalidConfiguration;
-    hipLaunchKernelGGL(prune_init_kernel, dim3(unsigned(init_blocks)), dim3(256), 0, s, M, k,
-                       int(Tr::KEY_BITS), w.slots, w.info, counts, w.eq, w.gt1, w.totals,
-                       w.fine);
+    // the state reset: its own launch, unless the sample (the first kernel of a call
+    // that splits) does it
+    const bool split = k > 0 && M * N * int64_t(sizeof(Bits)) >= kSplitMinBytes;
+    if (!split)
+        hipLaunchKernelGGL(prune_init_kernel, dim3(unsigned(init_blocks)), dim3(256), 0, s, M,
+                           k, int(Tr::KEY_BITS), w.slots, w.info, counts, w.eq, w.gt1, w.totals,
+                           w.fine);
     if (k == 0) return hipGetLastError();               // nothing kept: counts stay 0
 
     const bool aligned = (reinterpret_cast<uintptr_t>(W) % 16 == 0) &&
@@ -1153,7 +1180,7 @@ hipError_t launch_prune_t(int64_t M, int64_t N, const void *Wv, int64_t ldw, int
     };
     // the split pass pays for its extra launches only on large matrices: below
     // kSplitMinBytes of W every pass streams W
-    if (M * N * int64_t(sizeof(Bits)) >= kSplitMinBytes) {
+    if (split) {
         // the sample (ranges of kSampleChunk vectors per lane, one out of about every
         // kSampleEvery, the stride drifting by an odd number of vectors so that it
         // does not follow power-of-two rows), in as many workgroups as it has ranges
@@ -1166,10 +1193,12 @@ hipError_t launch_prune_t(int64_t M, int64_t N, const void *Wv, int64_t ldw, int
         const dim3 sgrid(unsigned(std::max<int64_t>(1, sample_groups)));
         if (aligned)
             hipLaunchKernelGGL((prune_sample_kernel<Bits, true>), sgrid, dim3(kHistThreads), 0, s,
-                               W, ldw, M, N, chunk, range_stride, w.fine);
+                               W, ldw, M, N, chunk, range_stride, w.fine, k, w.slots, w.info,
+                               counts, w.eq, w.gt1, w.totals);
         else
             hipLaunchKernelGGL((prune_sample_kernel<Bits, false>), sgrid, dim3(kHistThreads), 0,
-                               s, W, ldw, M, N, chunk, range_stride, w.fine);
+                               s, W, ldw, M, N, chunk, range_stride, w.fine, k, w.slots, w.info,
+                               counts, w.eq, w.gt1, w.totals);
         if (aligned)
             hipLaunchKernelGGL((prune_split_kernel<Bits, true>), dim3(groups), dim3(kHistThreads),
                                0, s, W, ldw, M, N, per_wave, w.slots, w.info, totals_u, w.fine,
@@ -1189,11 +1218,11 @@ hipError_t launch_prune_t(int64_t M, int64_t N, const void *Wv, int64_t ldw, int
     if (aligned)
         hipLaunchKernelGGL((prune_count_kernel<Bits, true>), dim3(groups), dim3(kHistThreads), 0,
                            s, W, ldw, M, N, per_wave, w.slots, w.info, totals_u, gt_u, eq_u,
-                           w.cand, gt1_u, cap, rd);
+                           w.cand, gt1_u, cap, rd, w.fine);
     else
         hipLaunchKernelGGL((prune_count_kernel<Bits, false>), dim3(groups), dim3(kHistThreads), 0,
                            s, W, ldw, M, N, per_wave, w.slots, w.info, totals_u, gt_u, eq_u,
-                           w.cand, gt1_u, cap, rd);
+                           w.cand, gt1_u, cap, rd, w.fine);
     return hipGetLastError();
 }
 

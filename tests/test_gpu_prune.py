@@ -147,6 +147,26 @@ def test_repeat_calls_reuse_workspace(darb):
         assert np.array_equal(c.cpu().numpy(), oracle.prune_counts(W, k)), k
 
 
+def test_split_with_a_workspace_that_held_other_data(darb):
+    # at the split size the sample's histogram starts as the workspace holds it (the
+    # count pass of a call leaves it at zero): a workspace that held other data
+    # biases the first call's bracket, which may cost passes over W, never the counts
+    rng = np.random.default_rng(21)
+    W = rng.standard_normal((4096, 4096)).astype(np.float32)      # 64 MiB of W
+    Wd = dev(W)
+    nbytes = ctypes.c_int64()
+    assert darb.lib().darb_prune_workspace(4096, 4096, darb.F32, ctypes.byref(nbytes)) == 0
+    ks = (int(0.1 * W.size), 12345)
+    ref = {k: oracle.prune_counts(W, k) for k in ks}
+    for fill in (0xAB, 0x00, 0x3F):
+        ws = torch.full((nbytes.value,), fill, dtype=torch.uint8, device="cuda")
+        for k in ks + ks:                               # each k on a used workspace too
+            say(f"split-size workspace filled with {fill:#x}, k = {k}")
+            c = darb.prune_counts(Wd, k, workspace=ws)
+            torch.cuda.synchronize()
+            assert np.array_equal(c.cpu().numpy(), ref[k]), (fill, k)
+
+
 @pytest.mark.parametrize("name", ["lstm_tiny", "gru_1536"])
 def test_whole_pipeline_on_device(darb, name):
     # W -> device pruning counts -> plan -> encode -> bit-packed offsets -> products,
