@@ -286,7 +286,9 @@ int darb_spmm_i8(const darb_plan *plan, const int8_t *codes, const float *scales
  *              returns (about M*N/4 bytes: room for the keys whose leading digit
  *              lies in a small bracket around the threshold's, which the later
  *              passes read instead of W when W has 64 MiB or more); its contents
- *              on entry do not matter
+ *              on entry do not change the counts (a workspace last used by this
+ *              call runs fastest: it leaves the part the next call's sample adds
+ *              into at zero; other contents may cost that call passes over W)
  * Work is enqueued on `stream` only (several kernels, no host synchronisation);
  * calls sharing a workspace must not overlap.
  * Errors: DARB_E_INVALID, DARB_E_DTYPE, DARB_E_WORKSPACE, DARB_E_HIP.
