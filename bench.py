@@ -67,7 +67,8 @@ def parse_args(argv=None):
 
 
 def step_bytes(M, N, nnz, s_w, s_x, B):
-    """Algorithmic bytes of each kernel (see the measurement notes in the design doc)."""
+    """Algorithmic bytes of each kernel: the format, x or X and y or Y once each (and
+    W once for the encode), the row order and the per-row table."""
     enc = M * N * s_w + nnz * (s_w + 1) + 4 * M
     spmv = nnz * (s_w + 1) + N * s_x + 4 * M + 4 * M
     spmm = nnz * (s_w + 1) + N * B * s_x + 4 * M * B + 4 * M
@@ -361,7 +362,7 @@ def main(argv=None):
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py measures one GPU: the DARB path here runs on a single MI355X and has "
-              "no multi-GPU mode (rows would shard with no communication; see DESIGN.md). "
+              "no multi-GPU mode (rows would shard across GPUs with no communication). "
               "Run with --gpus 1.", file=sys.stderr)
         sys.exit(2)
 
