@@ -457,3 +457,70 @@ def test_spmv_row_blocks_on_resident_workgroups(darb, wdtype):
         y8 = host(plan.spmv_i8(dev(q), dev(s), xd, **kw))
         compare(y8, oracle.spmm_i8(q, s, offs, lay, x), oracle.spmm_i8_absdot(q, s, offs, lay, x),
                 1e-5, f"row blocks spmv INT8 {label}")
+
+
+# --------------------------------------------------------------------------------
+# special values in x / X: a product reads only its row's kept columns, so inf and
+# nan reach exactly the outputs whose kept weights read them (a lane past a row's
+# weights, or a masked column, must add nothing, not 0 * inf)
+# --------------------------------------------------------------------------------
+
+def _with_specials(rng, X):
+    X = X.copy()
+    flat = X.reshape(-1)
+    idx = rng.choice(flat.size, size=max(6, flat.size // 3000), replace=False)
+    flat[idx] = np.array([np.inf, -np.inf, np.nan], dtype=X.dtype)[np.arange(idx.size) % 3]
+    return X
+
+
+def _check_specials(Y, ref, scale, tol, label):
+    Y = np.asarray(Y, dtype=np.float64)
+    assert np.isnan(ref).any() and np.isinf(ref).any(), label
+    assert np.array_equal(np.isnan(Y), np.isnan(ref)), label + ": nan positions differ"
+    inf = np.isinf(ref)
+    assert np.array_equal(np.isinf(Y), inf), label + ": inf positions differ"
+    assert np.array_equal(Y[inf], ref[inf]), label + ": inf signs differ"
+    fin = np.isfinite(ref)
+    compare(Y[fin], ref[fin], scale[fin], tol, label + " (finite outputs)")
+
+
+@pytest.mark.parametrize("path", ["spmv", "spmm64", "spmm_wide", "f16_spmm", "int8"])
+def test_products_special_values_reach_only_their_rows(darb, path):
+    rng = np.random.default_rng({"spmv": 1, "spmm64": 2, "spmm_wide": 3, "f16_spmm": 4,
+                                 "int8": 5}[path])
+    M, N, B = 300, 2048, {"spmv": 1, "spmm64": 64, "spmm_wide": 4100, "f16_spmm": 16,
+                          "int8": 64}[path]
+    if path == "spmm_wide":
+        N = 1024                                    # X slabs staged in LDS
+    wdt = np.float16 if path == "f16_spmm" else np.float32
+    say(f"special values in x/X: {path} ({M}x{N}, B={B})")
+    W = rng.standard_normal((M, N)).astype(wdt)
+    d = rng.integers(0, N // 3, size=M) / N
+    plan, lay, vals, offs = encode_both(darb, W, d, 0.1, 0, 1, 64)
+    X = _with_specials(rng, rng.standard_normal((N, B)).astype(wdt))
+    if B == 1:
+        X = X[:, 0].copy()
+    X0 = np.where(np.isfinite(X), X, 0).astype(X.dtype)
+    vd, od, Xd = dev(vals), dev(offs), dev(X)
+    pk = plan.pack_offsets(od)
+    prod = plan.spmv if B == 1 else plan.spmm
+    prod_pk = plan.spmv_packed if B == 1 else plan.spmm_packed
+    with np.errstate(invalid="ignore", over="ignore"):
+        if path == "int8":
+            q_ref, s_ref = oracle.quantize_i8(vals, lay)
+            q, s = plan.quantize_i8(vd)
+            assert np.array_equal(host(q), q_ref) and np.array_equal(
+                host(s).view(np.uint32), s_ref.view(np.uint32)), "codes or scales differ"
+            ref = oracle.spmm_i8(q_ref, s_ref, offs, lay, X)
+            scale = oracle.spmm_i8_absdot(q_ref, s_ref, offs, lay, X0)
+            outs = [host(plan.spmm_i8(q, s, Xd, offsets=od)),
+                    host(plan.spmm_i8(q, s, Xd, packed=pk))]
+        else:
+            ref = oracle.spmm(vals, offs, lay, X)
+            scale = oracle.spmm_absdot(vals, offs, lay, X0)
+            outs = [host(prod(vd, od, Xd)), host(prod_pk(vd, pk, Xd))]
+    tol = 2e-3 if wdt == np.float16 else 1e-5
+    for o, form in zip(outs, ("byte offsets", "packed offsets")):
+        _check_specials(o, ref, scale, tol, f"{path}, {form}")
+    assert np.array_equal(np.nan_to_num(outs[0]).view(np.uint32),
+                          np.nan_to_num(outs[1]).view(np.uint32)), "forms differ"
