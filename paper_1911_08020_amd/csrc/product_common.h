@@ -220,7 +220,7 @@ template <> struct Off<true, 16> {
 constexpr int kSpmvThreads = 256;
 constexpr int kSpmvWaves = kSpmvThreads / kWave;
 constexpr int kVmax = 8;                         // vectors per lane per round
-constexpr int kLoopVmax = 4;                     // the same for the looping form
+constexpr int kLoopVmax = 4;                     // per round, in the looping general form
 constexpr int kLdsMaxFloats = 16384;             // x staged in LDS up to 64 KiB
 constexpr int64_t kLdsPerCu = 160 * 1024;        // LDS of one gfx950 CU
 
@@ -318,7 +318,8 @@ __global__ __launch_bounds__(kSpmvThreads) void spmv_kernel(
     using OV = Off<PK, VEC>;
     using OS = Off<PK, 1>;
     // vectors per lane and round: the looping form keeps two blocks in registers, so it
-    // holds half as many per block (its launches are scheduled for kLoopVmax)
+    // holds half as many per round (its lanes take further rounds of vectors in the
+    // same order: the lanes per row, and so the sums, are the one-pass form's)
     constexpr int KV = LOOP ? kLoopVmax : kVmax;
     extern __shared__ float xs[];
 
@@ -335,7 +336,7 @@ __global__ __launch_bounds__(kSpmvThreads) void spmv_kernel(
     struct Tile {
         int g, lgL, L, lb, nblk, sub, nvec;
         int64_t j0, e0;
-        bool vec_path, row_ok;
+        bool vec_path, whole, row_ok;
         GroupOffsets go;
         int32_t dest;
         float scale;
@@ -352,6 +353,7 @@ __global__ __launch_bounds__(kSpmvThreads) void spmv_kernel(
         const int64_t rows = pick(bins.rows, T.g);
         const int64_t first_row = pick(bins.first_row, T.g);
         T.vec_path = pick(sch.vec, T.g) == VEC;
+        T.whole = T.nblk % VEC == 0 && pick(bins.first_elem, T.g) % VEC == 0;
         const int64_t tile = int64_t(blk - block_begin_of(sch, T.g)) * kSpmvWaves + wave;
         const int64_t row = (tile << (6 - T.lgL)) + (lane >> T.lgL);
         T.row_ok = row < rows;
@@ -411,6 +413,18 @@ __global__ __launch_bounds__(kSpmvThreads) void spmv_kernel(
                         T.wv[t] = __builtin_nontemporal_load(T.vrow + vc);
                         T.ov[t] = OV::load(T.go, T.j0 + int64_t(vc) * VEC);
                     }
+                }
+            }
+        } else if (T.whole) {
+            // the vector path's order with element loads (a pointer not aligned for
+            // vectors): lane sub takes vectors sub, sub + L, ..., each element in turn
+            const Tw *vr = values + T.e0;
+            for (int vi = T.sub; vi < T.nblk / VEC; vi += T.L) {
+#pragma unroll
+                for (int q = 0; q < VEC; ++q) {
+                    const int k = vi * VEC + q;
+                    const int o = OS::field(OS::bits(OS::load(T.go, T.j0 + k), T.go), 0, T.go);
+                    acc = fmaf(to_f32<Tw>(vr[k]), xat((k << T.lb) + o), acc);
                 }
             }
         } else {
@@ -1205,9 +1219,12 @@ bool spmv_schedule(const darb_plan &p, const void *values, const uint8_t *offset
     int64_t blocks = 0;
     for (int g = 0; g < s.nbins; ++g) {
         const int64_t nblk = p.bins.nblk[g];
-        const bool vec = ptr_ok && nblk % VEC == 0 && p.bins.first_elem[g] % VEC == 0;
-        s.vec[g] = vec ? VEC : 1;
-        const int64_t nvec = vec ? nblk / VEC : nblk;
+        // rows of whole vectors split into vectors whatever the pointers' alignment
+        // (which only chooses vector or element loads), so every path sums a row in
+        // the same order and gives the same bits
+        const bool whole = nblk % VEC == 0 && p.bins.first_elem[g] % VEC == 0;
+        s.vec[g] = ptr_ok && whole ? VEC : 1;
+        const int64_t nvec = whole ? nblk / VEC : nblk;
         int lgL = 0;     // fewest lanes per row that keep each lane within vmax vectors
         while (lgL < 6 && ((nvec + (int64_t(1) << lgL) - 1) >> lgL) > vmax) ++lgL;
         s.log2_lanes[g] = lgL;
@@ -1343,9 +1360,7 @@ hipError_t launch_spmv_t(const darb_plan &p, const void *values, const uint8_t *
     per_cu = per_cu < 1 ? 1 : (per_cu > 8 ? 8 : per_cu);
     const int64_t resident = int64_t(p.cus > 0 ? p.cus : 256) * per_cu;
 
-    // more blocks than fit at once: the looping form, scheduled for its registers
-    if (blocks > resident && !spmv_schedule<Tw>(p, values, offsets, s, kLoopVmax))
-        return hipErrorInvalidConfiguration;
+    // more blocks than fit at once: the looping form (same schedule, so the same sums)
     const int blocks_l = s.block_begin[s.nbins];
     const int grid = int(blocks_l < resident ? blocks_l : resident);
     if (p.N <= kLdsMaxFloats) {

@@ -147,6 +147,51 @@ def test_packed_misaligned_values_scalar_paths(darb):
                   "misaligned spmm packed")
 
 
+def _shifted(a: np.ndarray, shift: int):
+    """A device copy of `a` starting `shift` elements into its buffer (misaligned)."""
+    t = torch.zeros(a.size + shift, dtype=dev(a[:1]).dtype, device="cuda")
+    t[shift:].copy_(dev(a))
+    return t[shift:]
+
+
+@pytest.mark.parametrize("case", [(300, 2048, "f32"), (300, 2048, "f16"), (77, 1000, "f32"),
+                                  (20000, 2048, "f32"), (300, 2048, "i8")])
+def test_spmv_bits_depend_on_the_plan_only(darb, case):
+    # a row's lanes and their order follow the plan alone: values, offsets and x
+    # aligned or not (vector or element loads, the row-block or the general kernel),
+    # byte or packed offsets, one-pass or looping launches (20000 rows) -- same bits
+    M, N, kind = case
+    say(f"spmv bits across forms and alignments: {M}x{N} {kind}")
+    rng = np.random.default_rng(M + N)
+    W = rng.standard_normal((M, N)).astype(np.float16 if kind == "f16" else np.float32)
+    d = rng.integers(0, N // 3, size=M) / N
+    plan, lay, vals, offs = setup(darb, W, d, 0.1, 2, 128)
+    packed = plan.pack_offsets(dev(offs))
+    x = rng.standard_normal(N).astype(np.float32)
+    xs = [dev(x), _shifted(x, 1)]
+    if kind == "i8":
+        q, s = oracle.quantize_i8(vals, lay)
+        ws = [dev(q), _shifted(q, 1)]
+        run = lambda w, o, p, xx: plan.spmv_i8(w, dev(s), xx, offsets=o, packed=p)
+        ref = oracle.spmm_i8(q, s, offs, lay, x)
+        scale = oracle.spmm_i8_absdot(q, s, offs, lay, x)
+    else:
+        ws = [dev(vals), _shifted(vals, 1)]
+        run = lambda w, o, p, xx: plan.spmv(w, o, xx) if p is None else plan.spmv_packed(w, p, xx)
+        ref = oracle.spmm(vals, offs, lay, x)
+        scale = oracle.spmm_absdot(vals, offs, lay, x)
+    outs = {}
+    for wi, w in enumerate(ws):
+        for xi, xx in enumerate(xs):
+            outs[("bytes", wi, xi)] = host(run(w, dev(offs), None, xx))
+            outs[("bytes, offsets shifted", wi, xi)] = host(run(w, _shifted(offs, 1), None, xx))
+            outs[("packed", wi, xi)] = host(run(w, None, packed, xx))
+    first = outs[("bytes", 0, 0)]
+    compare(first, ref, scale, 2e-3 if kind == "f16" else 1e-5, f"{case}")
+    for key, y in outs.items():
+        assert np.array_equal(y.view(np.uint32), first.view(np.uint32)), key
+
+
 def test_packed_all_b_one_has_no_words(darb):
     # b = 1 everywhere: every index is 0, the packed form is empty and the C ABI
     # accepts a NULL packed pointer
