@@ -1053,7 +1053,8 @@ constexpr int kXldsFloats = 32768;                  // 128 KiB of LDS
 constexpr int kXldsStep = 16;                       // weights per row per step
 constexpr int kXldsBatch = 16;                      // LDS gathers in flight per lane
 
-// 16 consecutive retained values of one row, loaded as 16-byte vectors.
+// 16 consecutive retained values of one row, loaded as 16-byte vectors (load) or
+// element by element from any alignment (load_elem), to the same registers.
 template <typename Tw> struct Step16;
 template <> struct Step16<float> {
     f32x4 v[4];
@@ -1061,6 +1062,12 @@ template <> struct Step16<float> {
         Step16 s;
 #pragma unroll
         for (int i = 0; i < 4; ++i) s.v[i] = reinterpret_cast<const f32x4 *>(p)[i];
+        return s;
+    }
+    __device__ static Step16 load_elem(const float *p) {
+        Step16 s;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) s.v[i >> 2][i & 3] = p[i];
         return s;
     }
     __device__ float get(int i) const { return v[i >> 2][i & 3]; }
@@ -1073,17 +1080,28 @@ template <> struct Step16<__half> {
         for (int i = 0; i < 2; ++i) s.v[i] = reinterpret_cast<const u32x4 *>(p)[i];
         return s;
     }
+    __device__ static Step16 load_elem(const __half *p) {
+        const uint16_t *h = reinterpret_cast<const uint16_t *>(p);
+        Step16 s;
+#pragma unroll
+        for (int i = 0; i < 8; ++i)
+            s.v[i >> 2][i & 3] = uint32_t(h[2 * i]) | (uint32_t(h[2 * i + 1]) << 16);
+        return s;
+    }
     __device__ float get(int i) const {
         const uint32_t w = v[i >> 3][(i >> 1) & 3];
         return half_bits_to_f32((i & 1) ? (w >> 16) : w);
     }
 };
 
-template <typename Tw, int LGL, bool PK>
+// ELEM: values or byte offsets not 16-byte aligned, loaded element by element (the
+// same registers, so the same sums); xvec: X's rows 16-byte aligned and B a multiple
+// of 4 (staged as 16-byte vectors, otherwise element by element).
+template <typename Tw, int LGL, bool PK, bool ELEM>
 __global__ __launch_bounds__(kXldsThreads) void spmm_xlds_kernel(
     const Tw *__restrict__ values, const void *__restrict__ offs,
     const float *__restrict__ X, int64_t ldx, int64_t B, float *__restrict__ Y, int64_t ldy,
-    const int32_t *__restrict__ perm, int N, BinTable bins, ProductSchedule sch) {
+    const int32_t *__restrict__ perm, int N, BinTable bins, ProductSchedule sch, bool xvec) {
     constexpr int L = 1 << LGL;
     constexpr int R = kWave >> LGL;
     constexpr int SC = 4 * L;                           // slab columns
@@ -1093,8 +1111,8 @@ __global__ __launch_bounds__(kXldsThreads) void spmm_xlds_kernel(
     using OV = Off<PK, kXldsStep>;                      // a step's 16 offsets
 
     const int64_t colbase = int64_t(blockIdx.x) * SC;
-    // X[:, slab] -> xs[c * SC + j]; columns past B read as zero (4 divides B)
-    {
+    // X[:, slab] -> xs[c * SC + j]; columns past B read as zero
+    if (xvec) {                                         // uniform: 4 divides B
         constexpr int per_row = SC / 4;
         const int items = N * per_row;
         for (int base = 0; base < items; base += kStage * kXldsThreads) {
@@ -1118,8 +1136,34 @@ __global__ __launch_bounds__(kXldsThreads) void spmm_xlds_kernel(
                 }
             }
         }
+    } else {
+        for (int i = int(threadIdx.x); i < N * SC; i += kXldsThreads) {
+            const int c = i / SC, j = i - c * SC;
+            const int64_t col = colbase + j;
+            xs[i] = col < B ? X[int64_t(c) * ldx + col] : 0.0f;
+        }
     }
     __syncthreads();
+    // a step's 16 values and 16 offsets, as vectors or element by element
+    auto load_w = [&](int64_t e) {
+        if constexpr (ELEM) return Step16<Tw>::load_elem(values + e);
+        else return Step16<Tw>::load(values + e);
+    };
+    auto load_o = [&](const GroupOffsets &go, int64_t j) {
+        if constexpr (ELEM && !PK) {                    // 16 offset bytes, one at a time
+            typename OV::Raw r;
+#pragma unroll
+            for (int wd = 0; wd < 4; ++wd) {
+                uint32_t v = 0;
+#pragma unroll
+                for (int b = 0; b < 4; ++b) v |= uint32_t(go.u8[j + 4 * wd + b]) << (8 * b);
+                r[wd] = v;
+            }
+            return r;
+        } else {
+            return OV::load(go, j);                     // packed words need no alignment
+        }
+    };
 
     const int wave = wave_uniform(int(threadIdx.x) / kWave);
     const int lane = int(threadIdx.x) & (kWave - 1);
@@ -1143,12 +1187,12 @@ __global__ __launch_bounds__(kXldsThreads) void spmm_xlds_kernel(
             // every lane of the row loads the step's 16 (value, offset) pairs itself
             // (equal addresses within one load merge), so no lane exchange is needed;
             // the next step's pairs load while this step gathers
-            Step16<Tw> w = Step16<Tw>::load(values + e0);
-            typename OV::Raw ob = OV::load(go, j0);
+            Step16<Tw> w = load_w(e0);
+            typename OV::Raw ob = load_o(go, j0);
             for (int k0 = 0; k0 < nblk; k0 += kXldsStep) {
                 const int kn = k0 + kXldsStep < nblk ? k0 + kXldsStep : k0;
-                const Step16<Tw> w_next = Step16<Tw>::load(values + e0 + kn);
-                const typename OV::Raw ob_next = OV::load(go, j0 + kn);
+                const Step16<Tw> w_next = load_w(e0 + kn);
+                const typename OV::Raw ob_next = load_o(go, j0 + kn);
                 const typename OV::Bits obits = OV::bits(ob, go);
                 static_for<0, kXldsStep / kXldsBatch>([&](auto bc) {
                     constexpr int b0 = decltype(bc)::value * kXldsBatch;
@@ -1173,7 +1217,8 @@ __global__ __launch_bounds__(kXldsThreads) void spmm_xlds_kernel(
             if (row_ok && col_ok) {
                 float *yrow = Y + int64_t(perm[first_row + rl]) * ldy + col0;
 #pragma unroll
-                for (int q = 0; q < 4; ++q) yrow[q] = acc[q];
+                for (int q = 0; q < 4; ++q)
+                    if (col0 + q < B) yrow[q] = acc[q];
             }
         }
     }
@@ -1474,8 +1519,8 @@ hipError_t launch_spmm_cpl(const darb_plan &p, const ProductSchedule &s, const T
 }
 
 // Lanes per row of the LDS-slab SpMM (slab = 4 * lanes columns), or -1 when it does
-// not apply: fp32 X with 16-byte rows, a slab of >= 32 columns whose N rows fit in
-// LDS, and enough slabs (>= 128) to give every CU a workgroup.
+// not apply: fp32 X, a slab of >= 32 columns whose N rows fit in LDS, and enough
+// slabs (>= 128) to give every CU a workgroup.
 inline int xlds_lgl(const darb_plan &p, int64_t B) {
     for (int lgl = 4; lgl >= 3; --lgl) {
         const int64_t sc = int64_t(4) << lgl;
@@ -1490,16 +1535,14 @@ hipError_t launch_spmm_t(const darb_plan &p, const void *values, const uint8_t *
                          int64_t ldy, const float *scales, hipStream_t st) {
     constexpr int CPL = 16 / int(sizeof(Tx));
     if constexpr (std::is_same<Tx, float>::value && !kScaled<Tw>) {
-        const bool vec = (reinterpret_cast<uintptr_t>(X) % 16 == 0) &&
-                         ((ldx * int64_t(sizeof(Tx))) % 16 == 0) && (B % CPL == 0);
-        int lgl = vec ? xlds_lgl(p, B) : -1;
-        // every row's steps of 16 pairs load as 16-byte vectors
-        bool aligned16 = reinterpret_cast<uintptr_t>(values) % (kXldsStep * sizeof(Tw)) == 0 &&
-                         offsets_aligned(offsets, kXldsStep);
+        // the LDS-slab kernel is chosen from the plan and B alone (rows in whole steps
+        // of 16 weights, slabs that fit, enough of them), so every alignment of the
+        // pointers and both offset forms take it and give the same bits; alignment
+        // only chooses vector or element loads
+        int lgl = xlds_lgl(p, B);
         for (int g = 0; g < p.bins.nbins; ++g)
-            aligned16 = aligned16 && p.bins.nblk[g] % kXldsStep == 0 &&
-                        p.bins.first_elem[g] % kXldsStep == 0;
-        if (!aligned16) lgl = -1;
+            if (p.bins.nblk[g] % kXldsStep != 0 || p.bins.first_elem[g] % kXldsStep != 0)
+                lgl = -1;
         if (lgl >= 0) {
             ProductSchedule s;
             if (!spmm_schedule(p, B, CPL, sizeof(Tw), values, offsets, s))
@@ -1509,14 +1552,22 @@ hipError_t launch_spmm_t(const darb_plan &p, const void *values, const uint8_t *
             const Tw *v = static_cast<const Tw *>(values);
             const float *x = static_cast<const float *>(X);
             const void *offs = offset_source(p, offsets, packed);
-            if (lgl == 4)
-                hipLaunchKernelGGL((spmm_xlds_kernel<Tw, 4, PK>), dim3(unsigned(slabs)),
-                                   dim3(kXldsThreads), 0, st, v, offs, x, ldx, B, Y, ldy,
-                                   p.d_perm, int(p.N), p.bins, s);
-            else
-                hipLaunchKernelGGL((spmm_xlds_kernel<Tw, 3, PK>), dim3(unsigned(slabs)),
-                                   dim3(kXldsThreads), 0, st, v, offs, x, ldx, B, Y, ldy,
-                                   p.d_perm, int(p.N), p.bins, s);
+            const bool elem = reinterpret_cast<uintptr_t>(values) % 16 != 0 ||
+                              !offsets_aligned(offsets, kXldsStep);
+            const bool xvec = reinterpret_cast<uintptr_t>(X) % 16 == 0 && ldx % 4 == 0 &&
+                              B % 4 == 0;
+#define DARB_XLDS(LG, E)                                                                    \
+    hipLaunchKernelGGL((spmm_xlds_kernel<Tw, LG, PK, E>), dim3(unsigned(slabs)),           \
+                       dim3(kXldsThreads), 0, st, v, offs, x, ldx, B, Y, ldy, p.d_perm,      \
+                       int(p.N), p.bins, s, xvec)
+            if (lgl == 4) {
+                if (elem) DARB_XLDS(4, true);
+                else DARB_XLDS(4, false);
+            } else {
+                if (elem) DARB_XLDS(3, true);
+                else DARB_XLDS(3, false);
+            }
+#undef DARB_XLDS
             return hipGetLastError();
         }
     }

@@ -192,6 +192,39 @@ def test_spmv_bits_depend_on_the_plan_only(darb, case):
         assert np.array_equal(y.view(np.uint32), first.view(np.uint32)), key
 
 
+@pytest.mark.parametrize("case", [(4100, "f32"), (4098, "f32"), (4100, "f16")])
+def test_wide_spmm_bits_depend_on_the_plan_only(darb, case):
+    # the LDS-slab SpMM (N = 1024, B >= 4096) is chosen from the plan and B alone:
+    # values and byte offsets aligned or not (vector or element loads), packed
+    # offsets, X rows padded to any width (staged as vectors or element by element),
+    # B not a multiple of 4 -- same bits
+    B, kind = case
+    M, N = 200, 1024
+    say(f"wide spmm bits across forms and alignments: B={B} {kind}")
+    rng = np.random.default_rng(B)
+    W = rng.standard_normal((M, N)).astype(np.float16 if kind == "f16" else np.float32)
+    d = rng.integers(0, N // 3, size=M) / N
+    plan, lay, vals, offs = setup(darb, W, d, 0.1, 1, 64)
+    packed = plan.pack_offsets(dev(offs))
+    X = rng.standard_normal((N, B)).astype(np.float32)
+    first = None
+    for pad in (0, 4, 2, 1):
+        Xbig = np.zeros((N, B + pad), dtype=np.float32)
+        Xbig[:, :B] = X
+        Xd = dev(Xbig)[:, :B]
+        for w in (dev(vals), _shifted(vals, 1)):
+            for label, Y in (("bytes", lambda: plan.spmm(w, dev(offs), Xd)),
+                             ("bytes, offsets shifted", lambda: plan.spmm(w, _shifted(offs, 1), Xd)),
+                             ("packed", lambda: plan.spmm_packed(w, packed, Xd))):
+                y = host(Y())
+                if first is None:
+                    first = y
+                    compare(y, oracle.spmm(vals, offs, lay, X),
+                            oracle.spmm_absdot(vals, offs, lay, X),
+                            2e-3 if kind == "f16" else 1e-5, f"wide B={B} {kind}")
+                assert np.array_equal(y.view(np.uint32), first.view(np.uint32)), (pad, label)
+
+
 def test_packed_all_b_one_has_no_words(darb):
     # b = 1 everywhere: every index is 0, the packed form is empty and the C ABI
     # accepts a NULL packed pointer
