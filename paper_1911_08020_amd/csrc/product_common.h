@@ -1216,9 +1216,14 @@ __global__ __launch_bounds__(kXldsThreads) void spmm_xlds_kernel(
             }
             if (row_ok && col_ok) {
                 float *yrow = Y + int64_t(perm[first_row + rl]) * ldy + col0;
+                if (col0 + 3 < B) {                      // a whole quad: one 16-byte store
+                    typedef float f32x4_u __attribute__((ext_vector_type(4), aligned(4)));
+                    *reinterpret_cast<f32x4_u *>(yrow) = f32x4_u{acc[0], acc[1], acc[2], acc[3]};
+                } else {
 #pragma unroll
-                for (int q = 0; q < 4; ++q)
-                    if (col0 + q < B) yrow[q] = acc[q];
+                    for (int q = 0; q < 4; ++q)
+                        if (col0 + q < B) yrow[q] = acc[q];
+                }
             }
         }
     }
