@@ -192,6 +192,46 @@ def test_spmv_bits_depend_on_the_plan_only(darb, case):
         assert np.array_equal(y.view(np.uint32), first.view(np.uint32)), key
 
 
+@pytest.mark.parametrize("B", [3, 16, 64])
+@pytest.mark.parametrize("kind", ["f32", "f16", "i8"])
+def test_spmm_bits_depend_on_the_plan_only(darb, B, kind):
+    # the L2-gather SpMM: values and byte offsets aligned or not (vector or element
+    # pair loads), packed offsets, X rows padded to any width -- same bits
+    M, N = 300, 2048
+    say(f"spmm bits across forms and alignments: B={B} {kind}")
+    rng = np.random.default_rng(7 * B)
+    W = rng.standard_normal((M, N)).astype(np.float16 if kind == "f16" else np.float32)
+    d = rng.integers(0, N // 3, size=M) / N
+    plan, lay, vals, offs = setup(darb, W, d, 0.1, 2, 128)
+    packed = plan.pack_offsets(dev(offs))
+    X = rng.standard_normal((N, B)).astype(np.float32)
+    if kind == "i8":
+        q, sc = oracle.quantize_i8(vals, lay)
+        ws, scd = (dev(q), _shifted(q, 1)), dev(sc)
+        run = lambda w, o, p, Xd: plan.spmm_i8(w, scd, Xd, offsets=o, packed=p)
+        ref = oracle.spmm_i8(q, sc, offs, lay, X)
+        scale = oracle.spmm_i8_absdot(q, sc, offs, lay, X)
+    else:
+        ws = (dev(vals), _shifted(vals, 1))
+        run = lambda w, o, p, Xd: (plan.spmm(w, o, Xd) if p is None
+                                   else plan.spmm_packed(w, p, Xd))
+        ref = oracle.spmm(vals, offs, lay, X)
+        scale = oracle.spmm_absdot(vals, offs, lay, X)
+    first = None
+    for pad in (0, 1):
+        Xbig = np.zeros((N, B + pad), dtype=np.float32)
+        Xbig[:, :B] = X
+        Xd = dev(Xbig)[:, :B]
+        for w in ws:
+            for label, o, p in (("bytes", dev(offs), None), ("bytes, offsets shifted",
+                                 _shifted(offs, 1), None), ("packed", None, packed)):
+                y = host(run(w, o, p, Xd))
+                if first is None:
+                    first = y
+                    compare(y, ref, scale, 2e-3 if kind == "f16" else 1e-5, f"B={B} {kind}")
+                assert np.array_equal(y.view(np.uint32), first.view(np.uint32)), (pad, label)
+
+
 @pytest.mark.parametrize("case", [(4100, "f32"), (4098, "f32"), (4100, "f16")])
 def test_wide_spmm_bits_depend_on_the_plan_only(darb, case):
     # the LDS-slab SpMM (N = 1024, B >= 4096) is chosen from the plan and B alone:
